@@ -1,0 +1,189 @@
+/*
+ * spz.h -- C ABI of the large-batch actor-critic update on one MI355X (gfx950).
+ *
+ * The library implements the network-update process of Spreeze (Section 3.2:
+ * one updater drawing large uniform batches from a shared replay pool and
+ * training the actor and the double-Q critics with target networks; Section
+ * 3.2.2: actor and critic updated independently, here as two concurrent HIP
+ * streams on one GPU). SAC is the paper's worked example; TD3 is the
+ * alternative algorithm of Section 4.3 / Fig. 8. One update step:
+ *   1. Philox-sampled replay indices and a row gather from the HBM ring buffer;
+ *   2. critic stream: target action (actor + tanh-Gaussian head, or TD3 target
+ *      actor + smoothing), target critics, TD target, online critics, critic
+ *      loss, critic backward;
+ *   3. actor stream: actor forward on s, critics at their step-start parameters
+ *      on (s, a~), actor loss, backward to the actor, temperature gradient;
+ *   4. one fused Adam + Polyak pass over all parameters.
+ *
+ * Conventions
+ *   - Every call returns SPZ_OK (0) or a negative SPZ_E* code; no C++ exception
+ *     crosses the ABI. spz_create returns NULL on failure. The message of the
+ *     last failure on the calling thread is spz_last_error(NULL); per-context
+ *     messages are spz_last_error(ctx).
+ *   - Pointers are HOST pointers unless stated. The caller keeps ownership of
+ *     every array it passes; the library copies what it needs before returning.
+ *   - A context is not thread-safe; distinct contexts are independent.
+ *   - Flat parameter layout of one network (spz_read_params / spz_write_params):
+ *     layer by layer, W as [out, in] row-major float32, then b [out].
+ *     Actor (SAC): obs -> hidden... -> 2*act (mean | log-std); actor (TD3):
+ *     obs -> hidden... -> act; critic: (obs | act) -> hidden... -> 1.
+ */
+#ifndef SPZ_H
+#define SPZ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct spz_ctx spz_ctx;
+
+/* Return codes. */
+#define SPZ_OK 0
+#define SPZ_EINVAL (-1) /* bad argument (dimension, pointer, hyper-parameter, selector) */
+#define SPZ_ENOMEM (-2) /* device or host allocation failed                             */
+#define SPZ_EEMPTY (-3) /* spz_update on an empty replay buffer                          */
+#define SPZ_ESIZE (-4)  /* caller's array length does not match the requested object     */
+#define SPZ_EHIP (-5)   /* a HIP runtime call failed (message has the HIP error string)  */
+
+/* Algorithms and GEMM operand precisions. */
+#define SPZ_ALGO_SAC 0
+#define SPZ_ALGO_TD3 1
+#define SPZ_PREC_FP32 0 /* float32 operands, float32 accumulate                        */
+#define SPZ_PREC_BF16 1 /* bfloat16 operands (RNE), float32 accumulate, fp32 master    */
+
+/* Selectors for spz_param_count / spz_read_params / spz_write_params. */
+#define SPZ_ACTOR 0
+#define SPZ_CRITIC1 1
+#define SPZ_CRITIC2 2
+#define SPZ_TCRITIC1 3
+#define SPZ_TCRITIC2 4
+#define SPZ_TACTOR 5 /* TD3 only */
+#define SPZ_LOG_ALPHA 6
+#define SPZ_M_ACTOR 7 /* Adam first moments */
+#define SPZ_M_CRITIC1 8
+#define SPZ_M_CRITIC2 9
+#define SPZ_M_LOG_ALPHA 10
+#define SPZ_V_ACTOR 11 /* Adam second moments */
+#define SPZ_V_CRITIC1 12
+#define SPZ_V_CRITIC2 13
+#define SPZ_V_LOG_ALPHA 14
+#define SPZ_G_ACTOR 15 /* gradients of the last completed step (read only) */
+#define SPZ_G_CRITIC1 16
+#define SPZ_G_CRITIC2 17
+#define SPZ_G_LOG_ALPHA 18
+#define SPZ_N_SELECTORS 19
+
+/* Selectors for spz_debug_read. */
+#define SPZ_DBG_INDICES 0 /* int32 [batch]: replay rows sampled by the last step */
+
+/* Loss record of one step: 8 floats. */
+#define SPZ_REC_LQ 0        /* mean (q1-y)^2 + mean (q2-y)^2                      */
+#define SPZ_REC_LPI 1       /* actor loss (0 on TD3 steps without an actor update) */
+#define SPZ_REC_LALPHA 2    /* -log(alpha) * mean(log pi + target entropy)         */
+#define SPZ_REC_ALPHA 3     /* alpha used by the step                              */
+#define SPZ_REC_LOGPI 4     /* mean log pi of the actor sample                     */
+#define SPZ_REC_Q1 5        /* mean q1(s, a)                                       */
+#define SPZ_REC_NONFINITE 6 /* 1 if any of the values above is not finite          */
+#define SPZ_REC_ACTOR 7     /* 1 if the actor was updated in this step             */
+#define SPZ_REC_WIDTH 8
+
+/* Hyper-parameters. Fill with spz_hparams_default, then override. */
+typedef struct spz_hparams {
+  int32_t algo;      /* SPZ_ALGO_SAC | SPZ_ALGO_TD3                                */
+  int32_t gemm_prec; /* SPZ_PREC_FP32 | SPZ_PREC_BF16                              */
+  int64_t capacity;  /* replay ring rows (> 0)                                     */
+  float gamma;       /* discount                                                   */
+  float tau;         /* Polyak rate: tbar <- (1-tau) tbar + tau theta, in [0, 1]    */
+  float lr_actor, lr_critic, lr_alpha;
+  float beta1, beta2, eps; /* Adam                                                 */
+  float alpha_init;        /* SAC temperature at step 0 (> 0)                      */
+  int32_t learn_alpha;     /* SAC: 1 learns log(alpha) against target_entropy      */
+  float target_entropy;
+  float log_std_min, log_std_max; /* SAC log-std clamp                             */
+  float policy_noise, noise_clip; /* TD3 target policy smoothing                   */
+  int32_t policy_delay;           /* TD3: actor and targets every policy_delay steps */
+  int32_t device;                 /* HIP device ordinal                            */
+  int32_t n_streams;              /* 2: actor and critic on concurrent streams; 1: one stream */
+} spz_hparams;
+
+/* Defaults: SAC, fp32, capacity 1e6, gamma 0.99, tau 0.005, lr 3e-4, Adam
+ * (0.9, 0.999, 1e-8), alpha_init 1, learned alpha, target_entropy 0, log-std
+ * clamp [-20, 2], TD3 noise 0.2 clipped to 0.5, delay 2, device 0, 2 streams. */
+void spz_hparams_default(spz_hparams* hp);
+
+/* Create a learner. obs_dim, act_dim >= 1; hidden[0..n_hidden) >= 1 with
+ * 1 <= n_hidden <= 6; batch >= 1. Parameters are initialised on the host from
+ * `seed` with the fan-in uniform rule U(-1/sqrt(fan_in), 1/sqrt(fan_in)) drawn
+ * from Philox4x32-10 (counter = (i>>2, 0, 0, net*16 + layer*2 + {W:0,b:1}),
+ * word i&3); targets start as exact copies; log(alpha) = ln(alpha_init).
+ * `hidden` and `hp` are copied. NULL on failure (see spz_last_error(NULL)). */
+spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int32_t n_hidden,
+                    int32_t batch, const spz_hparams* hp, uint64_t seed);
+
+/* Release every device and host resource of ctx (NULL is ignored). Waits for
+ * the context's outstanding work first. */
+void spz_destroy(spz_ctx* ctx);
+
+/* Append n transitions to the replay ring (Section 3.3.2's shared experience
+ * pool). Host float32 arrays, row-major: obs [n, obs_dim], act [n, act_dim],
+ * rew [n], done [n] (0 or 1), next_obs [n, obs_dim]. Row i goes to slot
+ * (ptr + i) mod capacity; size = min(size + n, capacity). bf16 contexts store
+ * obs, act and next_obs rounded to bfloat16 (RNE). Synchronous: the arrays may
+ * be freed when the call returns. Errors: SPZ_EINVAL (n < 0, or a NULL array
+ * with n > 0), SPZ_EHIP. */
+int spz_buffer_push(spz_ctx* ctx, const float* obs, const float* act, const float* rew,
+                    const float* done, const float* next_obs, int64_t n);
+
+/* Rows currently held by the ring (0 .. capacity). */
+int64_t spz_buffer_size(const spz_ctx* ctx);
+
+/* Enqueue n_steps update steps on `hip_stream` (a hipStream_t; NULL = the null
+ * stream) and return without waiting. Step t (1-based, counted across calls)
+ * samples idx[b] = mulhi32(Philox(seed; b>>2, t, 1, 0)[b&3], size) with
+ * replacement, draws its normal deviates from purposes 2 (target) and 3
+ * (policy), and ends with the Adam/Polyak pass. Non-finite values do not make
+ * the call fail; they set SPZ_REC_NONFINITE in the step's loss record.
+ * Errors: SPZ_EEMPTY (no rows), SPZ_EINVAL (n_steps < 0), SPZ_EHIP. */
+int spz_update(spz_ctx* ctx, int32_t n_steps, void* hip_stream);
+
+/* Wait for all work the context enqueued. */
+int spz_synchronize(spz_ctx* ctx);
+
+/* Number of update steps enqueued so far (the step counter t of the last step). */
+int64_t spz_step(const spz_ctx* ctx);
+
+/* Set the step counter (checkpoint resume, teacher forcing). Waits first. */
+int spz_set_step(spz_ctx* ctx, int64_t step);
+
+/* Float count of the object `which` in the flat layout (negative code on error). */
+int64_t spz_param_count(const spz_ctx* ctx, int32_t which);
+
+/* Copy object `which` to the host array out[0..n_floats). Waits for the
+ * context's work first. SPZ_ESIZE if n_floats != spz_param_count(ctx, which);
+ * SPZ_EINVAL for a selector the algorithm does not have. */
+int spz_read_params(spz_ctx* ctx, int32_t which, float* out, int64_t n_floats);
+
+/* Overwrite object `which` from the host array in[0..n_floats) (checkpoint
+ * resume, teacher forcing). Gradient selectors are read only (SPZ_EINVAL). */
+int spz_write_params(spz_ctx* ctx, int32_t which, const float* in, int64_t n_floats);
+
+/* Copy the loss records of steps first_step .. first_step+n-1 (1-based) into
+ * out[n * SPZ_REC_WIDTH]. The library keeps the last 65536 records; older or
+ * not yet enqueued steps give SPZ_EINVAL. Waits first. */
+int spz_read_losses(spz_ctx* ctx, float* out, int64_t first_step, int32_t n);
+
+/* Debug copies of internal state of the last step (see SPZ_DBG_*). `bytes`
+ * must equal the object's size (SPZ_ESIZE otherwise). Waits first. */
+int spz_debug_read(spz_ctx* ctx, int32_t what, void* out, int64_t bytes);
+
+/* Message of the last failure: of ctx, or of the calling thread when ctx is
+ * NULL. Never NULL; empty when there was none. Valid until the next call. */
+const char* spz_last_error(const spz_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPZ_H */

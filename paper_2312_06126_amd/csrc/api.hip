@@ -1,0 +1,867 @@
+// C ABI and step orchestration of the actor-critic update.
+//
+// Memory layout in HBM (per context):
+//   parameter arenas P (online), T (targets), G (gradients), M, V (Adam), all
+//     float32 with one common layout: actor | critic1 | critic2 | log(alpha);
+//     each layer stores W [out_p, in_p] then b [out_p], 256-byte aligned, with
+//     feature dimensions padded to multiples of 32 and zero padding. For bf16
+//     contexts Pb / Tb hold the bfloat16 images of P / T used as GEMM operands.
+//   replay ring: capacity rows of [obs | act | next_obs | pad | rew | done],
+//     obs/act/next_obs in the operand type, rew/done float32, 16-byte rows.
+//   batch operands [Bp, Kc] (Bp = batch rounded up to 256): critic input
+//     [obs | 0 | act | 0] with the action block at column Ka = pad32(obs_dim);
+//     the actor reads the first Ka columns of the same tensors.
+//   per-stream workspaces for activations, gradients and reduction partials.
+//
+// One update step (snapshot semantics: every read of step t sees the parameters
+// of the start of step t; all parameter writes happen in the final Adam/Polyak
+// pass after the two streams join):
+//   s0: gather                          -> fork
+//   critic stream: target action, target critics, TD target, online critics,
+//                  critic loss, critic backward (weight and bias gradients)
+//   actor stream:  actor forward on s, critics on (s, a~), actor loss, critic
+//                  input-gradient to the action, head backward, actor backward
+//   s0: join -> finish (loss record, temperature gradient, step counter) -> Adam + Polyak
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "kernels.h"
+
+using namespace spz;
+
+namespace {
+
+thread_local std::string tl_err;
+
+struct Lay {
+  int in_f, out_f, in_p, out_p;
+  int64_t w, b;  // float offsets into an arena
+};
+
+struct Net {
+  std::vector<Lay> L;
+  int64_t off = 0, end = 0;
+};
+
+inline int pad32(int x) { return (x + 31) / 32 * 32; }
+inline int64_t align64(int64_t x) { return (x + 63) / 64 * 64; }
+inline int64_t align16(int64_t x) { return (x + 15) / 16 * 16; }
+
+}  // namespace
+
+struct spz_ctx {
+  // configuration
+  int O = 0, A = 0, B = 0, Bp = 0, Ka = 0, Ap = 0, Kc = 0;
+  std::vector<int> hidden;
+  spz_hparams hp{};
+  uint64_t seed = 0;
+  bool bf16 = false, td3 = false;
+  Net net[3];
+  int64_t la = 0, n_arena = 0;
+  int hmax = 0;
+  // parameters
+  float *P = nullptr, *G = nullptr, *M = nullptr, *V = nullptr, *T = nullptr;
+  bf16_t *Pb = nullptr, *Tb = nullptr;
+  // replay ring
+  uint8_t* buf = nullptr;
+  int64_t row_bytes = 0, cap = 0, ptr = 0, size = 0;
+  int off_a = 0, off_s2 = 0, off_r = 0, off_d = 0;
+  float* stage = nullptr;
+  int64_t stage_rows = 0;
+  // step state
+  int64_t* d_step = nullptr;
+  int64_t h_step = 0;
+  float* rec = nullptr;
+  int64_t rec_cap = 65536;
+  // batch
+  void *xsa = nullptr, *xs2 = nullptr, *xsp = nullptr;
+  float *r = nullptr, *d = nullptr;
+  int32_t* idx = nullptr;
+  // critic-stream workspace
+  void* cs_h[2] = {nullptr, nullptr};
+  float *z2 = nullptr, *logp2 = nullptr, *qt1 = nullptr, *qt2 = nullptr, *y = nullptr;
+  float *q1 = nullptr, *q2 = nullptr, *dq1 = nullptr, *dq2 = nullptr;
+  std::vector<void*> hc[2];
+  void* c_dz[2] = {nullptr, nullptr};
+  float *c_wpart = nullptr, *c_cpart = nullptr;
+  double* c_lpart = nullptr;
+  // actor-stream workspace
+  std::vector<void*> ha;
+  float *z = nullptr, *th = nullptr, *se = nullptr, *lm = nullptr, *logp = nullptr;
+  float *qp1 = nullptr, *qp2 = nullptr, *dqp1 = nullptr, *dqp2 = nullptr, *da1 = nullptr, *da2 = nullptr;
+  std::vector<void*> hpc[2];
+  void* a_dz[2] = {nullptr, nullptr};
+  void* dzh = nullptr;
+  float *a_wpart = nullptr, *a_cpart = nullptr;
+  double* a_lpart = nullptr;
+  // streams
+  hipStream_t sc = nullptr, sa = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_c = nullptr, ev_a = nullptr;
+  hipStream_t last = nullptr;
+  std::vector<void*> scratch;   // ping-pong view of cs_h, one entry per hidden layer
+  std::vector<void*> allocs;
+  std::string err;
+};
+
+namespace {
+
+int set_err(spz_ctx* c, int code, const std::string& msg) {
+  tl_err = msg;
+  if (c) c->err = msg;
+  return code;
+}
+
+int fail_hip(spz_ctx* c, hipError_t e, const char* what) {
+  return set_err(c, SPZ_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define CK(x)                                          \
+  do {                                                 \
+    hipError_t e_ = (x);                               \
+    if (e_ != hipSuccess) return fail_hip(c, e_, #x);  \
+  } while (0)
+
+#define HK(x)                               \
+  do {                                      \
+    hipError_t e_ = (x);                    \
+    if (e_ != hipSuccess) return e_;        \
+  } while (0)
+
+hipError_t dalloc(spz_ctx* c, void** p, size_t bytes) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 256;
+  HK(hipMalloc(p, bytes));
+  c->allocs.push_back(*p);
+  return hipMemset(*p, 0, bytes);
+}
+
+template <typename P>
+hipError_t dalloc_t(spz_ctx* c, P** p, size_t bytes) {
+  void* v = nullptr;
+  hipError_t e = dalloc(c, &v, bytes);
+  *p = static_cast<P*>(v);
+  return e;
+}
+
+// Flat (unpadded) column i of layer l of net ni -> padded column.
+inline int pcol(const spz_ctx* c, int ni, int l, int i) {
+  return (ni != 0 && l == 0 && i >= c->O) ? c->Ka + (i - c->O) : i;
+}
+
+int64_t flat_count(const Net& n) {
+  int64_t s = 0;
+  for (const Lay& L : n.L) s += (int64_t)L.in_f * L.out_f + L.out_f;
+  return s;
+}
+
+// ---------------------------------------------------------------------------------- layout
+void plan_layout(spz_ctx* c) {
+  const int O = c->O, A = c->A;
+  c->Ka = pad32(O);
+  c->Ap = pad32(A);
+  c->Kc = c->Ka + c->Ap;
+  int64_t off = 0;
+  for (int ni = 0; ni < 3; ++ni) {
+    Net& n = c->net[ni];
+    n.L.clear();
+    n.off = off;
+    std::vector<int> dims;
+    dims.push_back(ni == 0 ? O : O + A);
+    for (int h : c->hidden) dims.push_back(h);
+    dims.push_back(ni == 0 ? (c->td3 ? A : 2 * A) : 1);
+    const int nl = (int)dims.size() - 1;
+    for (int l = 0; l < nl; ++l) {
+      Lay L;
+      L.in_f = dims[l];
+      L.out_f = dims[l + 1];
+      L.in_p = l == 0 ? (ni == 0 ? c->Ka : c->Kc) : pad32(dims[l]);
+      L.out_p = (ni != 0 && l == nl - 1) ? 1 : pad32(dims[l + 1]);
+      L.w = off;
+      off = align64(off + (int64_t)L.out_p * L.in_p);
+      L.b = off;
+      off = align64(off + L.out_p);
+      n.L.push_back(L);
+    }
+    n.end = off;
+  }
+  c->la = off;
+  off = align64(off + 1);
+  c->n_arena = off;
+  c->hmax = 32;
+  for (int h : c->hidden) c->hmax = std::max(c->hmax, pad32(h));
+}
+
+// ---------------------------------------------------------------------------------- init
+// Fan-in uniform init from Philox (computed on the host, bit-exact):
+// k = fl32(1/sqrt(fan_in)), u = (w >> 8) 2^-24, value = fl32((2u - 1) k).
+void host_init(spz_ctx* c, std::vector<float>& img) {
+  img.assign(c->n_arena, 0.0f);
+  for (int ni = 0; ni < 3; ++ni) {
+    for (int l = 0; l < (int)c->net[ni].L.size(); ++l) {
+      const Lay& L = c->net[ni].L[l];
+      const double k = (double)(float)(1.0 / std::sqrt((double)L.in_f));
+      const uint32_t tw = (uint32_t)(ni * 16 + l * 2), tb = tw + 1;
+      for (int o = 0; o < L.out_f; ++o)
+        for (int i = 0; i < L.in_f; ++i) {
+          const uint64_t e = (uint64_t)o * L.in_f + i;
+          const double u = (double)(philox_word(c->seed, e, 0, P_INIT, tw) >> 8) * 0x1p-24;
+          img[L.w + (int64_t)o * L.in_p + pcol(c, ni, l, i)] = (float)((2.0 * u - 1.0) * k);
+        }
+      for (int o = 0; o < L.out_f; ++o) {
+        const double u = (double)(philox_word(c->seed, (uint64_t)o, 0, P_INIT, tb) >> 8) * 0x1p-24;
+        img[L.b + o] = (float)((2.0 * u - 1.0) * k);
+      }
+    }
+  }
+  img[c->la] = c->td3 ? 0.0f : (float)std::log((double)c->hp.alpha_init);
+}
+
+// ---------------------------------------------------------------------------------- pieces
+const void* wop(const spz_ctx* c, bool target, int64_t off) {
+  if (c->bf16) return (target ? c->Tb : c->Pb) + off;
+  return (target ? c->T : c->P) + off;
+}
+const float* wf(const spz_ctx* c, bool target, int64_t off) { return (target ? c->T : c->P) + off; }
+size_t es(const spz_ctx* c) { return c->bf16 ? 2 : 4; }
+const void* elem(const spz_ctx* c, const void* base, int64_t off) {
+  return static_cast<const uint8_t*>(base) + off * (int64_t)es(c);
+}
+
+// Forward of net ni. X: [Bp, ldx] operand tensor (the first in_p(0) columns are read).
+// hid[l] receives hidden layer l; critic heads write q [Bp], the actor head z [Bp, out_p].
+hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, void* const* hid,
+                   float* head, hipStream_t s) {
+  const Net& n = c->net[ni];
+  const int nl = (int)n.L.size();
+  const void* in = X;
+  int64_t ld = ldx;
+  for (int l = 0; l < nl; ++l) {
+    const Lay& L = n.L[l];
+    if (l == nl - 1 && ni != 0) {
+      RowdotArgs r{in, ld, L.in_p, c->Bp, wop(c, target, L.w), wf(c, target, L.b), head};
+      return launch_rowdot(c->bf16, r, s);
+    }
+    GemmArgs g{};
+    g.A = in; g.lda = ld;
+    g.B = wop(c, target, L.w); g.ldb = L.in_p;
+    g.bias = wf(c, target, L.b);
+    g.M = c->Bp; g.N = L.out_p; g.K = L.in_p;
+    if (l == nl - 1) {
+      g.C = head; g.ldc = L.out_p; g.relu = 0; g.out_f32 = 1;
+    } else {
+      g.C = hid[l]; g.ldc = L.out_p; g.relu = 1; g.out_f32 = 0;
+    }
+    HK(gemm(c->bf16, GEMM_FWD, g, s));
+    in = g.C;
+    ld = L.out_p;
+  }
+  return hipSuccess;
+}
+
+hipError_t wgrad(spz_ctx* c, const void* dz, int64_t lddz, const void* X, int64_t ldx, const Lay& L,
+                 float* part, float* cpart, hipStream_t s) {
+  GemmArgs g{};
+  g.A = dz; g.lda = lddz;
+  g.B = X; g.ldb = ldx;
+  g.M = L.out_p; g.N = L.in_p; g.K = c->Bp;
+  g.splits = wgrad_splits(g.M, g.N, g.K);
+  g.C = part; g.ldc = L.in_p;
+  HK(gemm(c->bf16, GEMM_WGRAD, g, s));
+  HK(splitk_reduce(part, g.splits, g.M, g.N, g.ldc, c->G + L.w, L.in_p, s));
+  ColsumArgs cs{dz, lddz, L.out_p, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart};
+  return launch_colsum(c->bf16, cs, c->G + L.b, nullptr, s);
+}
+
+hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_t ldw, int N,
+                 const void* mask, void* out, int64_t ldo, bool out_f32, hipStream_t s) {
+  GemmArgs g{};
+  g.A = dz; g.lda = L.out_p;
+  g.B = W; g.ldb = ldw;
+  g.C = out; g.ldc = ldo; g.out_f32 = out_f32 ? 1 : 0;
+  g.mask = mask; g.ldm = ldo;
+  g.M = c->Bp; g.N = N; g.K = L.out_p;
+  return gemm(c->bf16, GEMM_DGRAD, g, s);
+}
+
+// Critic ni in {1, 2}: weight and bias gradients of L = sum_b dq[b] q[b] given the
+// stored hidden activations hid of the forward on X.
+hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, void* const* hid,
+                           hipStream_t s) {
+  const Net& n = c->net[ni];
+  const int nl = (int)n.L.size();
+  const Lay& H = n.L[nl - 1];
+  ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, c->c_cpart};
+  HK(launch_colsum(c->bf16, cs, c->G + H.w, c->G + H.b, s));
+  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp};
+  HK(launch_head_bwd(c->bf16, hb, s));
+  int cur = 0;
+  for (int l = nl - 2; l >= 0; --l) {
+    const Lay& L = n.L[l];
+    const void* Xl = l == 0 ? X : hid[l - 1];
+    const int64_t ldx = l == 0 ? c->Kc : L.in_p;
+    HK(wgrad(c, c->c_dz[cur], L.out_p, Xl, ldx, L, c->c_wpart, c->c_cpart, s));
+    if (l > 0) {
+      HK(dgrad(c, c->c_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], c->c_dz[cur ^ 1],
+               L.in_p, false, s));
+      cur ^= 1;
+    }
+  }
+  return hipSuccess;
+}
+
+// Gradient of sum_b dq[b] Q_ni(s, a)[b] with respect to the action block, into da [Bp, Ap].
+hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* hid, float* da,
+                              hipStream_t s) {
+  const Net& n = c->net[ni];
+  const int nl = (int)n.L.size();
+  const Lay& H = n.L[nl - 1];
+  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->a_dz[0], H.in_p, H.in_p, c->Bp};
+  HK(launch_head_bwd(c->bf16, hb, s));
+  int cur = 0;
+  for (int l = nl - 2; l >= 1; --l) {
+    const Lay& L = n.L[l];
+    HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], c->a_dz[cur ^ 1],
+             L.in_p, false, s));
+    cur ^= 1;
+  }
+  const Lay& L0 = n.L[0];
+  return dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, c->Ap, nullptr, da,
+               c->Ap, true, s);
+}
+
+hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
+  const Net& n = c->net[0];
+  const int nl = (int)n.L.size();
+  const void* cur = c->dzh;
+  int nxt = 0;
+  for (int l = nl - 1; l >= 0; --l) {
+    const Lay& L = n.L[l];
+    const void* Xl = l == 0 ? c->xsa : c->ha[l - 1];
+    const int64_t ldx = l == 0 ? c->Kc : L.in_p;
+    HK(wgrad(c, cur, L.out_p, Xl, ldx, L, c->a_wpart, c->a_cpart, s));
+    if (l > 0) {
+      HK(dgrad(c, cur, L, wop(c, false, L.w), L.in_p, L.in_p, c->ha[l - 1], c->a_dz[nxt], L.in_p, false, s));
+      cur = c->a_dz[nxt];
+      nxt ^= 1;
+    }
+  }
+  return hipSuccess;
+}
+
+const float* log_alpha_ptr(const spz_ctx* c) { return c->P + c->la; }
+
+// Critic stream: TD target from the target networks, online critic forward on (s, a),
+// critic loss and critic backward.
+hipError_t critic_part(spz_ctx* c, hipStream_t s) {
+  const int pa = c->net[0].L.back().out_p;
+  const spz_hparams& hp = c->hp;
+  if (!c->td3) {
+    HK(forward(c, 0, false, c->xs2, c->Kc, c->scratch.data(), c->z2, s));
+    SacHeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_TGT, hp.log_std_min, hp.log_std_max,
+                  c->xs2, c->Kc, c->Ka, c->logp2, nullptr, nullptr, nullptr};
+    HK(launch_sac_head(c->bf16, h, s));
+  } else {
+    HK(forward(c, 0, true, c->xs2, c->Kc, c->scratch.data(), c->z2, s));
+    Td3HeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, 1, hp.policy_noise, hp.noise_clip,
+                  c->xs2, c->Kc, c->Ka, nullptr};
+    HK(launch_td3_head(c->bf16, h, s));
+  }
+  HK(forward(c, 1, true, c->xs2, c->Kc, c->scratch.data(), c->qt1, s));
+  HK(forward(c, 2, true, c->xs2, c->Kc, c->scratch.data(), c->qt2, s));
+  TdArgs td{c->qt1, c->qt2, c->r, c->d, c->td3 ? nullptr : c->logp2, log_alpha_ptr(c), c->y, hp.gamma,
+            c->B, c->Bp};
+  HK(launch_td_target(td, s));
+  HK(forward(c, 1, false, c->xsa, c->Kc, c->hc[0].data(), c->q1, s));
+  HK(forward(c, 2, false, c->xsa, c->Kc, c->hc[1].data(), c->q2, s));
+  CriticLossArgs cl{c->q1, c->q2, c->y, c->dq1, c->dq2, c->c_lpart, c->B, c->Bp};
+  HK(launch_critic_loss(cl, s));
+  HK(critic_backward(c, 1, c->dq1, c->xsa, c->hc[0].data(), s));
+  HK(critic_backward(c, 2, c->dq2, c->xsa, c->hc[1].data(), s));
+  return hipSuccess;
+}
+
+// Actor stream: reparameterised action on s, critics at their step-start values on
+// (s, a~), actor loss, gradient through the critics to the action, head and actor backward.
+hipError_t actor_part(spz_ctx* c, hipStream_t s) {
+  const int pa = c->net[0].L.back().out_p;
+  const spz_hparams& hp = c->hp;
+  HK(forward(c, 0, false, c->xsa, c->Kc, c->ha.data(), c->z, s));
+  if (!c->td3) {
+    SacHeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_POL, hp.log_std_min, hp.log_std_max,
+                  c->xsp, c->Kc, c->Ka, c->logp, c->th, c->se, c->lm};
+    HK(launch_sac_head(c->bf16, h, s));
+  } else {
+    Td3HeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, 0, 0.0f, 0.0f, c->xsp, c->Kc, c->Ka, c->th};
+    HK(launch_td3_head(c->bf16, h, s));
+  }
+  HK(forward(c, 1, false, c->xsp, c->Kc, c->hpc[0].data(), c->qp1, s));
+  if (!c->td3) HK(forward(c, 2, false, c->xsp, c->Kc, c->hpc[1].data(), c->qp2, s));
+  ActorLossArgs al{c->qp1, c->td3 ? nullptr : c->qp2, c->logp, log_alpha_ptr(c), c->dqp1,
+                   c->td3 ? nullptr : c->dqp2, c->a_lpart, c->B, c->Bp};
+  HK(launch_actor_loss(al, s));
+  HK(critic_action_grad(c, 1, c->dqp1, c->hpc[0].data(), c->da1, s));
+  if (!c->td3) HK(critic_action_grad(c, 2, c->dqp2, c->hpc[1].data(), c->da2, s));
+  ActorHeadBwdArgs hb{c->da1, c->td3 ? nullptr : c->da2, c->Ap, c->th, c->se, c->lm, log_alpha_ptr(c),
+                      c->dzh, pa, c->A, c->B, c->td3 ? 0 : 1};
+  HK(launch_actor_head_bwd(c->bf16, hb, s));
+  return actor_backward(c, s);
+}
+
+int enqueue_step(spz_ctx* c, hipStream_t s0) {
+  const int64_t t = c->h_step + 1;
+  const bool actor_step = !c->td3 || (t % c->hp.policy_delay == 0);
+  GatherArgs g{c->buf, c->row_bytes, c->off_a, c->off_s2, c->off_r, c->off_d, c->O, c->A, c->Ka, c->Kc,
+               c->B, c->seed, (uint32_t)c->size, c->d_step, c->xsa, c->xs2, c->xsp, c->r, c->d, c->idx};
+  CK(launch_gather(c->bf16, g, s0));
+  hipStream_t sc = s0, sa = s0;
+  const bool two = c->hp.n_streams == 2;
+  if (two) {
+    CK(hipEventRecord(c->ev_fork, s0));
+    CK(hipStreamWaitEvent(c->sc, c->ev_fork, 0));
+    CK(hipStreamWaitEvent(c->sa, c->ev_fork, 0));
+    sc = c->sc;
+    sa = c->sa;
+  }
+  CK(critic_part(c, sc));
+  if (actor_step) CK(actor_part(c, sa));
+  if (two) {
+    CK(hipEventRecord(c->ev_c, sc));
+    CK(hipStreamWaitEvent(s0, c->ev_c, 0));
+    if (actor_step) {
+      CK(hipEventRecord(c->ev_a, sa));
+      CK(hipStreamWaitEvent(s0, c->ev_a, 0));
+    }
+  }
+  FinishArgs f{c->c_lpart, c->a_lpart, loss_blocks(c->Bp), loss_blocks(c->Bp), c->B, c->td3 ? 0 : 1,
+               actor_step ? 1 : 0, c->hp.learn_alpha, c->hp.target_entropy, log_alpha_ptr(c),
+               c->td3 ? nullptr : c->G + c->la, c->rec, c->rec_cap, c->d_step};
+  CK(launch_finish(f, s0));
+  const Net& an = c->net[0];
+  AdamArgs a{};
+  a.P = c->P; a.M = c->M; a.V = c->V; a.T = c->T; a.G = c->G; a.Pb = c->Pb; a.Tb = c->Tb;
+  a.n = c->n_arena;
+  a.a0 = an.off; a.a1 = an.end;
+  a.c0 = c->net[1].off; a.c1 = c->net[2].end;
+  a.la = c->la;
+  a.do_actor = actor_step ? 1 : 0;
+  a.do_alpha = (!c->td3 && c->hp.learn_alpha) ? 1 : 0;
+  a.polyak_critic = (!c->td3 || actor_step) ? 1 : 0;
+  a.polyak_actor = (c->td3 && actor_step) ? 1 : 0;
+  a.td3 = c->td3 ? 1 : 0;
+  a.delay = c->hp.policy_delay;
+  a.lr_a = c->hp.lr_actor; a.lr_c = c->hp.lr_critic; a.lr_al = c->hp.lr_alpha;
+  a.b1 = c->hp.beta1; a.b2 = c->hp.beta2; a.eps = c->hp.eps; a.tau = c->hp.tau;
+  a.step = c->d_step;
+  CK(launch_adam(a, s0));
+  c->h_step = t;
+  return SPZ_OK;
+}
+
+int ctx_sync(spz_ctx* c) {
+  if (c->last) CK(hipStreamSynchronize(c->last));
+  CK(hipStreamSynchronize(c->sc));
+  CK(hipStreamSynchronize(c->sa));
+  return SPZ_OK;
+}
+
+int setup(spz_ctx* c) {
+  const size_t e = es(c);
+  const int64_t Bp = c->Bp;
+  const int nh = (int)c->hidden.size();
+  // replay ring
+  c->off_a = (int)(c->O * e);
+  c->off_s2 = (int)((c->O + c->A) * e);
+  c->off_r = (int)((2 * (int64_t)c->O + c->A) * e + 3) / 4 * 4;
+  c->off_d = c->off_r + 4;
+  c->row_bytes = align16(c->off_d + 4);
+  c->cap = c->hp.capacity;
+  CK(dalloc_t(c, &c->buf, (size_t)(c->row_bytes * c->cap)));
+  // parameters
+  const size_t ab = (size_t)c->n_arena * 4;
+  CK(dalloc_t(c, &c->P, ab));
+  CK(dalloc_t(c, &c->G, ab));
+  CK(dalloc_t(c, &c->M, ab));
+  CK(dalloc_t(c, &c->V, ab));
+  CK(dalloc_t(c, &c->T, ab));
+  if (c->bf16) {
+    CK(dalloc_t(c, &c->Pb, (size_t)c->n_arena * 2));
+    CK(dalloc_t(c, &c->Tb, (size_t)c->n_arena * 2));
+  }
+  CK(dalloc_t(c, &c->d_step, 8));
+  CK(dalloc_t(c, &c->rec, (size_t)c->rec_cap * SPZ_REC_WIDTH * 4));
+  // batch
+  const size_t xb = (size_t)Bp * c->Kc * e;
+  CK(dalloc(c, &c->xsa, xb));
+  CK(dalloc(c, &c->xs2, xb));
+  CK(dalloc(c, &c->xsp, xb));
+  CK(dalloc_t(c, &c->r, Bp * 4));
+  CK(dalloc_t(c, &c->d, Bp * 4));
+  CK(dalloc_t(c, &c->idx, Bp * 4));
+  const size_t hb = (size_t)Bp * c->hmax * e;
+  const int pa = c->net[0].L.back().out_p;
+  float** f32s[] = {&c->logp2, &c->qt1, &c->qt2, &c->y, &c->q1, &c->q2, &c->dq1, &c->dq2,
+                    &c->logp, &c->qp1, &c->qp2, &c->dqp1, &c->dqp2};
+  for (float** p : f32s) CK(dalloc_t(c, p, Bp * 4));
+  CK(dalloc_t(c, &c->z2, (size_t)Bp * pa * 4));
+  CK(dalloc_t(c, &c->z, (size_t)Bp * pa * 4));
+  CK(dalloc_t(c, &c->th, (size_t)Bp * c->A * 4));
+  CK(dalloc_t(c, &c->se, (size_t)Bp * c->A * 4));
+  CK(dalloc_t(c, &c->lm, (size_t)Bp * c->A * 4));
+  CK(dalloc_t(c, &c->da1, (size_t)Bp * c->Ap * 4));
+  CK(dalloc_t(c, &c->da2, (size_t)Bp * c->Ap * 4));
+  CK(dalloc(c, &c->dzh, (size_t)Bp * pa * e));
+  for (int i = 0; i < 2; ++i) {
+    CK(dalloc(c, &c->cs_h[i], hb));
+    CK(dalloc(c, &c->c_dz[i], hb));
+    CK(dalloc(c, &c->a_dz[i], hb));
+    c->hc[i].assign(nh, nullptr);
+    c->hpc[i].assign(nh, nullptr);
+    for (int l = 0; l < nh; ++l) {
+      CK(dalloc(c, &c->hc[i][l], (size_t)Bp * pad32(c->hidden[l]) * e));
+      CK(dalloc(c, &c->hpc[i][l], (size_t)Bp * pad32(c->hidden[l]) * e));
+    }
+  }
+  c->ha.assign(nh, nullptr);
+  c->scratch.assign(nh, nullptr);
+  for (int l = 0; l < nh; ++l) {
+    CK(dalloc(c, &c->ha[l], (size_t)Bp * pad32(c->hidden[l]) * e));
+    c->scratch[l] = c->cs_h[l & 1];
+  }
+  // reduction workspaces
+  int64_t wmax = 0, cmax = 0;
+  for (int ni = 0; ni < 3; ++ni)
+    for (const Lay& L : c->net[ni].L) {
+      wmax = std::max<int64_t>(wmax, (int64_t)wgrad_splits(L.out_p, L.in_p, (int)Bp) * L.out_p * L.in_p);
+      cmax = std::max<int64_t>(cmax, (int64_t)std::max(L.out_p, L.in_p) + 1);
+    }
+  const int chunks = colsum_chunks((int)Bp);
+  CK(dalloc_t(c, &c->c_wpart, (size_t)wmax * 4));
+  CK(dalloc_t(c, &c->a_wpart, (size_t)wmax * 4));
+  CK(dalloc_t(c, &c->c_cpart, (size_t)chunks * cmax * 4));
+  CK(dalloc_t(c, &c->a_cpart, (size_t)chunks * cmax * 4));
+  CK(dalloc_t(c, &c->c_lpart, (size_t)loss_blocks((int)Bp) * 3 * 8));
+  CK(dalloc_t(c, &c->a_lpart, (size_t)loss_blocks((int)Bp) * 2 * 8));
+  // streams (default priority)
+  CK(hipStreamCreateWithFlags(&c->sc, hipStreamNonBlocking));
+  CK(hipStreamCreateWithFlags(&c->sa, hipStreamNonBlocking));
+  CK(hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming));
+  CK(hipEventCreateWithFlags(&c->ev_c, hipEventDisableTiming));
+  CK(hipEventCreateWithFlags(&c->ev_a, hipEventDisableTiming));
+  // parameters: host init, targets = online, bf16 images
+  std::vector<float> img;
+  host_init(c, img);
+  CK(hipMemcpy(c->P, img.data(), ab, hipMemcpyHostToDevice));
+  CK(hipMemcpy(c->T, img.data(), ab, hipMemcpyHostToDevice));
+  if (c->bf16) {
+    CK(launch_to_bf16(c->P, c->Pb, c->n_arena, c->sc));
+    CK(launch_to_bf16(c->T, c->Tb, c->n_arena, c->sc));
+  }
+  CK(hipStreamSynchronize(c->sc));
+  CK(hipDeviceSynchronize());
+  return SPZ_OK;
+}
+
+void release(spz_ctx* c) {
+  if (!c) return;
+  (void)hipSetDevice(c->hp.device);
+  if (c->sc) (void)hipStreamSynchronize(c->sc);
+  if (c->sa) (void)hipStreamSynchronize(c->sa);
+  if (c->last) (void)hipStreamSynchronize(c->last);
+  for (void* p : c->allocs) (void)hipFree(p);
+  if (c->stage) (void)hipFree(c->stage);
+  if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
+  if (c->ev_c) (void)hipEventDestroy(c->ev_c);
+  if (c->ev_a) (void)hipEventDestroy(c->ev_a);
+  if (c->sc) (void)hipStreamDestroy(c->sc);
+  if (c->sa) (void)hipStreamDestroy(c->sa);
+  delete c;
+}
+
+// Selector -> (arena, net index or -1 for log alpha).
+int resolve(const spz_ctx* c, int32_t which, float** arena, int* ni) {
+  switch (which) {
+    case SPZ_ACTOR: *arena = c->P; *ni = 0; return 0;
+    case SPZ_CRITIC1: *arena = c->P; *ni = 1; return 0;
+    case SPZ_CRITIC2: *arena = c->P; *ni = 2; return 0;
+    case SPZ_TCRITIC1: *arena = c->T; *ni = 1; return 0;
+    case SPZ_TCRITIC2: *arena = c->T; *ni = 2; return 0;
+    case SPZ_TACTOR: if (!c->td3) return -1; *arena = c->T; *ni = 0; return 0;
+    case SPZ_LOG_ALPHA: *arena = c->P; *ni = -1; return 0;
+    case SPZ_M_ACTOR: *arena = c->M; *ni = 0; return 0;
+    case SPZ_M_CRITIC1: *arena = c->M; *ni = 1; return 0;
+    case SPZ_M_CRITIC2: *arena = c->M; *ni = 2; return 0;
+    case SPZ_M_LOG_ALPHA: *arena = c->M; *ni = -1; return 0;
+    case SPZ_V_ACTOR: *arena = c->V; *ni = 0; return 0;
+    case SPZ_V_CRITIC1: *arena = c->V; *ni = 1; return 0;
+    case SPZ_V_CRITIC2: *arena = c->V; *ni = 2; return 0;
+    case SPZ_V_LOG_ALPHA: *arena = c->V; *ni = -1; return 0;
+    case SPZ_G_ACTOR: *arena = c->G; *ni = 0; return 0;
+    case SPZ_G_CRITIC1: *arena = c->G; *ni = 1; return 0;
+    case SPZ_G_CRITIC2: *arena = c->G; *ni = 2; return 0;
+    case SPZ_G_LOG_ALPHA: *arena = c->G; *ni = -1; return 0;
+  }
+  return -1;
+}
+
+}  // namespace
+
+// ====================================================================================== C ABI
+extern "C" {
+
+void spz_hparams_default(spz_hparams* hp) {
+  if (!hp) return;
+  std::memset(hp, 0, sizeof(*hp));
+  hp->algo = SPZ_ALGO_SAC;
+  hp->gemm_prec = SPZ_PREC_FP32;
+  hp->capacity = 1000000;
+  hp->gamma = 0.99f;
+  hp->tau = 0.005f;
+  hp->lr_actor = hp->lr_critic = hp->lr_alpha = 3e-4f;
+  hp->beta1 = 0.9f;
+  hp->beta2 = 0.999f;
+  hp->eps = 1e-8f;
+  hp->alpha_init = 1.0f;
+  hp->learn_alpha = 1;
+  hp->target_entropy = 0.0f;
+  hp->log_std_min = -20.0f;
+  hp->log_std_max = 2.0f;
+  hp->policy_noise = 0.2f;
+  hp->noise_clip = 0.5f;
+  hp->policy_delay = 2;
+  hp->device = 0;
+  hp->n_streams = 2;
+}
+
+spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int32_t n_hidden, int32_t batch,
+                    const spz_hparams* hp, uint64_t seed) {
+  tl_err.clear();
+  if (!hp || !hidden) { set_err(nullptr, SPZ_EINVAL, "spz_create: NULL hidden or hparams"); return nullptr; }
+  if (obs_dim < 1 || act_dim < 1 || n_hidden < 1 || n_hidden > 6 || batch < 1) {
+    set_err(nullptr, SPZ_EINVAL, "spz_create: dimensions out of range");
+    return nullptr;
+  }
+  for (int i = 0; i < n_hidden; ++i)
+    if (hidden[i] < 1 || hidden[i] > 65536) {
+      set_err(nullptr, SPZ_EINVAL, "spz_create: hidden width out of range");
+      return nullptr;
+    }
+  if ((hp->algo != SPZ_ALGO_SAC && hp->algo != SPZ_ALGO_TD3) ||
+      (hp->gemm_prec != SPZ_PREC_FP32 && hp->gemm_prec != SPZ_PREC_BF16) || hp->capacity < 1 ||
+      hp->capacity > 0xFFFFFFFFll || !(hp->tau >= 0.0f && hp->tau <= 1.0f) ||
+      (hp->algo == SPZ_ALGO_SAC && !(hp->alpha_init > 0.0f)) || hp->policy_delay < 1 ||
+      (hp->n_streams != 1 && hp->n_streams != 2) || !(hp->log_std_min <= hp->log_std_max)) {
+    set_err(nullptr, SPZ_EINVAL, "spz_create: invalid hyper-parameters");
+    return nullptr;
+  }
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || hp->device < 0 || hp->device >= ndev) {
+    set_err(nullptr, SPZ_EINVAL, "spz_create: no such HIP device");
+    return nullptr;
+  }
+  spz_ctx* c = new (std::nothrow) spz_ctx();
+  if (!c) { set_err(nullptr, SPZ_ENOMEM, "spz_create: out of host memory"); return nullptr; }
+  c->O = obs_dim;
+  c->A = act_dim;
+  c->B = batch;
+  c->Bp = (batch + 255) / 256 * 256;
+  c->hidden.assign(hidden, hidden + n_hidden);
+  c->hp = *hp;
+  c->seed = seed;
+  c->bf16 = hp->gemm_prec == SPZ_PREC_BF16;
+  c->td3 = hp->algo == SPZ_ALGO_TD3;
+  if (hipSetDevice(hp->device) != hipSuccess) {
+    set_err(nullptr, SPZ_EHIP, "spz_create: hipSetDevice failed");
+    delete c;
+    return nullptr;
+  }
+  plan_layout(c);
+  const int rc = setup(c);
+  if (rc != SPZ_OK) {
+    const std::string msg = c->err;
+    release(c);
+    set_err(nullptr, rc == SPZ_EHIP && msg.find("hipMalloc") != std::string::npos ? SPZ_ENOMEM : rc, msg);
+    return nullptr;
+  }
+  return c;
+}
+
+void spz_destroy(spz_ctx* c) { release(c); }
+
+int spz_buffer_push(spz_ctx* c, const float* obs, const float* act, const float* rew, const float* done,
+                    const float* next_obs, int64_t n) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_buffer_push: NULL context");
+  if (n < 0) return set_err(c, SPZ_EINVAL, "spz_buffer_push: n < 0");
+  if (n == 0) return SPZ_OK;
+  if (!obs || !act || !rew || !done || !next_obs) return set_err(c, SPZ_EINVAL, "spz_buffer_push: NULL array");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  const int64_t CH = 65536;
+  const int64_t rowf = 2 * (int64_t)c->O + c->A + 2;
+  if (!c->stage) {
+    CK(hipMalloc(&c->stage, (size_t)(CH * rowf * 4)));
+    c->stage_rows = CH;
+  }
+  // Rows overwritten within this push never need to be written.
+  const int64_t skip = n > c->cap ? n - c->cap : 0;
+  for (int64_t r0 = skip; r0 < n; r0 += CH) {
+    const int64_t m = std::min(CH, n - r0);
+    float* so = c->stage;
+    float* sa_ = so + CH * c->O;
+    float* sr = sa_ + CH * c->A;
+    float* sd = sr + CH;
+    float* sn = sd + CH;
+    CK(hipMemcpy(so, obs + r0 * c->O, (size_t)(m * c->O * 4), hipMemcpyHostToDevice));
+    CK(hipMemcpy(sa_, act + r0 * c->A, (size_t)(m * c->A * 4), hipMemcpyHostToDevice));
+    CK(hipMemcpy(sr, rew + r0, (size_t)(m * 4), hipMemcpyHostToDevice));
+    CK(hipMemcpy(sd, done + r0, (size_t)(m * 4), hipMemcpyHostToDevice));
+    CK(hipMemcpy(sn, next_obs + r0 * c->O, (size_t)(m * c->O * 4), hipMemcpyHostToDevice));
+    PackArgs p{c->buf, c->row_bytes, c->off_a, c->off_s2, c->off_r, c->off_d, c->O, c->A, m,
+               (c->ptr + r0) % c->cap, c->cap, so, sa_, sr, sd, sn};
+    CK(launch_pack(c->bf16, p, c->sc));
+    CK(hipStreamSynchronize(c->sc));
+  }
+  c->ptr = (c->ptr + n) % c->cap;
+  c->size = std::min(c->size + n, c->cap);
+  return SPZ_OK;
+}
+
+int64_t spz_buffer_size(const spz_ctx* c) { return c ? c->size : SPZ_EINVAL; }
+
+int spz_update(spz_ctx* c, int32_t n_steps, void* hip_stream) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_update: NULL context");
+  if (n_steps < 0) return set_err(c, SPZ_EINVAL, "spz_update: n_steps < 0");
+  if (c->size == 0) return set_err(c, SPZ_EEMPTY, "spz_update: replay buffer is empty");
+  CK(hipSetDevice(c->hp.device));
+  hipStream_t s0 = static_cast<hipStream_t>(hip_stream);
+  c->last = s0;
+  for (int i = 0; i < n_steps; ++i) {
+    const int rc = enqueue_step(c, s0);
+    if (rc) return rc;
+  }
+  return SPZ_OK;
+}
+
+int spz_synchronize(spz_ctx* c) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_synchronize: NULL context");
+  CK(hipSetDevice(c->hp.device));
+  return ctx_sync(c);
+}
+
+int64_t spz_step(const spz_ctx* c) { return c ? c->h_step : SPZ_EINVAL; }
+
+int spz_set_step(spz_ctx* c, int64_t step) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_set_step: NULL context");
+  if (step < 0) return set_err(c, SPZ_EINVAL, "spz_set_step: step < 0");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  CK(hipMemcpy(c->d_step, &step, 8, hipMemcpyHostToDevice));
+  c->h_step = step;
+  return SPZ_OK;
+}
+
+int64_t spz_param_count(const spz_ctx* c, int32_t which) {
+  if (!c) return SPZ_EINVAL;
+  float* arena = nullptr;
+  int ni = 0;
+  if (resolve(c, which, &arena, &ni)) return SPZ_EINVAL;
+  return ni < 0 ? 1 : flat_count(c->net[ni]);
+}
+
+int spz_read_params(spz_ctx* c, int32_t which, float* out, int64_t n_floats) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_read_params: NULL context");
+  float* arena = nullptr;
+  int ni = 0;
+  if (resolve(c, which, &arena, &ni)) return set_err(c, SPZ_EINVAL, "spz_read_params: bad selector");
+  const int64_t cnt = ni < 0 ? 1 : flat_count(c->net[ni]);
+  if (n_floats != cnt) return set_err(c, SPZ_ESIZE, "spz_read_params: size mismatch");
+  if (!out) return set_err(c, SPZ_EINVAL, "spz_read_params: NULL out");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  if (ni < 0) {
+    CK(hipMemcpy(out, arena + c->la, 4, hipMemcpyDeviceToHost));
+    return SPZ_OK;
+  }
+  const Net& n = c->net[ni];
+  std::vector<float> img((size_t)(n.end - n.off));
+  CK(hipMemcpy(img.data(), arena + n.off, img.size() * 4, hipMemcpyDeviceToHost));
+  int64_t o = 0;
+  for (int l = 0; l < (int)n.L.size(); ++l) {
+    const Lay& L = n.L[l];
+    for (int r = 0; r < L.out_f; ++r)
+      for (int i = 0; i < L.in_f; ++i) out[o++] = img[L.w - n.off + (int64_t)r * L.in_p + pcol(c, ni, l, i)];
+    for (int r = 0; r < L.out_f; ++r) out[o++] = img[L.b - n.off + r];
+  }
+  return SPZ_OK;
+}
+
+int spz_write_params(spz_ctx* c, int32_t which, const float* in, int64_t n_floats) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_write_params: NULL context");
+  float* arena = nullptr;
+  int ni = 0;
+  if (which >= SPZ_G_ACTOR || resolve(c, which, &arena, &ni))
+    return set_err(c, SPZ_EINVAL, "spz_write_params: bad selector");
+  const int64_t cnt = ni < 0 ? 1 : flat_count(c->net[ni]);
+  if (n_floats != cnt) return set_err(c, SPZ_ESIZE, "spz_write_params: size mismatch");
+  if (!in) return set_err(c, SPZ_EINVAL, "spz_write_params: NULL input");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  if (ni < 0) {
+    CK(hipMemcpy(arena + c->la, in, 4, hipMemcpyHostToDevice));
+    return SPZ_OK;
+  }
+  const Net& n = c->net[ni];
+  std::vector<float> img((size_t)(n.end - n.off), 0.0f);
+  int64_t o = 0;
+  for (int l = 0; l < (int)n.L.size(); ++l) {
+    const Lay& L = n.L[l];
+    for (int r = 0; r < L.out_f; ++r)
+      for (int i = 0; i < L.in_f; ++i) img[L.w - n.off + (int64_t)r * L.in_p + pcol(c, ni, l, i)] = in[o++];
+    for (int r = 0; r < L.out_f; ++r) img[L.b - n.off + r] = in[o++];
+  }
+  CK(hipMemcpy(arena + n.off, img.data(), img.size() * 4, hipMemcpyHostToDevice));
+  if (c->bf16 && (arena == c->P || arena == c->T)) {
+    bf16_t* sh = arena == c->P ? c->Pb : c->Tb;
+    CK(launch_to_bf16(arena + n.off, sh + n.off, n.end - n.off, c->sc));
+    CK(hipStreamSynchronize(c->sc));
+  }
+  return SPZ_OK;
+}
+
+int spz_read_losses(spz_ctx* c, float* out, int64_t first_step, int32_t n) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_read_losses: NULL context");
+  if (n < 0 || first_step < 1 || first_step + n - 1 > c->h_step || first_step <= c->h_step - c->rec_cap)
+    return set_err(c, SPZ_EINVAL, "spz_read_losses: steps not available");
+  if (n == 0) return SPZ_OK;
+  if (!out) return set_err(c, SPZ_EINVAL, "spz_read_losses: NULL out");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  for (int i = 0; i < n; ++i) {
+    const int64_t slot = (first_step - 1 + i) % c->rec_cap;
+    CK(hipMemcpy(out + (int64_t)i * SPZ_REC_WIDTH, c->rec + slot * SPZ_REC_WIDTH, SPZ_REC_WIDTH * 4,
+                 hipMemcpyDeviceToHost));
+  }
+  return SPZ_OK;
+}
+
+int spz_debug_read(spz_ctx* c, int32_t what, void* out, int64_t bytes) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_debug_read: NULL context");
+  if (what != SPZ_DBG_INDICES) return set_err(c, SPZ_EINVAL, "spz_debug_read: bad selector");
+  if (bytes != (int64_t)c->B * 4) return set_err(c, SPZ_ESIZE, "spz_debug_read: size mismatch");
+  if (!out) return set_err(c, SPZ_EINVAL, "spz_debug_read: NULL out");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  CK(hipMemcpy(out, c->idx, (size_t)bytes, hipMemcpyDeviceToHost));
+  return SPZ_OK;
+}
+
+const char* spz_last_error(const spz_ctx* c) { return c ? c->err.c_str() : tl_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,311 @@
+// MFMA GEMMs of the MLP forward, input-gradient (dgrad) and weight-gradient
+// (wgrad) products, with their elementwise epilogues fused.
+//
+//   FWD   C[m, n] = act( sum_k X[m, k] W[n, k] + b[n] )       X [M, K], W [N, K]
+//   DGRAD C[m, n] = (sum_k dZ[m, k] W[k, n]) * (H[m, n] > 0)   dZ [M, K], W [K, N]
+//   WGRAD C[s, m, n] = sum_{k in slice s} dZ[k, m] X[k, n]     dZ [K, M], X [K, N]
+//
+// All operands are row-major. A workgroup owns a BM x BN tile; its waves (2x2,
+// 2x1, 1x2 or 1x1) each own TM x TN blocks of 32x32 and step through K in
+// slices of BK = 32 staged in LDS (register prefetch of the next slice while the
+// current one is consumed). Each lane feeds the matrix core with consecutive k
+// values of one row: operands that are k-contiguous in memory are read from LDS
+// as 16-byte vectors, operands that are m/n-contiguous are read element-wise
+// down an LDS column. A and B use the same k-to-lane assignment, which is all
+// the instruction needs. Accumulation is float32 in both precisions:
+//   fp32: v_mfma_f32_32x32x2_f32, 4 instructions per 8 k (one float4 per lane)
+//   bf16: v_mfma_f32_32x32x16_bf16, 1 instruction per 16 k
+// Dimensions are multiples of the tile (the caller pads features to 32 and the
+// batch to 256), so the kernel carries no bounds checks; the host verifies the
+// divisibility before every launch.
+#include "internal.h"
+
+namespace spz {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int BK = 32;
+
+template <typename T> struct Traits;
+template <> struct Traits<float> { static constexpr int VEC = 4, PAD = 4; };
+template <> struct Traits<bf16_t> { static constexpr int VEC = 8, PAD = 8; };
+
+// One operand tile (ROWS along m or n, BK along k) moving global -> registers -> LDS.
+// KC: global element (r, k) at base[(r0 + r) * ld + k0 + k]; LDS [ROWS][BK + PAD].
+// !KC: global element (r, k) at base[(k0 + k) * ld + r0 + r]; LDS [BK][ROWS + PAD].
+template <typename T, bool KC, int ROWS, int NT>
+struct Tile {
+  static constexpr int VEC = Traits<T>::VEC;
+  static constexpr int LD = KC ? (BK + Traits<T>::PAD) : (ROWS + Traits<T>::PAD);
+  static constexpr int SIZE = (KC ? ROWS : BK) * LD;
+  static constexpr int NVEC = ROWS * BK / VEC;
+  static constexpr int PER = (NVEC + NT - 1) / NT;
+  static constexpr int VPR = (KC ? BK : ROWS) / VEC;
+  u32x4 r[PER];
+
+  __device__ inline void load(const T* __restrict__ base, int64_t ld, int r0, int k0, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      if (NVEC % NT == 0 || v < NVEC) {
+        const int a = v / VPR, b = (v % VPR) * VEC;
+        const T* src = KC ? base + (int64_t)(r0 + a) * ld + (k0 + b)
+                          : base + (int64_t)(k0 + a) * ld + (r0 + b);
+        r[p] = *reinterpret_cast<const u32x4*>(src);
+      }
+    }
+  }
+  __device__ inline void store(T* lds, int tid) const {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      if (NVEC % NT == 0 || v < NVEC) {
+        const int a = v / VPR, b = (v % VPR) * VEC;
+        *reinterpret_cast<u32x4*>(lds + a * LD + b) = r[p];
+      }
+    }
+  }
+};
+
+// bf16 fragment: lane supplies 8 consecutive k (ks + 8*(lane/32) ...) of row rb + lane%32.
+template <bool KC, int LD>
+__device__ inline bf16x8 frag_bf16(const bf16_t* lds, int rb, int ks, int lane) {
+  const int row = rb + (lane & 31), kb = ks + 8 * (lane >> 5);
+  if constexpr (KC) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(lds + row * LD + kb));
+  } else {
+    u16x8 t;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) t[j] = lds[(kb + j) * LD + row];
+    return __builtin_bit_cast(bf16x8, t);
+  }
+}
+
+// fp32 fragment: lane supplies 4 consecutive k (ks + 4*(lane/32) ...) of row rb + lane%32,
+// one per instruction.
+template <bool KC, int LD>
+__device__ inline float4 frag_f32(const float* lds, int rb, int ks, int lane) {
+  const int row = rb + (lane & 31), kb = ks + 4 * (lane >> 5);
+  if constexpr (KC) {
+    return *reinterpret_cast<const float4*>(lds + row * LD + kb);
+  } else {
+    return make_float4(lds[kb * LD + row], lds[(kb + 1) * LD + row], lds[(kb + 2) * LD + row],
+                       lds[(kb + 3) * LD + row]);
+  }
+}
+
+constexpr int gemm_threads(int bm, int bn) { return 64 * (bm >= 64 ? 2 : 1) * (bn >= 64 ? 2 : 1); }
+
+template <int BM, int BN> struct Shape {
+  static constexpr int WM = BM >= 64 ? 2 : 1, WN = BN >= 64 ? 2 : 1;
+  static constexpr int NT = 64 * WM * WN;
+  static constexpr int TM = BM / (32 * WM), TN = BN / (32 * WN);
+};
+
+template <typename T, int MODE, int BM, int BN>
+__global__ void __launch_bounds__(gemm_threads(BM, BN)) k_gemm(GemmArgs g) {
+  using S = Shape<BM, BN>;
+  constexpr int TM = S::TM, TN = S::TN, NT = S::NT;
+  constexpr bool AKC = MODE != GEMM_WGRAD;
+  constexpr bool BKC = MODE == GEMM_FWD;
+  using TA = Tile<T, AKC, BM, NT>;
+  using TB = Tile<T, BKC, BN, NT>;
+  __shared__ __attribute__((aligned(16))) T lds_a[TA::SIZE];
+  __shared__ __attribute__((aligned(16))) T lds_b[TB::SIZE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / S::WN, wn = wave % S::WN;
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+  int kbeg = 0, kend = g.K;
+  if constexpr (MODE == GEMM_WGRAD) {
+    const int ks = g.K / g.splits;
+    kbeg = blockIdx.z * ks;
+    kend = kbeg + ks;
+  }
+  const T* __restrict__ A = static_cast<const T*>(g.A);
+  const T* __restrict__ B = static_cast<const T*>(g.B);
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
+
+  TA ta;
+  TB tb;
+  ta.load(A, g.lda, m0, kbeg, tid);
+  tb.load(B, g.ldb, n0, kbeg, tid);
+  for (int k0 = kbeg; k0 < kend; k0 += BK) {
+    __syncthreads();
+    ta.store(lds_a, tid);
+    tb.store(lds_b, tid);
+    __syncthreads();
+    if (k0 + BK < kend) {
+      ta.load(A, g.lda, m0, k0 + BK, tid);
+      tb.load(B, g.ldb, n0, k0 + BK, tid);
+    }
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int ks = 0; ks < BK; ks += 16) {
+        bf16x8 af[TM], bw[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) af[i] = frag_bf16<AKC, TA::LD>(lds_a, (wm * TM + i) * 32, ks, lane);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) bw[j] = frag_bf16<BKC, TB::LD>(lds_b, (wn * TN + j) * 32, ks, lane);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < BK; ks += 8) {
+        float4 af[TM], bw[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) af[i] = frag_f32<AKC, TA::LD>(lds_a, (wm * TM + i) * 32, ks, lane);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) bw[j] = frag_f32<BKC, TB::LD>(lds_b, (wn * TN + j) * 32, ks, lane);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i].x, bw[j].x, acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i].y, bw[j].y, acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i].z, bw[j].z, acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i].w, bw[j].w, acc[i][j], 0, 0, 0);
+          }
+      }
+    }
+  }
+
+  // Epilogue. 32x32 accumulator layout: lane holds column lane%32; register q holds
+  // row 8*(q/4) + 4*(lane/32) + q%4.
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int col = n0 + (wn * TN + j) * 32 + (lane & 31);
+      const int rowb = m0 + (wm * TM + i) * 32 + 4 * (lane >> 5);
+      float bias = 0.0f;
+      if constexpr (MODE == GEMM_FWD) bias = g.bias ? g.bias[col] : 0.0f;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int row = rowb + 8 * (q >> 2) + (q & 3);
+        float v = acc[i][j][q];
+        if constexpr (MODE == GEMM_WGRAD) {
+          static_cast<float*>(g.C)[((int64_t)blockIdx.z * g.M + row) * g.ldc + col] = v;
+        } else {
+          if constexpr (MODE == GEMM_FWD) {
+            v += bias;
+            if (g.relu) v = v < 0.0f ? 0.0f : v;
+          } else {
+            if (g.mask) {
+              const float h = to_f<T>(static_cast<const T*>(g.mask)[(int64_t)row * g.ldm + col]);
+              if (!(h > 0.0f)) v = 0.0f;
+            }
+          }
+          if (g.out_f32) static_cast<float*>(g.C)[(int64_t)row * g.ldc + col] = v;
+          else static_cast<T*>(g.C)[(int64_t)row * g.ldc + col] = from_f<T>(v);
+        }
+      }
+    }
+}
+
+__global__ void k_splitk_reduce(const float* __restrict__ part, int splits, int M, int N, int64_t ldc,
+                                float* __restrict__ out, int64_t ldo) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)M * N) return;
+  const int m = (int)(i / N), n = (int)(i % N);
+  float s = 0.0f;
+  for (int z = 0; z < splits; ++z) s += part[((int64_t)z * M + m) * ldc + n];
+  out[(int64_t)m * ldo + n] = s;
+}
+
+int pick_tile(int n) { return n % 128 == 0 ? 128 : n % 64 == 0 ? 64 : n % 32 == 0 ? 32 : 0; }
+
+template <typename T, int MODE, int BM, int BN>
+hipError_t launch(const GemmArgs& g, hipStream_t s) {
+  dim3 grid(g.N / BN, g.M / BM, MODE == GEMM_WGRAD ? g.splits : 1);
+  k_gemm<T, MODE, BM, BN><<<grid, Shape<BM, BN>::NT, 0, s>>>(g);
+  return hipGetLastError();
+}
+
+template <typename T, int MODE, int BM>
+hipError_t launch_bn(const GemmArgs& g, int bn, hipStream_t s) {
+  switch (bn) {
+    case 128: return launch<T, MODE, BM, 128>(g, s);
+    case 64: return launch<T, MODE, BM, 64>(g, s);
+    case 32: return launch<T, MODE, BM, 32>(g, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T, int MODE>
+hipError_t launch_mode(const GemmArgs& g, hipStream_t s) {
+  const int bn = pick_tile(g.N);
+  if constexpr (MODE == GEMM_WGRAD) {
+    switch (pick_tile(g.M)) {
+      case 128: return launch_bn<T, MODE, 128>(g, bn, s);
+      case 64: return launch_bn<T, MODE, 64>(g, bn, s);
+      case 32: return launch_bn<T, MODE, 32>(g, bn, s);
+    }
+    return hipErrorInvalidValue;
+  } else {
+    return launch_bn<T, MODE, 128>(g, bn, s);
+  }
+}
+
+}  // namespace
+
+int wgrad_splits(int M, int N, int K) {
+  const int bm = pick_tile(M), bn = pick_tile(N);
+  if (!bm || !bn) return 1;
+  const int tiles = (M / bm) * (N / bn);
+  int s = 1;
+  while (tiles * s < 1024 && K % (2 * s * BK) == 0 && K / (2 * s) >= 256) s *= 2;
+  return s;
+}
+
+hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
+  // Shape contract: tiles divide the problem, K slices are whole BK steps,
+  // operand rows are 16-byte aligned.
+  if (g.M <= 0 || g.N <= 0 || g.K <= 0) return hipErrorInvalidValue;
+  if (!pick_tile(g.N)) return hipErrorInvalidValue;
+  if (mode == GEMM_WGRAD) {
+    if (!pick_tile(g.M) || g.splits < 1 || g.K % (g.splits * BK)) return hipErrorInvalidValue;
+  } else {
+    if (g.M % 128 || g.K % BK) return hipErrorInvalidValue;
+  }
+  const int vec = bf16 ? 8 : 4;
+  if (g.lda % vec || g.ldb % vec) return hipErrorInvalidValue;
+  if (bf16) {
+    switch (mode) {
+      case GEMM_FWD: return launch_mode<bf16_t, GEMM_FWD>(g, s);
+      case GEMM_DGRAD: return launch_mode<bf16_t, GEMM_DGRAD>(g, s);
+      case GEMM_WGRAD: return launch_mode<bf16_t, GEMM_WGRAD>(g, s);
+    }
+  } else {
+    switch (mode) {
+      case GEMM_FWD: return launch_mode<float, GEMM_FWD>(g, s);
+      case GEMM_DGRAD: return launch_mode<float, GEMM_DGRAD>(g, s);
+      case GEMM_WGRAD: return launch_mode<float, GEMM_WGRAD>(g, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t splitk_reduce(const float* part, int splits, int M, int N, int64_t ldc, float* out,
+                         int64_t ldo, hipStream_t s) {
+  const int64_t n = (int64_t)M * N;
+  k_splitk_reduce<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, splits, M, N, ldc, out, ldo);
+  return hipGetLastError();
+}
+
+}  // namespace spz

@@ -1,0 +1,104 @@
+// Argument blocks and launchers of the non-GEMM kernels (kernels.hip).
+#pragma once
+
+#include "internal.h"
+
+namespace spz {
+
+constexpr int COLSUM_CHUNK = 512;  // rows per first-pass block of the column sums
+
+struct GatherArgs {
+  const uint8_t* buf; int64_t row_bytes;
+  int off_a, off_s2, off_r, off_d;   // byte offsets inside a ring row (obs at 0)
+  int O, A, Ka, Kc, B;
+  uint64_t seed; uint32_t size; const int64_t* step;
+  void* xsa; void* xs2; void* xsp;   // [Bp, Kc] operand tensors
+  float* r; float* d; int32_t* idx;
+};
+
+struct PackArgs {
+  uint8_t* buf; int64_t row_bytes; int off_a, off_s2, off_r, off_d;
+  int O, A; int64_t n, ptr, capacity;
+  const float *obs, *act, *rew, *done, *nobs;   // device staging
+};
+
+struct SacHeadArgs {
+  const float* z; int ldz; int A, B;
+  uint64_t seed; const int64_t* step; uint32_t purpose;
+  float lmin, lmax;
+  void* x; int64_t ldx; int xoff;      // action columns of the next operand tensor
+  float* logp;
+  float *th, *se, *lm;                 // backward cache [B, A] (null for the target side)
+};
+
+struct Td3HeadArgs {
+  const float* z; int ldz; int A, B;
+  uint64_t seed; const int64_t* step;
+  int smooth; float noise, clip;
+  void* x; int64_t ldx; int xoff;
+  float* th;                           // cache of tanh z (policy side) or null
+};
+
+struct RowdotArgs {
+  const void* H; int64_t ld; int K, rows;
+  const void* w; const float* bias; float* q;
+};
+
+struct HeadBwdArgs {
+  const float* dq; const void* w; const void* H; void* dH; int64_t ld; int K, rows;
+};
+
+struct TdArgs {
+  const float *q1, *q2, *r, *d, *logp, *log_alpha; float* y; float gamma; int B, Bp;
+};
+
+struct CriticLossArgs {
+  const float *q1, *q2, *y; float *dq1, *dq2; double* part; int B, Bp;
+};
+
+struct ActorLossArgs {
+  const float *qp1, *qp2, *logp, *log_alpha; float *dqp1, *dqp2; double* part; int B, Bp;
+};
+
+struct ActorHeadBwdArgs {
+  const float *da1, *da2; int ldda; const float *th, *se, *lm, *log_alpha;
+  void* dz; int ldz; int A, B; int sac;
+};
+
+struct ColsumArgs {
+  const void* X; int64_t ld; int N, rows, chunk; const float* weights; int extra; float* part;
+};
+
+struct AdamArgs {
+  float *P, *M, *V, *T; const float* G; bf16_t *Pb, *Tb;
+  int64_t n, a0, a1, c0, c1, la;
+  int do_actor, do_alpha, polyak_critic, polyak_actor, td3, delay;
+  float lr_a, lr_c, lr_al, b1, b2, eps, tau;
+  const int64_t* step;
+};
+
+struct FinishArgs {
+  const double *cpart, *apart; int nc, na, B;
+  int sac, actor_step, learn_alpha; float target_entropy;
+  const float* log_alpha; float* grad_alpha;
+  float* rec; int64_t rec_cap; int64_t* step;
+};
+
+hipError_t launch_gather(bool bf16, const GatherArgs& g, hipStream_t s);
+hipError_t launch_pack(bool bf16, const PackArgs& p, hipStream_t s);
+hipError_t launch_sac_head(bool bf16, const SacHeadArgs& h, hipStream_t s);
+hipError_t launch_td3_head(bool bf16, const Td3HeadArgs& h, hipStream_t s);
+hipError_t launch_rowdot(bool bf16, const RowdotArgs& r, hipStream_t s);
+hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s);
+hipError_t launch_td_target(const TdArgs& a, hipStream_t s);
+int loss_blocks(int Bp);
+hipError_t launch_critic_loss(const CriticLossArgs& a, hipStream_t s);
+hipError_t launch_actor_loss(const ActorLossArgs& a, hipStream_t s);
+hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream_t s);
+int colsum_chunks(int rows);
+hipError_t launch_colsum(bool bf16, const ColsumArgs& a, float* out, float* out_extra, hipStream_t s);
+hipError_t launch_adam(const AdamArgs& a, hipStream_t s);
+hipError_t launch_finish(const FinishArgs& f, hipStream_t s);
+hipError_t launch_to_bf16(const float* src, bf16_t* dst, int64_t n, hipStream_t s);
+
+}  // namespace spz

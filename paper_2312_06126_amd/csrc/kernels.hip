@@ -1,0 +1,477 @@
+// Elementwise, row and reduction kernels of the update step (everything that is
+// not a matrix product): replay sampling and gather, policy heads, twin-Q / TD
+// target / losses, critic output head, bias-gradient column sums, the fused
+// Adam + Polyak pass and the per-step finish (loss record, temperature gradient,
+// step counter).
+//
+// Reductions are deterministic: fixed per-thread order, fixed tree inside a
+// block, partials reduced in index order by a second pass. No atomics.
+#include "kernels.h"
+
+namespace spz {
+namespace {
+
+constexpr float LN2F = 0.69314718055994531f;
+constexpr float HALF_LN_2PI_F = 0.91893853320467274f;
+
+__device__ inline float softplusf(float x) { return x > 0.0f ? x + log1pf(expf(-x)) : log1pf(expf(x)); }
+
+// Standard normal deviate for flat element i of the stream (seed, step, purpose):
+// Box-Muller on words (0,1) -> lanes 0,1 and (2,3) -> lanes 2,3 of each Philox block.
+__device__ inline float normal_at(uint64_t seed, uint64_t i, uint32_t step, uint32_t purpose) {
+  const U4 w = philox(U4{(uint32_t)(i >> 2), step, purpose, 0u}, (uint32_t)seed, (uint32_t)(seed >> 32));
+  const int lane = (int)(i & 3);
+  const uint32_t wa = lane < 2 ? w.x : w.z, wb = lane < 2 ? w.y : w.w;
+  const float u1 = (float)((wa >> 8) + 1u) * 5.9604644775390625e-8f;  // (0, 1]
+  const float u2 = (float)(wb >> 8) * 5.9604644775390625e-8f;          // [0, 1)
+  const float rad = sqrtf(-2.0f * logf(u1));
+  float sn, cs;
+  sincospif(2.0f * u2, &sn, &cs);
+  return rad * ((lane & 1) ? sn : cs);
+}
+
+template <int NT>
+__device__ inline double block_sum(double v, double* sh) {
+  const int t = threadIdx.x;
+  sh[t] = v;
+  __syncthreads();
+#pragma unroll
+  for (int s = NT / 2; s > 0; s >>= 1) {
+    if (t < s) sh[t] += sh[t + s];
+    __syncthreads();
+  }
+  const double r = sh[0];
+  __syncthreads();
+  return r;
+}
+
+// ------------------------------------------------------------------------------ replay
+template <typename T>
+__global__ void __launch_bounds__(256) k_gather(GatherArgs g) {
+  const int lane = threadIdx.x & 63;
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= g.B) return;
+  const uint32_t t = (uint32_t)(*g.step + 1);
+  const uint32_t w = philox_word(g.seed, (uint64_t)b, t, P_IDX, 0u);
+  const uint32_t row = mulhi32(w, g.size);
+  const uint8_t* src = g.buf + (int64_t)row * g.row_bytes;
+  const T* s = reinterpret_cast<const T*>(src);
+  const T* a = reinterpret_cast<const T*>(src + g.off_a);
+  const T* s2 = reinterpret_cast<const T*>(src + g.off_s2);
+  T* xsa = static_cast<T*>(g.xsa) + (int64_t)b * g.Kc;
+  T* xsp = static_cast<T*>(g.xsp) + (int64_t)b * g.Kc;
+  T* xs2 = static_cast<T*>(g.xs2) + (int64_t)b * g.Kc;
+  for (int j = lane; j < g.O; j += 64) {
+    const T v = s[j];
+    xsa[j] = v;
+    xsp[j] = v;
+    xs2[j] = s2[j];
+  }
+  for (int j = lane; j < g.A; j += 64) xsa[g.Ka + j] = a[j];
+  if (lane == 0) {
+    g.r[b] = *reinterpret_cast<const float*>(src + g.off_r);
+    g.d[b] = *reinterpret_cast<const float*>(src + g.off_d);
+    g.idx[b] = (int32_t)row;
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) k_pack_rows(PackArgs p) {
+  const int lane = threadIdx.x & 63;
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= p.n) return;
+  const int64_t slot = (p.ptr + i) % p.capacity;
+  uint8_t* dst = p.buf + slot * p.row_bytes;
+  T* s = reinterpret_cast<T*>(dst);
+  T* a = reinterpret_cast<T*>(dst + p.off_a);
+  T* s2 = reinterpret_cast<T*>(dst + p.off_s2);
+  for (int j = lane; j < p.O; j += 64) {
+    s[j] = from_f<T>(p.obs[i * p.O + j]);
+    s2[j] = from_f<T>(p.nobs[i * p.O + j]);
+  }
+  for (int j = lane; j < p.A; j += 64) a[j] = from_f<T>(p.act[i * p.A + j]);
+  if (lane == 0) {
+    *reinterpret_cast<float*>(dst + p.off_r) = p.rew[i];
+    *reinterpret_cast<float*>(dst + p.off_d) = p.done[i];
+  }
+}
+
+// ------------------------------------------------------------------------------ heads
+// SAC head: z = [mu | l] -> a = tanh(mu + exp(clip(l)) eps) written into the action
+// columns of x, and the tanh-Gaussian log-density (overflow-free form of
+// log(1 - tanh^2 u) = 2 (ln 2 - u - softplus(-2u))). Optional cache for backward.
+template <typename T>
+__global__ void __launch_bounds__(256) k_sac_head(SacHeadArgs h) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= h.B) return;
+  const uint32_t t = (uint32_t)(*h.step + 1);
+  const float* z = h.z + (int64_t)b * h.ldz;
+  T* x = static_cast<T*>(h.x) + (int64_t)b * h.ldx + h.xoff;
+  float lp = 0.0f;
+  for (int j = 0; j < h.A; ++j) {
+    const float eps = normal_at(h.seed, (uint64_t)b * h.A + j, t, h.purpose);
+    const float mu = z[j], l = z[h.A + j];
+    const float lc = fminf(fmaxf(l, h.lmin), h.lmax);
+    const float sig = expf(lc);
+    const float u = mu + sig * eps;
+    const float a = tanhf(u);
+    x[j] = from_f<T>(a);
+    lp += -0.5f * eps * eps - lc - HALF_LN_2PI_F - 2.0f * (LN2F - u - softplusf(-2.0f * u));
+    if (h.th) {
+      const int64_t c = (int64_t)b * h.A + j;
+      h.th[c] = a;
+      h.se[c] = sig * eps;
+      h.lm[c] = (l >= h.lmin && l <= h.lmax) ? 1.0f : 0.0f;
+    }
+  }
+  h.logp[b] = lp;
+}
+
+// TD3 heads. Target: a' = clip(tanh z + clip(noise * eps, -c, c), -1, 1). Policy: a = tanh z.
+template <typename T>
+__global__ void __launch_bounds__(256) k_td3_head(Td3HeadArgs h) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= h.B) return;
+  const uint32_t t = (uint32_t)(*h.step + 1);
+  const float* z = h.z + (int64_t)b * h.ldz;
+  T* x = static_cast<T*>(h.x) + (int64_t)b * h.ldx + h.xoff;
+  for (int j = 0; j < h.A; ++j) {
+    float a = tanhf(z[j]);
+    if (h.smooth) {
+      const float eps = normal_at(h.seed, (uint64_t)b * h.A + j, t, P_NOISE_TGT);
+      const float nz = fminf(fmaxf(h.noise * eps, -h.clip), h.clip);
+      a = fminf(fmaxf(a + nz, -1.0f), 1.0f);
+    }
+    x[j] = from_f<T>(a);
+    if (h.th) h.th[(int64_t)b * h.A + j] = a;
+  }
+}
+
+// Critic output layer (width 1): q[b] = sum_k H[b, k] w[k] + bias. One wave per row.
+template <typename T>
+__global__ void __launch_bounds__(256) k_rowdot(RowdotArgs r) {
+  const int lane = threadIdx.x & 63;
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= r.rows) return;
+  const T* h = static_cast<const T*>(r.H) + (int64_t)b * r.ld;
+  const T* w = static_cast<const T*>(r.w);
+  float s = 0.0f;
+  for (int k = lane; k < r.K; k += 64) s = fmaf(to_f<T>(h[k]), to_f<T>(w[k]), s);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if (lane == 0) r.q[b] = s + *r.bias;
+}
+
+// Critic output layer backward: dH[b, k] = rnd(dq[b]) * w[k] * (H[b, k] > 0), stored
+// in the operand type. Pad rows have dq = 0 and pad columns have w = 0.
+template <typename T>
+__global__ void __launch_bounds__(256) k_head_bwd(HeadBwdArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)a.rows * a.K) return;
+  const int b = (int)(i / a.K), k = (int)(i % a.K);
+  const float dq = to_f<T>(from_f<T>(a.dq[b]));
+  const T* H = static_cast<const T*>(a.H);
+  float v = dq * to_f<T>(static_cast<const T*>(a.w)[k]);
+  if (!(to_f<T>(H[(int64_t)b * a.ld + k]) > 0.0f)) v = 0.0f;
+  static_cast<T*>(a.dH)[(int64_t)b * a.ld + k] = from_f<T>(v);
+}
+
+// ------------------------------------------------------------------------------ TD target, losses
+__global__ void __launch_bounds__(256) k_td_target(TdArgs a) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= a.Bp) return;
+  if (b >= a.B) { a.y[b] = 0.0f; return; }
+  float m = fminf(a.q1[b], a.q2[b]);
+  if (a.logp) m -= expf(*a.log_alpha) * a.logp[b];
+  a.y[b] = a.r[b] + a.gamma * (1.0f - a.d[b]) * m;
+}
+
+// dq_i = 2 (q_i - y) / B and per-block partial sums of (q1-y)^2, (q2-y)^2, q1.
+__global__ void __launch_bounds__(256) k_critic_loss(CriticLossArgs a) {
+  __shared__ double sh[256];
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  double e1s = 0.0, e2s = 0.0, q1s = 0.0;
+  if (b < a.Bp) {
+    float d1 = 0.0f, d2 = 0.0f;
+    if (b < a.B) {
+      const float e1 = a.q1[b] - a.y[b], e2 = a.q2[b] - a.y[b];
+      d1 = 2.0f * e1 / (float)a.B;
+      d2 = 2.0f * e2 / (float)a.B;
+      e1s = (double)e1 * e1;
+      e2s = (double)e2 * e2;
+      q1s = a.q1[b];
+    }
+    a.dq1[b] = d1;
+    a.dq2[b] = d2;
+  }
+  e1s = block_sum<256>(e1s, sh);
+  e2s = block_sum<256>(e2s, sh);
+  q1s = block_sum<256>(q1s, sh);
+  if (threadIdx.x == 0) {
+    a.part[blockIdx.x * 3 + 0] = e1s;
+    a.part[blockIdx.x * 3 + 1] = e2s;
+    a.part[blockIdx.x * 3 + 2] = q1s;
+  }
+}
+
+// SAC: dqp_i routes -1/B to the smaller critic (critic 1 on ties); partial sums of
+// alpha log pi - min(q1, q2) and log pi. TD3 (qp2 == null): dqp1 = -1/B; partial sum of q1.
+__global__ void __launch_bounds__(256) k_actor_loss(ActorLossArgs a) {
+  __shared__ double sh[256];
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  double l0 = 0.0, l1 = 0.0;
+  if (b < a.Bp) {
+    float g1 = 0.0f, g2 = 0.0f;
+    if (b < a.B) {
+      const float inv = -1.0f / (float)a.B;
+      if (a.qp2) {
+        const float q1 = a.qp1[b], q2 = a.qp2[b];
+        const bool take1 = q1 <= q2;
+        g1 = take1 ? inv : 0.0f;
+        g2 = take1 ? 0.0f : inv;
+        const float alpha = expf(*a.log_alpha);
+        l0 = (double)alpha * a.logp[b] - (double)(take1 ? q1 : q2);
+        l1 = a.logp[b];
+      } else {
+        g1 = inv;
+        l0 = a.qp1[b];
+      }
+    }
+    a.dqp1[b] = g1;
+    if (a.dqp2) a.dqp2[b] = g2;
+  }
+  l0 = block_sum<256>(l0, sh);
+  l1 = block_sum<256>(l1, sh);
+  if (threadIdx.x == 0) {
+    a.part[blockIdx.x * 2 + 0] = l0;
+    a.part[blockIdx.x * 2 + 1] = l1;
+  }
+}
+
+// Actor head backward. SAC: g_u = da (1 - a^2) + (alpha/B) 2 a, d mu = g_u,
+// d l = (g_u sigma eps - alpha/B) * [lmin <= l <= lmax]. TD3: dz = da (1 - a^2).
+template <typename T>
+__global__ void __launch_bounds__(256) k_actor_head_bwd(ActorHeadBwdArgs h) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= h.B) return;
+  T* dz = static_cast<T*>(h.dz) + (int64_t)b * h.ldz;
+  const float aB = h.sac ? expf(*h.log_alpha) / (float)h.B : 0.0f;
+  for (int j = 0; j < h.A; ++j) {
+    const int64_t c = (int64_t)b * h.A + j;
+    float da = h.da1[(int64_t)b * h.ldda + j];
+    if (h.da2) da += h.da2[(int64_t)b * h.ldda + j];
+    const float a = h.th[c];
+    float gu = da * (1.0f - a * a);
+    if (h.sac) {
+      gu += aB * 2.0f * a;
+      dz[h.A + j] = from_f<T>((gu * h.se[c] - aB) * h.lm[c]);
+    }
+    dz[j] = from_f<T>(gu);
+  }
+}
+
+// ------------------------------------------------------------------------------ column sums
+// part[c, n] = sum over rows of chunk c of wt(b) X[b, n] for n < N, and wt(b) for n == N
+// (when extra). wt(b) = rnd(weights[b]) or 1.
+template <typename T>
+__global__ void __launch_bounds__(256) k_colsum(ColsumArgs a) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  const int ncol = a.N + (a.extra ? 1 : 0);
+  if (n >= ncol) return;
+  const int b0 = blockIdx.y * a.chunk, b1 = min(b0 + a.chunk, a.rows);
+  const T* X = static_cast<const T*>(a.X);
+  float s = 0.0f;
+  for (int b = b0; b < b1; ++b) {
+    const float w = a.weights ? to_f<T>(from_f<T>(a.weights[b])) : 1.0f;
+    const float x = n < a.N ? to_f<T>(X[(int64_t)b * a.ld + n]) : 1.0f;
+    s = fmaf(w, x, s);
+  }
+  a.part[(int64_t)blockIdx.y * ncol + n] = s;
+}
+
+__global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ part, int chunks, int N,
+                                                      int extra, float* __restrict__ out,
+                                                      float* __restrict__ out_extra) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  const int ncol = N + (extra ? 1 : 0);
+  if (n >= ncol) return;
+  float s = 0.0f;
+  for (int c = 0; c < chunks; ++c) s += part[(int64_t)c * ncol + n];
+  if (n < N) out[n] = s;
+  else *out_extra = s;
+}
+
+// ------------------------------------------------------------------------------ optimizer
+// Adam (bias-corrected, one counter per optimizer) on the actor range, the critic
+// range and log(alpha); then Polyak tbar <- (1 - tau) tbar + tau theta on the
+// target ranges; refreshes the bfloat16 shadows of what it wrote.
+__global__ void __launch_bounds__(256) k_adam_polyak(AdamArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.n) return;
+  const int64_t t = *a.step;
+  const bool in_actor = i >= a.a0 && i < a.a1;
+  const bool in_critic = i >= a.c0 && i < a.c1;
+  const bool is_alpha = i == a.la;
+  float lr;
+  int64_t tt;
+  if (in_actor && a.do_actor) {
+    lr = a.lr_a;
+    tt = a.td3 ? t / a.delay : t;
+  } else if (in_critic) {
+    lr = a.lr_c;
+    tt = t;
+  } else if (is_alpha && a.do_alpha) {
+    lr = a.lr_al;
+    tt = t;
+  } else {
+    return;
+  }
+  const float bc1 = (float)(1.0 - pow((double)a.b1, (double)tt));
+  const float bc2 = (float)(1.0 - pow((double)a.b2, (double)tt));
+  const float g = a.G[i];
+  const float m = a.b1 * a.M[i] + (1.0f - a.b1) * g;
+  const float v = a.b2 * a.V[i] + (1.0f - a.b2) * g * g;
+  a.M[i] = m;
+  a.V[i] = v;
+  const float p = a.P[i] - lr * (m / bc1) / (sqrtf(v / bc2) + a.eps);
+  a.P[i] = p;
+  if (a.Pb) a.Pb[i] = f2bf(p);
+  const bool pol = (in_critic && a.polyak_critic) || (in_actor && a.polyak_actor);
+  if (pol) {
+    const float tb = (1.0f - a.tau) * a.T[i] + a.tau * p;
+    a.T[i] = tb;
+    if (a.Tb) a.Tb[i] = f2bf(tb);
+  }
+}
+
+// One block: reduce the step's loss partials in index order, write the loss
+// record, the temperature gradient, and advance the device step counter.
+__global__ void __launch_bounds__(256) k_finish(FinishArgs f) {
+  __shared__ double sh[256];
+  double e1 = 0.0, e2 = 0.0, q1 = 0.0, l0 = 0.0, l1 = 0.0;
+  for (int i = threadIdx.x; i < f.nc; i += 256) {
+    e1 += f.cpart[i * 3 + 0];
+    e2 += f.cpart[i * 3 + 1];
+    q1 += f.cpart[i * 3 + 2];
+  }
+  if (f.actor_step)
+    for (int i = threadIdx.x; i < f.na; i += 256) {
+      l0 += f.apart[i * 2 + 0];
+      l1 += f.apart[i * 2 + 1];
+    }
+  e1 = block_sum<256>(e1, sh);
+  e2 = block_sum<256>(e2, sh);
+  q1 = block_sum<256>(q1, sh);
+  l0 = block_sum<256>(l0, sh);
+  l1 = block_sum<256>(l1, sh);
+  if (threadIdx.x != 0) return;
+  const int64_t t = *f.step + 1;
+  const double invB = 1.0 / (double)f.B;
+  float rec[SPZ_REC_WIDTH];
+  rec[SPZ_REC_LQ] = (float)((e1 + e2) * invB);
+  rec[SPZ_REC_Q1] = (float)(q1 * invB);
+  rec[SPZ_REC_LPI] = 0.0f;
+  rec[SPZ_REC_LALPHA] = 0.0f;
+  rec[SPZ_REC_ALPHA] = 0.0f;
+  rec[SPZ_REC_LOGPI] = 0.0f;
+  if (f.sac) {
+    const float log_alpha = *f.log_alpha;
+    const double mean_lp = l1 * invB;
+    rec[SPZ_REC_LPI] = (float)(l0 * invB);
+    rec[SPZ_REC_LOGPI] = (float)mean_lp;
+    rec[SPZ_REC_ALPHA] = expf(log_alpha);
+    const double mh = mean_lp + (double)f.target_entropy;
+    rec[SPZ_REC_LALPHA] = (float)(-(double)log_alpha * mh);
+    if (f.grad_alpha) *f.grad_alpha = f.learn_alpha ? (float)(-mh) : 0.0f;
+  } else if (f.actor_step) {
+    rec[SPZ_REC_LPI] = (float)(-l0 * invB);
+  }
+  bool bad = false;
+  for (int i = 0; i < 6; ++i) bad = bad || !isfinite(rec[i]);
+  rec[SPZ_REC_NONFINITE] = bad ? 1.0f : 0.0f;
+  rec[SPZ_REC_ACTOR] = f.actor_step ? 1.0f : 0.0f;
+  float* dst = f.rec + ((t - 1) % f.rec_cap) * SPZ_REC_WIDTH;
+  for (int i = 0; i < SPZ_REC_WIDTH; ++i) dst[i] = rec[i];
+  *f.step = t;
+}
+
+__global__ void __launch_bounds__(256) k_to_bf16(const float* __restrict__ src, bf16_t* __restrict__ dst, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = f2bf(src[i]);
+}
+
+inline unsigned blocks(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+// ------------------------------------------------------------------------------ launchers
+#define SPZ_LAUNCH_T(bf16, kern, grid, block, s, arg)                 \
+  do {                                                               \
+    if (bf16) kern<bf16_t><<<(grid), (block), 0, (s)>>>(arg);        \
+    else kern<float><<<(grid), (block), 0, (s)>>>(arg);              \
+  } while (0)
+
+hipError_t launch_gather(bool bf16, const GatherArgs& g, hipStream_t s) {
+  SPZ_LAUNCH_T(bf16, k_gather, blocks(g.B, 4), 256, s, g);
+  return hipGetLastError();
+}
+hipError_t launch_pack(bool bf16, const PackArgs& p, hipStream_t s) {
+  SPZ_LAUNCH_T(bf16, k_pack_rows, blocks(p.n, 4), 256, s, p);
+  return hipGetLastError();
+}
+hipError_t launch_sac_head(bool bf16, const SacHeadArgs& h, hipStream_t s) {
+  SPZ_LAUNCH_T(bf16, k_sac_head, blocks(h.B, 256), 256, s, h);
+  return hipGetLastError();
+}
+hipError_t launch_td3_head(bool bf16, const Td3HeadArgs& h, hipStream_t s) {
+  SPZ_LAUNCH_T(bf16, k_td3_head, blocks(h.B, 256), 256, s, h);
+  return hipGetLastError();
+}
+hipError_t launch_rowdot(bool bf16, const RowdotArgs& r, hipStream_t s) {
+  SPZ_LAUNCH_T(bf16, k_rowdot, blocks(r.rows, 4), 256, s, r);
+  return hipGetLastError();
+}
+hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s) {
+  SPZ_LAUNCH_T(bf16, k_head_bwd, blocks((int64_t)a.rows * a.K, 256), 256, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_td_target(const TdArgs& a, hipStream_t s) {
+  k_td_target<<<blocks(a.Bp, 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+int loss_blocks(int Bp) { return (int)blocks(Bp, 256); }
+hipError_t launch_critic_loss(const CriticLossArgs& a, hipStream_t s) {
+  k_critic_loss<<<blocks(a.Bp, 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+hipError_t launch_actor_loss(const ActorLossArgs& a, hipStream_t s) {
+  k_actor_loss<<<blocks(a.Bp, 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream_t s) {
+  SPZ_LAUNCH_T(bf16, k_actor_head_bwd, blocks(h.B, 256), 256, s, h);
+  return hipGetLastError();
+}
+int colsum_chunks(int rows) { return (int)blocks(rows, COLSUM_CHUNK); }
+hipError_t launch_colsum(bool bf16, const ColsumArgs& a, float* out, float* out_extra, hipStream_t s) {
+  const int ncol = a.N + (a.extra ? 1 : 0);
+  const int chunks = (int)blocks(a.rows, a.chunk);
+  dim3 grid(blocks(ncol, 256), chunks);
+  SPZ_LAUNCH_T(bf16, k_colsum, grid, 256, s, a);
+  k_colsum_final<<<blocks(ncol, 256), 256, 0, s>>>(a.part, chunks, a.N, a.extra, out, out_extra);
+  return hipGetLastError();
+}
+hipError_t launch_adam(const AdamArgs& a, hipStream_t s) {
+  k_adam_polyak<<<blocks(a.n, 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+hipError_t launch_finish(const FinishArgs& f, hipStream_t s) {
+  k_finish<<<1, 256, 0, s>>>(f);
+  return hipGetLastError();
+}
+hipError_t launch_to_bf16(const float* src, bf16_t* dst, int64_t n, hipStream_t s) {
+  k_to_bf16<<<blocks(n, 256), 256, 0, s>>>(src, dst, n);
+  return hipGetLastError();
+}
+
+}  // namespace spz

@@ -1,0 +1,193 @@
+"""ctypes binding of libspz.so (include/spz.h): argument marshalling only.
+
+Every step of the update runs in the HIP library. If the library is missing the
+import of this module fails; there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspz.so")
+
+SPZ_OK, SPZ_EINVAL, SPZ_ENOMEM, SPZ_EEMPTY, SPZ_ESIZE, SPZ_EHIP = 0, -1, -2, -3, -4, -5
+ALGOS = {"sac": 0, "td3": 1}
+PRECS = {"fp32": 0, "bf16": 1}
+SELECTORS = {
+    "actor": 0, "critic1": 1, "critic2": 2, "tcritic1": 3, "tcritic2": 4, "tactor": 5, "log_alpha": 6,
+    "m_actor": 7, "m_critic1": 8, "m_critic2": 9, "m_log_alpha": 10,
+    "v_actor": 11, "v_critic1": 12, "v_critic2": 13, "v_log_alpha": 14,
+    "g_actor": 15, "g_critic1": 16, "g_critic2": 17, "g_log_alpha": 18,
+}
+DBG_INDICES = 0
+REC_WIDTH = 8
+EXPORTS = ["spz_hparams_default", "spz_create", "spz_destroy", "spz_buffer_push", "spz_buffer_size",
+           "spz_update", "spz_synchronize", "spz_step", "spz_set_step", "spz_param_count",
+           "spz_read_params", "spz_write_params", "spz_read_losses", "spz_debug_read", "spz_last_error"]
+
+
+class SpzError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("spz error %d: %s" % (code, msg))
+        self.code = code
+
+
+class Hparams(ctypes.Structure):
+    _fields_ = [("algo", ctypes.c_int32), ("gemm_prec", ctypes.c_int32), ("capacity", ctypes.c_int64),
+                ("gamma", ctypes.c_float), ("tau", ctypes.c_float), ("lr_actor", ctypes.c_float),
+                ("lr_critic", ctypes.c_float), ("lr_alpha", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps", ctypes.c_float), ("alpha_init", ctypes.c_float),
+                ("learn_alpha", ctypes.c_int32), ("target_entropy", ctypes.c_float),
+                ("log_std_min", ctypes.c_float), ("log_std_max", ctypes.c_float),
+                ("policy_noise", ctypes.c_float), ("noise_clip", ctypes.c_float),
+                ("policy_delay", ctypes.c_int32), ("device", ctypes.c_int32), ("n_streams", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libspz.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError("libspz.so not built (run paper_2312_06126_amd/build.py or __graft_entry__.build())")
+    lib = ctypes.CDLL(path)
+    P, fp = ctypes.c_void_p, ctypes.POINTER(ctypes.c_float)
+    sig = {
+        "spz_hparams_default": (None, [ctypes.POINTER(Hparams)]),
+        "spz_create": (P, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                           ctypes.c_int32, ctypes.POINTER(Hparams), ctypes.c_uint64]),
+        "spz_destroy": (None, [P]),
+        "spz_buffer_push": (ctypes.c_int, [P, fp, fp, fp, fp, fp, ctypes.c_int64]),
+        "spz_buffer_size": (ctypes.c_int64, [P]),
+        "spz_update": (ctypes.c_int, [P, ctypes.c_int32, P]),
+        "spz_synchronize": (ctypes.c_int, [P]),
+        "spz_step": (ctypes.c_int64, [P]),
+        "spz_set_step": (ctypes.c_int, [P, ctypes.c_int64]),
+        "spz_param_count": (ctypes.c_int64, [P, ctypes.c_int32]),
+        "spz_read_params": (ctypes.c_int, [P, ctypes.c_int32, fp, ctypes.c_int64]),
+        "spz_write_params": (ctypes.c_int, [P, ctypes.c_int32, fp, ctypes.c_int64]),
+        "spz_read_losses": (ctypes.c_int, [P, fp, ctypes.c_int64, ctypes.c_int32]),
+        "spz_debug_read": (ctypes.c_int, [P, ctypes.c_int32, P, ctypes.c_int64]),
+        "spz_last_error": (ctypes.c_char_p, [P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def default_hparams() -> Hparams:
+    hp = Hparams()
+    load().spz_hparams_default(ctypes.byref(hp))
+    return hp
+
+
+def make_hparams(d: dict, device: int = 0, n_streams: int = 2) -> Hparams:
+    hp = default_hparams()
+    for k, v in d.items():
+        if k == "algo":
+            v = ALGOS[v]
+        elif k == "gemm_prec":
+            v = PRECS[v]
+        elif k == "learn_alpha":
+            v = int(bool(v))
+        setattr(hp, k, v)
+    hp.device = device
+    hp.n_streams = n_streams
+    return hp
+
+
+def _fptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None or isinstance(stream, int):
+        return stream
+    return int(stream.cuda_stream)   # torch.cuda.Stream
+
+
+class Spz:
+    """One learner context (spz_create ... spz_destroy)."""
+
+    def __init__(self, obs_dim: int, act_dim: int, hidden, batch: int, hp: dict, seed: int,
+                 device: int = 0, n_streams: int = 2):
+        self.lib = load()
+        self.obs_dim, self.act_dim, self.batch = obs_dim, act_dim, batch
+        h = (ctypes.c_int32 * len(hidden))(*hidden)
+        self.hp = make_hparams(hp, device, n_streams)
+        self.ctx = self.lib.spz_create(obs_dim, act_dim, h, len(hidden), batch, ctypes.byref(self.hp), seed)
+        if not self.ctx:
+            raise SpzError(SPZ_EINVAL, self.lib.spz_last_error(None).decode())
+
+    def _check(self, rc: int):
+        if rc != SPZ_OK:
+            raise SpzError(rc, self.lib.spz_last_error(self.ctx).decode())
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            self.lib.spz_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- calls with the C names ------------------------------------------------------
+    def buffer_push(self, obs, act, rew, done, next_obs):
+        arrs = [np.ascontiguousarray(x, dtype=np.float32) for x in (obs, act, rew, done, next_obs)]
+        n = arrs[2].shape[0]
+        assert arrs[0].shape == (n, self.obs_dim) and arrs[4].shape == (n, self.obs_dim)
+        assert arrs[1].shape == (n, self.act_dim) and arrs[3].shape == (n,)
+        self._check(self.lib.spz_buffer_push(self.ctx, *map(_fptr, arrs), n))
+
+    def buffer_size(self) -> int:
+        return int(self.lib.spz_buffer_size(self.ctx))
+
+    def update(self, n_steps: int, stream=None):
+        self._check(self.lib.spz_update(self.ctx, int(n_steps), _stream_handle(stream)))
+
+    def synchronize(self):
+        self._check(self.lib.spz_synchronize(self.ctx))
+
+    def step(self) -> int:
+        return int(self.lib.spz_step(self.ctx))
+
+    def set_step(self, step: int):
+        self._check(self.lib.spz_set_step(self.ctx, int(step)))
+
+    def param_count(self, which: str) -> int:
+        n = int(self.lib.spz_param_count(self.ctx, SELECTORS[which]))
+        if n < 0:
+            raise SpzError(n, "bad selector %s" % which)
+        return n
+
+    def read_params(self, which: str) -> np.ndarray:
+        out = np.empty(self.param_count(which), np.float32)
+        self._check(self.lib.spz_read_params(self.ctx, SELECTORS[which], _fptr(out), out.size))
+        return out
+
+    def write_params(self, which: str, values):
+        a = np.ascontiguousarray(values, dtype=np.float32)
+        self._check(self.lib.spz_write_params(self.ctx, SELECTORS[which], _fptr(a), a.size))
+
+    def read_losses(self, first_step: int, n: int) -> np.ndarray:
+        out = np.empty((n, REC_WIDTH), np.float32)
+        self._check(self.lib.spz_read_losses(self.ctx, _fptr(out), int(first_step), int(n)))
+        return out
+
+    def debug_indices(self) -> np.ndarray:
+        out = np.empty(self.batch, np.int32)
+        self._check(self.lib.spz_debug_read(self.ctx, DBG_INDICES, out.ctypes.data_as(ctypes.c_void_p),
+                                            out.nbytes))
+        return out

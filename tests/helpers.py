@@ -1,0 +1,91 @@
+"""Shared set-up for parity tests: one workload, the HIP learner and the oracle on
+the same seeded inputs (synthetic rows from `synth`, library seed, data seed)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import synth
+from oracle import Oracle
+
+NET_KEYS = ("actor", "critic1", "critic2")
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def fill_rows(w, n_rows, data_seed, sinks, chunk=1 << 18):
+    """Push rows 0..n_rows-1 of the synthetic stream into every sink (in order)."""
+    for r0 in range(0, n_rows, chunk):
+        rows = synth.workload_rows(w, r0, min(chunk, n_rows - r0), data_seed)
+        for push in sinks:
+            push(*rows)
+
+
+def make_oracle(w, seed=1, data_seed=0, virtual_rows=None):
+    hp = w.hparams()
+    if virtual_rows is not None:
+        o = Oracle(w.obs_dim, w.act_dim, w.hidden, w.batch, hp, seed,
+                   row_source=lambda idx: synth.workload_rows_at(w, idx, data_seed))
+        o.set_virtual_size(virtual_rows)
+        return o
+    return Oracle(w.obs_dim, w.act_dim, w.hidden, w.batch, hp, seed)
+
+
+def make_gpu(w, seed=1, n_streams=2):
+    from paper_2312_06126_amd import Spz
+    return Spz(w.obs_dim, w.act_dim, w.hidden, w.batch, w.hparams(), seed, n_streams=n_streams)
+
+
+def make_pair(w, n_rows, seed=1, data_seed=0, n_streams=2, virtual=False):
+    g = make_gpu(w, seed, n_streams)
+    if virtual:
+        o = make_oracle(w, seed, data_seed, virtual_rows=n_rows)
+        fill_rows(w, n_rows, data_seed, [g.buffer_push])
+    else:
+        o = make_oracle(w, seed, data_seed)
+        fill_rows(w, n_rows, data_seed, [g.buffer_push, o.push])
+    return g, o
+
+
+def state_keys(algo):
+    keys = ["actor", "critic1", "critic2", "tcritic1", "tcritic2", "log_alpha"]
+    if algo == "td3":
+        keys.append("tactor")
+    keys += ["m_actor", "m_critic1", "m_critic2", "m_log_alpha", "v_actor", "v_critic1", "v_critic2",
+             "v_log_alpha"]
+    return keys
+
+
+def teacher_force(o, g):
+    """Round the oracle's state to float32, keep that in the oracle, and write it to the GPU."""
+    for k in state_keys(o.algo):
+        v = o.params(k).astype(np.float32)
+        o.set_params(k, v.astype(np.float64))
+        g.write_params(k, v)
+    g.set_step(o.t)
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
+
+
+def oracle_grad_flat(o, key):
+    gr = o.last_grads[key]
+    return np.concatenate([np.concatenate([gw.ravel(), gb.ravel()]) for gw, gb in gr])
+
+
+def per_tensor_rel(o, key, flat_gpu, flat_ref):
+    """Largest per-tensor relative L2 difference over the W and b tensors of one net."""
+    worst = 0.0
+    off = 0
+    for fi, fo in o.dims(key):
+        for n in (fi * fo, fo):
+            worst = max(worst, rel(flat_gpu[off:off + n], flat_ref[off:off + n]))
+            off += n
+    return worst
