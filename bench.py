@@ -1,0 +1,196 @@
+#!/usr/bin/env python3
+"""Update-throughput benchmark of the actor-critic learner on one MI355X.
+
+Metric: update frames/s = batch rows fully processed per second, i.e. update
+steps per second times the batch size (the paper's "network update frame rate",
+Section 4.2, Tables 2 and 3). One step is the whole update: replay gather,
+target action, target and online twin critics, critic loss and backward,
+actor forward/backward through the critics, temperature, Adam and Polyak.
+
+Default workload: the large-batch SAC case (obs 376, act 17, 3x1024 ReLU MLPs,
+batch 131072, 4M-row ring, bf16 GEMM operands with fp32 accumulation and fp32
+master weights / Adam). The ring is filled with synthetic rows before timing and
+stays resident in HBM; nothing is transferred from the host in the timed region.
+
+Prints one JSON line (rank 0). Also reports the dominant kernel against its
+roofline (per-launch event timings taken by the library on the stream each
+kernel runs on, during the timed region) and the CPU oracle's rate on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "actor-critic update frames/sec (batch rows/s) at 1 MI355X; MFMA util %"
+PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense matrix peaks
+PEAK_HBM_GBS = 8000.0
+GEMMS = ("gemm_fwd", "gemm_dgrad", "gemm_wgrad")
+
+
+def progress(msg: str):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def frames_per_second(batch: int, steps: int, seconds: float) -> float:
+    """Update frame rate = update frequency x batch size (rows per second)."""
+    return batch * steps / seconds
+
+
+def fill_ring(g, w, data_seed: int, rows: int):
+    import synth
+    chunk = 1 << 18
+    t0 = time.time()
+    for r0 in range(0, rows, chunk):
+        n = min(chunk, rows - r0)
+        g.buffer_push(*synth.workload_rows(w, r0, n, data_seed))
+        if (r0 // chunk) % 4 == 3 or r0 + n >= rows:
+            progress("ring %d / %d rows (%.1fs)" % (r0 + n, rows, time.time() - t0))
+
+
+def roofline(stats, prec: str):
+    """The dominant kernel (largest total time) against its MI355X roofline."""
+    top = stats[0]
+    avg_s = top["avg_ms"] / 1e3
+    if top["name"] in GEMMS:
+        achieved = top["flops"] / avg_s / 1e12
+        peak = PEAK_TFLOPS[prec]
+        r = dict(bound="mfma", achieved=round(achieved, 2), peak=peak, unit="TFLOP/s")
+    else:
+        achieved = top["bytes"] / avg_s / 1e9
+        peak = PEAK_HBM_GBS
+        r = dict(bound="hbm", achieved=round(achieved, 1), peak=peak, unit="GB/s")
+    r["frac"] = round(achieved / peak, 4)
+    r["traffic"] = None
+    r["kernel"] = "%s M=%d N=%d K=%d" % (top["name"], top["M"], top["N"], top["K"])
+    r["avg_launch_ms"] = round(top["avg_ms"], 5)
+    r["launches"] = top["launches"]
+    r["per_launch"] = top["flops"] if top["name"] in GEMMS else top["bytes"]
+    return r
+
+
+def cpu_baseline(w, seed: int, data_seed: int, sample_batch: int):
+    import numpy as np  # noqa: F401
+    import synth
+    from oracle import Oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    ws = w.replace(batch=sample_batch)
+    o = Oracle(ws.obs_dim, ws.act_dim, ws.hidden, ws.batch, ws.hparams(), seed,
+               row_source=lambda idx: synth.workload_rows_at(ws, idx, data_seed))
+    o.set_virtual_size(ws.capacity)
+    t0 = time.perf_counter()
+    o.update(1)
+    dt = time.perf_counter() - t0
+    return dict(value=round(sample_batch / dt, 1), unit="rows/s", cores=threads, kind="oracle",
+                sample="1 update step of %s at batch %d (full widths, %s operand emulation), %.1f s" %
+                       (w.name, sample_batch, w.prec, dt))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's)")
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="sac_large_bf16")
+    ap.add_argument("--batch", type=int, default=None, help="override the workload batch")
+    ap.add_argument("--streams", type=int, default=2, choices=(1, 2))
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--data-seed", type=int, default=0)
+    ap.add_argument("--cpu-sample-batch", type=int, default=16384)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    if int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs as a single process on one GPU", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2312_06126_amd import Spz
+
+    w = synth.workload(args.workload)
+    if args.batch:
+        w = w.replace(batch=args.batch)
+    steps = args.steps if args.steps is not None else w.steps
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+
+    progress("workload %s batch %d ring %d prec %s streams %d" % (w.name, w.batch, w.capacity, w.prec,
+                                                                  args.streams))
+    g = Spz(w.obs_dim, w.act_dim, w.hidden, w.batch, w.hparams(), args.seed, n_streams=args.streams)
+    fill_ring(g, w, args.data_seed, w.capacity)
+
+    g.update(args.warmup, stream)
+    g.synchronize()
+    torch.cuda.synchronize()
+    progress("warmup %d steps done" % args.warmup)
+
+    if not args.no_profile:
+        g.profile_enable(True, reserve_launches=120 * steps)
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    g.update(steps, stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    g.synchronize()
+    elapsed_ms = t_start.elapsed_time(t_end)
+    progress("timed %d steps: %.3f ms/step" % (steps, elapsed_ms / steps))
+
+    stats = g.profile_read() if not args.no_profile else []
+    rec = g.read_losses(g.step() - steps + 1, steps)
+    finite = bool((rec[:, 6] == 0).all())
+    g.close()
+
+    value = frames_per_second(w.batch, steps, elapsed_ms / 1e3)
+    prec = w.prec
+    out = dict(metric=METRIC, value=round(value, 1), unit="rows/s", n_gpus=1, steps=steps, warmup=args.warmup,
+               ms_per_step=round(elapsed_ms / steps, 4), higher_is_better=True, scaling="weak",
+               vs_baseline=None, dtype=prec, data="synthetic",
+               config=dict(workload=w.name, algo=w.algo, global_batch=w.batch, obs_dim=w.obs_dim,
+                           act_dim=w.act_dim, hidden=list(w.hidden), replay_rows=w.capacity,
+                           gemm_operands=prec, accumulate="fp32", master_weights="fp32",
+                           streams=args.streams, seed=args.seed, data_seed=args.data_seed,
+                           parallelism="single GPU; actor and critic on concurrent streams"),
+               losses_finite=finite)
+    if stats:
+        gemm_ms = sum(s["total_ms"] for s in stats if s["name"] in GEMMS)
+        gemm_flops = sum(s["flops"] * s["launches"] for s in stats if s["name"] in GEMMS)
+        peak = PEAK_TFLOPS[prec] * 1e12
+        out["mfma_util"] = dict(
+            gemm_kernels=round(gemm_flops / (gemm_ms / 1e3) / peak, 4) if gemm_ms else None,
+            whole_step=round(gemm_flops / (elapsed_ms / 1e3) / peak, 4),
+            gemm_flops_per_step=gemm_flops / steps, peak_tflops=PEAK_TFLOPS[prec],
+            note="gemm_kernels: GEMM flops / summed GEMM kernel time (events; concurrent streams overlap)")
+        out["roofline"] = roofline(stats, prec)
+        out["kernels"] = [dict(name=s["name"], M=s["M"], N=s["N"], K=s["K"], launches=s["launches"],
+                               avg_ms=round(s["avg_ms"], 5), total_ms=round(s["total_ms"], 3))
+                          for s in stats[:12]]
+    if not args.no_cpu_baseline:
+        progress("cpu baseline (oracle) at batch %d" % args.cpu_sample_batch)
+        out["cpu_baseline"] = cpu_baseline(w, args.seed, args.data_seed, args.cpu_sample_batch)
+        out["cpu_baseline"]["cpu"] = platform.processor() or platform.machine()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -178,6 +178,30 @@ int spz_read_losses(spz_ctx* ctx, float* out, int64_t first_step, int32_t n);
  * must equal the object's size (SPZ_ESIZE otherwise). Waits first. */
 int spz_debug_read(spz_ctx* ctx, int32_t what, void* out, int64_t bytes);
 
+/* Kernel timing (measurement). While enabled, every kernel launch of
+ * spz_update is bracketed by a pair of HIP events recorded on the stream the
+ * kernel runs on; spz_profile_read aggregates them per kernel shape. Enabling
+ * pre-creates events for `reserve_launches` launches (more are created on
+ * demand); disabling drops the records. Waits for the context's work first. */
+int spz_profile_enable(spz_ctx* ctx, int32_t on, int64_t reserve_launches);
+
+/* One aggregated kernel shape. flops / bytes are the algorithmic work of one
+ * launch (2*M*N*K for matrix products; bytes the kernel must move for the
+ * memory-bound kernels, 0 when not meaningful). */
+typedef struct spz_kernel_stat {
+  char name[32];   /* kernel family, e.g. "gemm_fwd", "gather", "adam_polyak" */
+  int32_t M, N, K; /* launch shape (0 where not applicable)                   */
+  int32_t bf16;    /* operand precision of a matrix product                   */
+  int64_t launches;
+  double total_ms; /* sum of event-measured durations                         */
+  double flops;    /* per launch                                              */
+  double bytes;    /* per launch                                              */
+} spz_kernel_stat;
+
+/* Copy up to max aggregated records (sorted by total time, largest first)
+ * into out and their count into *n_out; waits for the context's work first. */
+int spz_profile_read(spz_ctx* ctx, spz_kernel_stat* out, int32_t max, int32_t* n_out);
+
 /* Message of the last failure: of ctx, or of the calling thread when ctx is
  * NULL. Never NULL; empty when there was none. Valid until the next call. */
 const char* spz_last_error(const spz_ctx* ctx);

@@ -22,6 +22,7 @@
 //   actor stream:  actor forward on s, critics on (s, a~), actor loss, critic
 //                  input-gradient to the action, head backward, actor backward
 //   s0: join -> finish (loss record, temperature gradient, step counter) -> Adam + Polyak
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -102,6 +103,13 @@ struct spz_ctx {
   hipStream_t last = nullptr;
   std::vector<void*> scratch;   // ping-pong view of cs_h, one entry per hidden layer
   std::vector<void*> allocs;
+  // kernel timing
+  struct ProfKey { std::string name; int M, N, K; double flops, bytes; int64_t launches; double ms; };
+  struct ProfEv { int key; hipEvent_t a, b; };
+  bool prof = false;
+  std::vector<ProfKey> pkeys;
+  std::vector<ProfEv> pevs;
+  std::vector<hipEvent_t> pool;
   std::string err;
 };
 
@@ -143,6 +151,38 @@ hipError_t dalloc_t(spz_ctx* c, P** p, size_t bytes) {
   hipError_t e = dalloc(c, &v, bytes);
   *p = static_cast<P*>(v);
   return e;
+}
+
+// ---------------------------------------------------------------------------------- timing
+int prof_key(spz_ctx* c, const char* name, int M, int N, int K, double flops, double bytes) {
+  for (size_t i = 0; i < c->pkeys.size(); ++i) {
+    const auto& k = c->pkeys[i];
+    if (k.M == M && k.N == N && k.K == K && k.name == name) return (int)i;
+  }
+  c->pkeys.push_back({name, M, N, K, flops, bytes, 0, 0.0});
+  return (int)c->pkeys.size() - 1;
+}
+
+hipError_t prof_take(spz_ctx* c, hipEvent_t* e) {
+  if (c->pool.empty()) return hipEventCreate(e);
+  *e = c->pool.back();
+  c->pool.pop_back();
+  return hipSuccess;
+}
+
+// Run one launch; while timing is enabled, bracket it with events on its stream.
+template <class F>
+hipError_t timed(spz_ctx* c, const char* name, int M, int N, int K, double flops, double bytes, hipStream_t s,
+                 F&& f) {
+  if (!c->prof) return f();
+  hipEvent_t a, b;
+  HK(prof_take(c, &a));
+  HK(prof_take(c, &b));
+  HK(hipEventRecord(a, s));
+  HK(f());
+  HK(hipEventRecord(b, s));
+  c->pevs.push_back({prof_key(c, name, M, N, K, flops, bytes), a, b});
+  return hipSuccess;
 }
 
 // Flat (unpadded) column i of layer l of net ni -> padded column.
@@ -241,7 +281,8 @@ hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, 
     const Lay& L = n.L[l];
     if (l == nl - 1 && ni != 0) {
       RowdotArgs r{in, ld, L.in_p, c->Bp, wop(c, target, L.w), wf(c, target, L.b), head};
-      return launch_rowdot(c->bf16, r, s);
+      return timed(c, "rowdot", c->Bp, 1, L.in_p, 2.0 * c->Bp * L.in_p,
+                   (double)c->Bp * L.in_p * es(c) + 4.0 * c->Bp, s, [&] { return launch_rowdot(c->bf16, r, s); });
     }
     GemmArgs g{};
     g.A = in; g.lda = ld;
@@ -253,7 +294,8 @@ hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, 
     } else {
       g.C = hid[l]; g.ldc = L.out_p; g.relu = 1; g.out_f32 = 0;
     }
-    HK(gemm(c->bf16, GEMM_FWD, g, s));
+    HK(timed(c, "gemm_fwd", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
+             [&] { return gemm(c->bf16, GEMM_FWD, g, s); }));
     in = g.C;
     ld = L.out_p;
   }
@@ -268,10 +310,13 @@ hipError_t wgrad(spz_ctx* c, const void* dz, int64_t lddz, const void* X, int64_
   g.M = L.out_p; g.N = L.in_p; g.K = c->Bp;
   g.splits = wgrad_splits(g.M, g.N, g.K);
   g.C = part; g.ldc = L.in_p;
-  HK(gemm(c->bf16, GEMM_WGRAD, g, s));
-  HK(splitk_reduce(part, g.splits, g.M, g.N, g.ldc, c->G + L.w, L.in_p, s));
+  HK(timed(c, "gemm_wgrad", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
+           [&] { return gemm(c->bf16, GEMM_WGRAD, g, s); }));
+  HK(timed(c, "splitk_reduce", g.M, g.N, g.splits, 0.0, 4.0 * g.M * g.N * (g.splits + 1), s,
+           [&] { return splitk_reduce(part, g.splits, g.M, g.N, g.ldc, c->G + L.w, L.in_p, s); }));
   ColsumArgs cs{dz, lddz, L.out_p, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart};
-  return launch_colsum(c->bf16, cs, c->G + L.b, nullptr, s);
+  return timed(c, "colsum", c->Bp, L.out_p, 0, 0.0, (double)c->Bp * L.out_p * es(c), s,
+               [&] { return launch_colsum(c->bf16, cs, c->G + L.b, nullptr, s); });
 }
 
 hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_t ldw, int N,
@@ -282,7 +327,8 @@ hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_
   g.C = out; g.ldc = ldo; g.out_f32 = out_f32 ? 1 : 0;
   g.mask = mask; g.ldm = ldo;
   g.M = c->Bp; g.N = N; g.K = L.out_p;
-  return gemm(c->bf16, GEMM_DGRAD, g, s);
+  return timed(c, "gemm_dgrad", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
+               [&] { return gemm(c->bf16, GEMM_DGRAD, g, s); });
 }
 
 // Critic ni in {1, 2}: weight and bias gradients of L = sum_b dq[b] q[b] given the
@@ -293,9 +339,11 @@ hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, v
   const int nl = (int)n.L.size();
   const Lay& H = n.L[nl - 1];
   ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, c->c_cpart};
-  HK(launch_colsum(c->bf16, cs, c->G + H.w, c->G + H.b, s));
+  HK(timed(c, "colsum", c->Bp, H.in_p, 1, 0.0, (double)c->Bp * H.in_p * es(c), s,
+           [&] { return launch_colsum(c->bf16, cs, c->G + H.w, c->G + H.b, s); }));
   HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp};
-  HK(launch_head_bwd(c->bf16, hb, s));
+  HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, 2.0 * c->Bp * H.in_p * es(c), s,
+           [&] { return launch_head_bwd(c->bf16, hb, s); }));
   int cur = 0;
   for (int l = nl - 2; l >= 0; --l) {
     const Lay& L = n.L[l];
@@ -318,7 +366,8 @@ hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* 
   const int nl = (int)n.L.size();
   const Lay& H = n.L[nl - 1];
   HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->a_dz[0], H.in_p, H.in_p, c->Bp};
-  HK(launch_head_bwd(c->bf16, hb, s));
+  HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, 2.0 * c->Bp * H.in_p * es(c), s,
+           [&] { return launch_head_bwd(c->bf16, hb, s); }));
   int cur = 0;
   for (int l = nl - 2; l >= 1; --l) {
     const Lay& L = n.L[l];
@@ -361,22 +410,22 @@ hipError_t critic_part(spz_ctx* c, hipStream_t s) {
     HK(forward(c, 0, false, c->xs2, c->Kc, c->scratch.data(), c->z2, s));
     SacHeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_TGT, hp.log_std_min, hp.log_std_max,
                   c->xs2, c->Kc, c->Ka, c->logp2, nullptr, nullptr, nullptr};
-    HK(launch_sac_head(c->bf16, h, s));
+    HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, h, s); }));
   } else {
     HK(forward(c, 0, true, c->xs2, c->Kc, c->scratch.data(), c->z2, s));
     Td3HeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, 1, hp.policy_noise, hp.noise_clip,
                   c->xs2, c->Kc, c->Ka, nullptr};
-    HK(launch_td3_head(c->bf16, h, s));
+    HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
   HK(forward(c, 1, true, c->xs2, c->Kc, c->scratch.data(), c->qt1, s));
   HK(forward(c, 2, true, c->xs2, c->Kc, c->scratch.data(), c->qt2, s));
   TdArgs td{c->qt1, c->qt2, c->r, c->d, c->td3 ? nullptr : c->logp2, log_alpha_ptr(c), c->y, hp.gamma,
             c->B, c->Bp};
-  HK(launch_td_target(td, s));
+  HK(timed(c, "td_target", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_td_target(td, s); }));
   HK(forward(c, 1, false, c->xsa, c->Kc, c->hc[0].data(), c->q1, s));
   HK(forward(c, 2, false, c->xsa, c->Kc, c->hc[1].data(), c->q2, s));
   CriticLossArgs cl{c->q1, c->q2, c->y, c->dq1, c->dq2, c->c_lpart, c->B, c->Bp};
-  HK(launch_critic_loss(cl, s));
+  HK(timed(c, "critic_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_critic_loss(cl, s); }));
   HK(critic_backward(c, 1, c->dq1, c->xsa, c->hc[0].data(), s));
   HK(critic_backward(c, 2, c->dq2, c->xsa, c->hc[1].data(), s));
   return hipSuccess;
@@ -391,21 +440,21 @@ hipError_t actor_part(spz_ctx* c, hipStream_t s) {
   if (!c->td3) {
     SacHeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_POL, hp.log_std_min, hp.log_std_max,
                   c->xsp, c->Kc, c->Ka, c->logp, c->th, c->se, c->lm};
-    HK(launch_sac_head(c->bf16, h, s));
+    HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, h, s); }));
   } else {
     Td3HeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, 0, 0.0f, 0.0f, c->xsp, c->Kc, c->Ka, c->th};
-    HK(launch_td3_head(c->bf16, h, s));
+    HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
   HK(forward(c, 1, false, c->xsp, c->Kc, c->hpc[0].data(), c->qp1, s));
   if (!c->td3) HK(forward(c, 2, false, c->xsp, c->Kc, c->hpc[1].data(), c->qp2, s));
   ActorLossArgs al{c->qp1, c->td3 ? nullptr : c->qp2, c->logp, log_alpha_ptr(c), c->dqp1,
                    c->td3 ? nullptr : c->dqp2, c->a_lpart, c->B, c->Bp};
-  HK(launch_actor_loss(al, s));
+  HK(timed(c, "actor_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_actor_loss(al, s); }));
   HK(critic_action_grad(c, 1, c->dqp1, c->hpc[0].data(), c->da1, s));
   if (!c->td3) HK(critic_action_grad(c, 2, c->dqp2, c->hpc[1].data(), c->da2, s));
   ActorHeadBwdArgs hb{c->da1, c->td3 ? nullptr : c->da2, c->Ap, c->th, c->se, c->lm, log_alpha_ptr(c),
                       c->dzh, pa, c->A, c->B, c->td3 ? 0 : 1};
-  HK(launch_actor_head_bwd(c->bf16, hb, s));
+  HK(timed(c, "actor_head_bwd", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_actor_head_bwd(c->bf16, hb, s); }));
   return actor_backward(c, s);
 }
 
@@ -414,7 +463,11 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
   const bool actor_step = !c->td3 || (t % c->hp.policy_delay == 0);
   GatherArgs g{c->buf, c->row_bytes, c->off_a, c->off_s2, c->off_r, c->off_d, c->O, c->A, c->Ka, c->Kc,
                c->B, c->seed, (uint32_t)c->size, c->d_step, c->xsa, c->xs2, c->xsp, c->r, c->d, c->idx};
-  CK(launch_gather(c->bf16, g, s0));
+  {
+    const double e = (double)es(c);
+    const double bytes = (double)c->B * ((2.0 * c->O + c->A) * e + 8.0 + (3.0 * c->O + c->A) * e + 12.0);
+    CK(timed(c, "gather", c->B, c->O, c->A, 0.0, bytes, s0, [&] { return launch_gather(c->bf16, g, s0); }));
+  }
   hipStream_t sc = s0, sa = s0;
   const bool two = c->hp.n_streams == 2;
   if (two) {
@@ -437,7 +490,7 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
   FinishArgs f{c->c_lpart, c->a_lpart, loss_blocks(c->Bp), loss_blocks(c->Bp), c->B, c->td3 ? 0 : 1,
                actor_step ? 1 : 0, c->hp.learn_alpha, c->hp.target_entropy, log_alpha_ptr(c),
                c->td3 ? nullptr : c->G + c->la, c->rec, c->rec_cap, c->d_step};
-  CK(launch_finish(f, s0));
+  CK(timed(c, "finish", 0, 0, 0, 0.0, 0.0, s0, [&] { return launch_finish(f, s0); }));
   const Net& an = c->net[0];
   AdamArgs a{};
   a.P = c->P; a.M = c->M; a.V = c->V; a.T = c->T; a.G = c->G; a.Pb = c->Pb; a.Tb = c->Tb;
@@ -454,7 +507,14 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
   a.lr_a = c->hp.lr_actor; a.lr_c = c->hp.lr_critic; a.lr_al = c->hp.lr_alpha;
   a.b1 = c->hp.beta1; a.b2 = c->hp.beta2; a.eps = c->hp.eps; a.tau = c->hp.tau;
   a.step = c->d_step;
-  CK(launch_adam(a, s0));
+  {
+    const double n_adam = (double)(c->net[2].end - c->net[1].off) + (actor_step ? (double)(an.end - an.off) : 0.0) +
+                          (a.do_alpha ? 1.0 : 0.0);
+    const double n_pol = (a.polyak_critic ? (double)(c->net[2].end - c->net[1].off) : 0.0) +
+                         (a.polyak_actor ? (double)(an.end - an.off) : 0.0);
+    const double bytes = 28.0 * n_adam + 8.0 * n_pol + (c->bf16 ? 2.0 * (n_adam + n_pol) : 0.0);
+    CK(timed(c, "adam_polyak", (int)c->n_arena, 0, actor_step ? 1 : 0, 0.0, bytes, s0, [&] { return launch_adam(a, s0); }));
+  }
   c->h_step = t;
   return SPZ_OK;
 }
@@ -571,6 +631,11 @@ void release(spz_ctx* c) {
   if (c->last) (void)hipStreamSynchronize(c->last);
   for (void* p : c->allocs) (void)hipFree(p);
   if (c->stage) (void)hipFree(c->stage);
+  for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
+  for (auto& pe : c->pevs) {
+    (void)hipEventDestroy(pe.a);
+    (void)hipEventDestroy(pe.b);
+  }
   if (c->ev_fork) (void)hipEventDestroy(c->ev_fork);
   if (c->ev_c) (void)hipEventDestroy(c->ev_c);
   if (c->ev_a) (void)hipEventDestroy(c->ev_a);
@@ -859,6 +924,67 @@ int spz_debug_read(spz_ctx* c, int32_t what, void* out, int64_t bytes) {
   int rc = ctx_sync(c);
   if (rc) return rc;
   CK(hipMemcpy(out, c->idx, (size_t)bytes, hipMemcpyDeviceToHost));
+  return SPZ_OK;
+}
+
+int spz_profile_enable(spz_ctx* c, int32_t on, int64_t reserve_launches) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_profile_enable: NULL context");
+  if (reserve_launches < 0) return set_err(c, SPZ_EINVAL, "spz_profile_enable: reserve < 0");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  for (auto& pe : c->pevs) {
+    c->pool.push_back(pe.a);
+    c->pool.push_back(pe.b);
+  }
+  c->pevs.clear();
+  c->pkeys.clear();
+  c->prof = on != 0;
+  if (c->prof) {
+    while ((int64_t)c->pool.size() < 2 * reserve_launches) {
+      hipEvent_t e;
+      CK(hipEventCreate(&e));
+      c->pool.push_back(e);
+    }
+    c->pevs.reserve((size_t)reserve_launches);
+  }
+  return SPZ_OK;
+}
+
+int spz_profile_read(spz_ctx* c, spz_kernel_stat* out, int32_t max, int32_t* n_out) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_profile_read: NULL context");
+  if (max < 0 || (max > 0 && !out) || !n_out) return set_err(c, SPZ_EINVAL, "spz_profile_read: bad output");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  for (auto& pe : c->pevs) {
+    float ms = 0.0f;
+    CK(hipEventElapsedTime(&ms, pe.a, pe.b));
+    c->pkeys[pe.key].ms += ms;
+    c->pkeys[pe.key].launches += 1;
+    c->pool.push_back(pe.a);
+    c->pool.push_back(pe.b);
+  }
+  c->pevs.clear();
+  std::vector<int> order(c->pkeys.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
+  std::sort(order.begin(), order.end(), [&](int a, int b) { return c->pkeys[a].ms > c->pkeys[b].ms; });
+  const int n = std::min<int>(max, (int)order.size());
+  for (int i = 0; i < n; ++i) {
+    const auto& k = c->pkeys[order[i]];
+    spz_kernel_stat& o = out[i];
+    std::memset(&o, 0, sizeof(o));
+    std::snprintf(o.name, sizeof(o.name), "%s", k.name.c_str());
+    o.M = k.M;
+    o.N = k.N;
+    o.K = k.K;
+    o.bf16 = c->bf16 ? 1 : 0;
+    o.launches = k.launches;
+    o.total_ms = k.ms;
+    o.flops = k.flops;
+    o.bytes = k.bytes;
+  }
+  *n_out = (int32_t)order.size();
   return SPZ_OK;
 }
 

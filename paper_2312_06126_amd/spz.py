@@ -26,7 +26,8 @@ DBG_INDICES = 0
 REC_WIDTH = 8
 EXPORTS = ["spz_hparams_default", "spz_create", "spz_destroy", "spz_buffer_push", "spz_buffer_size",
            "spz_update", "spz_synchronize", "spz_step", "spz_set_step", "spz_param_count",
-           "spz_read_params", "spz_write_params", "spz_read_losses", "spz_debug_read", "spz_last_error"]
+           "spz_read_params", "spz_write_params", "spz_read_losses", "spz_debug_read", "spz_last_error",
+           "spz_profile_enable", "spz_profile_read"]
 
 
 class SpzError(RuntimeError):
@@ -44,6 +45,12 @@ class Hparams(ctypes.Structure):
                 ("log_std_min", ctypes.c_float), ("log_std_max", ctypes.c_float),
                 ("policy_noise", ctypes.c_float), ("noise_clip", ctypes.c_float),
                 ("policy_delay", ctypes.c_int32), ("device", ctypes.c_int32), ("n_streams", ctypes.c_int32)]
+
+
+class KernelStat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("M", ctypes.c_int32), ("N", ctypes.c_int32),
+                ("K", ctypes.c_int32), ("bf16", ctypes.c_int32), ("launches", ctypes.c_int64),
+                ("total_ms", ctypes.c_double), ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
 
 
 _lib = None
@@ -75,6 +82,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "spz_read_losses": (ctypes.c_int, [P, fp, ctypes.c_int64, ctypes.c_int32]),
         "spz_debug_read": (ctypes.c_int, [P, ctypes.c_int32, P, ctypes.c_int64]),
         "spz_last_error": (ctypes.c_char_p, [P]),
+        "spz_profile_enable": (ctypes.c_int, [P, ctypes.c_int32, ctypes.c_int64]),
+        "spz_profile_read": (ctypes.c_int, [P, ctypes.POINTER(KernelStat), ctypes.c_int32,
+                                            ctypes.POINTER(ctypes.c_int32)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -190,4 +200,19 @@ class Spz:
         out = np.empty(self.batch, np.int32)
         self._check(self.lib.spz_debug_read(self.ctx, DBG_INDICES, out.ctypes.data_as(ctypes.c_void_p),
                                             out.nbytes))
+        return out
+
+    def profile_enable(self, on: bool = True, reserve_launches: int = 0):
+        self._check(self.lib.spz_profile_enable(self.ctx, 1 if on else 0, int(reserve_launches)))
+
+    def profile_read(self, max_entries: int = 256):
+        """Aggregated kernel timings: list of dicts sorted by total time (largest first)."""
+        arr = (KernelStat * max_entries)()
+        n = ctypes.c_int32(0)
+        self._check(self.lib.spz_profile_read(self.ctx, arr, max_entries, ctypes.byref(n)))
+        out = []
+        for k in arr[:min(n.value, max_entries)]:
+            out.append(dict(name=k.name.decode(), M=k.M, N=k.N, K=k.K, bf16=k.bf16, launches=k.launches,
+                            total_ms=k.total_ms, flops=k.flops, bytes=k.bytes,
+                            avg_ms=k.total_ms / max(k.launches, 1)))
         return out

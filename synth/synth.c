@@ -13,8 +13,8 @@
  * Every value is a pure function of (seed, row, field, column), so any row can be
  * regenerated without materialising the buffer. The hash is the SplitMix64 output
  * mixer (Steele, Lea, Flood, "Fast splittable pseudorandom number generators",
- * OOPSLA 2014). Normals use the Box-Muller transform in double precision and are
- * rounded once to float.
+ * OOPSLA 2014). Normals use the Box-Muller transform in double precision (both
+ * outputs of one draw fill two adjacent columns) and are rounded once to float.
  *
  * This file holds input generation only: none of the update's arithmetic.
  */
@@ -39,27 +39,39 @@ static inline uint64_t draw(uint64_t seed, uint64_t row, uint32_t field, uint32_
   return mix64(h ^ (((uint64_t)field << 32) | col));
 }
 
-static inline float normal_from(uint64_t z) {
+/* Two independent N(0,1) values from one 64-bit draw (both Box-Muller outputs). */
+static inline void normal_pair(uint64_t z, float* c, float* s) {
   double u1 = ((double)(z >> 40) + 1.0) * 0x1p-24;            /* (0, 1] */
   double u2 = (double)((z >> 8) & 0xFFFFFFull) * 0x1p-24;      /* [0, 1) */
-  return (float)(sqrt(-2.0 * log(u1)) * cos(6.283185307179586 * u2));
+  double r = sqrt(-2.0 * log(u1)), a = 6.283185307179586 * u2;
+  *c = (float)(r * cos(a));
+  *s = (float)(r * sin(a));
 }
 
 static inline float uniform_pm1(uint64_t z) {
   return (float)((double)(z >> 40) * 0x1p-23 - 1.0);          /* [-1, 1) */
 }
 
+static void normals(uint64_t seed, int64_t row, uint32_t field, int32_t O, int32_t zero_mod,
+                    float* out) {
+  for (int32_t j = 0; j < O; j += 2) {
+    float c, s;
+    normal_pair(draw(seed, (uint64_t)row, field, (uint32_t)(j >> 1)), &c, &s);
+    out[j] = (zero_mod > 0 && j % zero_mod == 0) ? 0.0f : c;
+    if (j + 1 < O) out[j + 1] = (zero_mod > 0 && (j + 1) % zero_mod == 0) ? 0.0f : s;
+  }
+}
+
 static void one_row(uint64_t seed, int64_t row, int32_t O, int32_t A, int32_t zero_mod,
                     double p_done, float* obs, float* act, float* rew, float* done,
                     float* nobs) {
-  for (int32_t j = 0; j < O; ++j) {
-    int zero = zero_mod > 0 && (j % zero_mod) == 0;
-    obs[j] = zero ? 0.0f : normal_from(draw(seed, (uint64_t)row, FIELD_OBS, (uint32_t)j));
-    nobs[j] = zero ? 0.0f : normal_from(draw(seed, (uint64_t)row, FIELD_NOBS, (uint32_t)j));
-  }
+  normals(seed, row, FIELD_OBS, O, zero_mod, obs);
+  normals(seed, row, FIELD_NOBS, O, zero_mod, nobs);
   for (int32_t j = 0; j < A; ++j)
     act[j] = uniform_pm1(draw(seed, (uint64_t)row, FIELD_ACT, (uint32_t)j));
-  *rew = normal_from(draw(seed, (uint64_t)row, FIELD_REW, 0));
+  float r, unused;
+  normal_pair(draw(seed, (uint64_t)row, FIELD_REW, 0), &r, &unused);
+  *rew = r;
   uint64_t zd = draw(seed, (uint64_t)row, FIELD_DONE, 0);
   *done = ((double)(zd >> 11) * 0x1p-53) < p_done ? 1.0f : 0.0f;
 }
