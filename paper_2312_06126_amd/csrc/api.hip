@@ -86,7 +86,7 @@ struct spz_ctx {
   float *q1 = nullptr, *q2 = nullptr, *dq1 = nullptr, *dq2 = nullptr;
   std::vector<void*> hc[2];
   void* c_dz[2] = {nullptr, nullptr};
-  float *c_wpart = nullptr, *c_cpart = nullptr;
+  float *c_wpart = nullptr, *c_cpart = nullptr, *c_cextra = nullptr;
   double* c_lpart = nullptr;
   // actor-stream workspace
   std::vector<void*> ha;
@@ -302,33 +302,52 @@ hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, 
   return hipSuccess;
 }
 
+// Weight gradient of layer L (split-K over the batch, slices reduced in order) and,
+// when `bias`, its bias gradient as the column sums of dz.
 hipError_t wgrad(spz_ctx* c, const void* dz, int64_t lddz, const void* X, int64_t ldx, const Lay& L,
-                 float* part, float* cpart, hipStream_t s) {
+                 float* part, float* cpart, bool bias, hipStream_t s) {
   GemmArgs g{};
   g.A = dz; g.lda = lddz;
   g.B = X; g.ldb = ldx;
   g.M = L.out_p; g.N = L.in_p; g.K = c->Bp;
-  g.splits = wgrad_splits(g.M, g.N, g.K);
+  g.splits = wgrad_splits(c->bf16, g.M, g.N, g.K);
   g.C = part; g.ldc = L.in_p;
   HK(timed(c, "gemm_wgrad", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
            [&] { return gemm(c->bf16, GEMM_WGRAD, g, s); }));
   HK(timed(c, "splitk_reduce", g.M, g.N, g.splits, 0.0, 4.0 * g.M * g.N * (g.splits + 1), s,
            [&] { return splitk_reduce(part, g.splits, g.M, g.N, g.ldc, c->G + L.w, L.in_p, s); }));
-  ColsumArgs cs{dz, lddz, L.out_p, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart};
+  if (!bias) return hipSuccess;
+  ColsumArgs cs{dz, lddz, L.out_p, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
   return timed(c, "colsum", c->Bp, L.out_p, 0, 0.0, (double)c->Bp * L.out_p * es(c), s,
                [&] { return launch_colsum(c->bf16, cs, c->G + L.b, nullptr, s); });
 }
 
+// Input gradient through layer L: out[Bp, N] = (dz . W) masked by mask > 0. With
+// bias_out, also the column sums of the stored out (the bias gradient of the layer
+// below): fused into the product's epilogue where the large-tile kernel covers it.
 hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_t ldw, int N,
-                 const void* mask, void* out, int64_t ldo, bool out_f32, hipStream_t s) {
+                 const void* mask, void* out, int64_t ldo, bool out_f32, float* bias_out, float* cpart,
+                 hipStream_t s) {
   GemmArgs g{};
   g.A = dz; g.lda = L.out_p;
   g.B = W; g.ldb = ldw;
   g.C = out; g.ldc = ldo; g.out_f32 = out_f32 ? 1 : 0;
   g.mask = mask; g.ldm = ldo;
   g.M = c->Bp; g.N = N; g.K = L.out_p;
-  return timed(c, "gemm_dgrad", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
-               [&] { return gemm(c->bf16, GEMM_DGRAD, g, s); });
+  const bool fused = bias_out && gemm_colsum_fused(c->bf16, GEMM_DGRAD, g.M, g.N, g.K);
+  if (fused) {
+    g.colsum = cpart;
+    g.ldcs = N;
+  }
+  HK(timed(c, "gemm_dgrad", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
+           [&] { return gemm(c->bf16, GEMM_DGRAD, g, s); }));
+  if (!bias_out) return hipSuccess;
+  if (fused)
+    return timed(c, "colsum_final", c->Bp / 256, N, 0, 0.0, 4.0 * (c->Bp / 256) * N, s,
+                 [&] { return launch_colsum_final(cpart, c->Bp / 256, N, bias_out, s); });
+  ColsumArgs cs{out, ldo, N, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
+  return timed(c, "colsum", c->Bp, N, 0, 0.0, (double)c->Bp * N * es(c), s,
+               [&] { return launch_colsum(c->bf16, cs, bias_out, nullptr, s); });
 }
 
 // Critic ni in {1, 2}: weight and bias gradients of L = sum_b dq[b] q[b] given the
@@ -338,21 +357,24 @@ hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, v
   const Net& n = c->net[ni];
   const int nl = (int)n.L.size();
   const Lay& H = n.L[nl - 1];
-  ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, c->c_cpart};
+  ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, c->c_cpart, c->c_cextra};
   HK(timed(c, "colsum", c->Bp, H.in_p, 1, 0.0, (double)c->Bp * H.in_p * es(c), s,
            [&] { return launch_colsum(c->bf16, cs, c->G + H.w, c->G + H.b, s); }));
   HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp};
   HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, 2.0 * c->Bp * H.in_p * es(c), s,
            [&] { return launch_head_bwd(c->bf16, hb, s); }));
+  // dz of the last hidden layer comes from the head backward; its bias gradient is a
+  // separate column sum. Every later dz comes from a dgrad that also produces its
+  // bias gradient.
   int cur = 0;
   for (int l = nl - 2; l >= 0; --l) {
     const Lay& L = n.L[l];
     const void* Xl = l == 0 ? X : hid[l - 1];
     const int64_t ldx = l == 0 ? c->Kc : L.in_p;
-    HK(wgrad(c, c->c_dz[cur], L.out_p, Xl, ldx, L, c->c_wpart, c->c_cpart, s));
+    HK(wgrad(c, c->c_dz[cur], L.out_p, Xl, ldx, L, c->c_wpart, c->c_cpart, l == nl - 2, s));
     if (l > 0) {
       HK(dgrad(c, c->c_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], c->c_dz[cur ^ 1],
-               L.in_p, false, s));
+               L.in_p, false, c->G + n.L[l - 1].b, c->c_cpart, s));
       cur ^= 1;
     }
   }
@@ -372,12 +394,12 @@ hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* 
   for (int l = nl - 2; l >= 1; --l) {
     const Lay& L = n.L[l];
     HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], c->a_dz[cur ^ 1],
-             L.in_p, false, s));
+             L.in_p, false, nullptr, nullptr, s));
     cur ^= 1;
   }
   const Lay& L0 = n.L[0];
   return dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, c->Ap, nullptr, da,
-               c->Ap, true, s);
+               c->Ap, true, nullptr, nullptr, s);
 }
 
 hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
@@ -389,9 +411,10 @@ hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
     const Lay& L = n.L[l];
     const void* Xl = l == 0 ? c->xsa : c->ha[l - 1];
     const int64_t ldx = l == 0 ? c->Kc : L.in_p;
-    HK(wgrad(c, cur, L.out_p, Xl, ldx, L, c->a_wpart, c->a_cpart, s));
+    HK(wgrad(c, cur, L.out_p, Xl, ldx, L, c->a_wpart, c->a_cpart, l == nl - 1, s));
     if (l > 0) {
-      HK(dgrad(c, cur, L, wop(c, false, L.w), L.in_p, L.in_p, c->ha[l - 1], c->a_dz[nxt], L.in_p, false, s));
+      HK(dgrad(c, cur, L, wop(c, false, L.w), L.in_p, L.in_p, c->ha[l - 1], c->a_dz[nxt], L.in_p, false,
+               c->G + n.L[l - 1].b, c->a_cpart, s));
       cur = c->a_dz[nxt];
       nxt ^= 1;
     }
@@ -531,9 +554,10 @@ int setup(spz_ctx* c) {
   const int64_t Bp = c->Bp;
   const int nh = (int)c->hidden.size();
   // replay ring
-  c->off_a = (int)(c->O * e);
-  c->off_s2 = (int)((c->O + c->A) * e);
-  c->off_r = (int)((2 * (int64_t)c->O + c->A) * e + 3) / 4 * 4;
+  // [obs | act | next_obs | rew done], each segment starting on a 16-byte boundary.
+  c->off_a = (int)align16((int64_t)c->O * e);
+  c->off_s2 = c->off_a + (int)align16((int64_t)c->A * e);
+  c->off_r = c->off_s2 + (int)align16((int64_t)c->O * e);
   c->off_d = c->off_r + 4;
   c->row_bytes = align16(c->off_d + 4);
   c->cap = c->hp.capacity;
@@ -593,14 +617,17 @@ int setup(spz_ctx* c) {
   int64_t wmax = 0, cmax = 0;
   for (int ni = 0; ni < 3; ++ni)
     for (const Lay& L : c->net[ni].L) {
-      wmax = std::max<int64_t>(wmax, (int64_t)wgrad_splits(L.out_p, L.in_p, (int)Bp) * L.out_p * L.in_p);
+      wmax = std::max<int64_t>(wmax, (int64_t)wgrad_splits(c->bf16, L.out_p, L.in_p, (int)Bp) * L.out_p * L.in_p);
       cmax = std::max<int64_t>(cmax, (int64_t)std::max(L.out_p, L.in_p) + 1);
     }
-  const int chunks = colsum_chunks((int)Bp);
+  // column-sum partials: first-pass chunks of the standalone kernel, or one row per
+  // 256-row tile of a fused dgrad epilogue
+  const int chunks = std::max(colsum_chunks((int)Bp), (int)(Bp / 256));
   CK(dalloc_t(c, &c->c_wpart, (size_t)wmax * 4));
   CK(dalloc_t(c, &c->a_wpart, (size_t)wmax * 4));
   CK(dalloc_t(c, &c->c_cpart, (size_t)chunks * cmax * 4));
   CK(dalloc_t(c, &c->a_cpart, (size_t)chunks * cmax * 4));
+  CK(dalloc_t(c, &c->c_cextra, (size_t)chunks * 4));
   CK(dalloc_t(c, &c->c_lpart, (size_t)loss_blocks((int)Bp) * 3 * 8));
   CK(dalloc_t(c, &c->a_lpart, (size_t)loss_blocks((int)Bp) * 2 * 8));
   // streams (default priority)

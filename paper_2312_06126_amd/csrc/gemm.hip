@@ -218,14 +218,19 @@ __global__ void __launch_bounds__(gemm_threads(BM, BN)) k_gemm(GemmArgs g) {
     }
 }
 
+// out[m, n] = sum over slices z in order of part[z, m, n]; 4 columns per thread.
 __global__ void k_splitk_reduce(const float* __restrict__ part, int splits, int M, int N, int64_t ldc,
                                 float* __restrict__ out, int64_t ldo) {
+  const int nv = N / 4;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)M * N) return;
-  const int m = (int)(i / N), n = (int)(i % N);
-  float s = 0.0f;
-  for (int z = 0; z < splits; ++z) s += part[((int64_t)z * M + m) * ldc + n];
-  out[(int64_t)m * ldo + n] = s;
+  if (i >= (int64_t)M * nv) return;
+  const int m = (int)(i / nv), n = (int)(i % nv) * 4;
+  float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int z = 0; z < splits; ++z) {
+    const float4 v = *reinterpret_cast<const float4*>(part + ((int64_t)z * M + m) * ldc + n);
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  *reinterpret_cast<float4*>(out + (int64_t)m * ldo + n) = s;
 }
 
 int pick_tile(int n) { return n % 128 == 0 ? 128 : n % 64 == 0 ? 64 : n % 32 == 0 ? 32 : 0; }
@@ -264,27 +269,33 @@ hipError_t launch_mode(const GemmArgs& g, hipStream_t s) {
 
 }  // namespace
 
-int wgrad_splits(int M, int N, int K) {
-  const int bm = pick_tile(M), bn = pick_tile(N);
-  if (!bm || !bn) return 1;
-  const int tiles = (M / bm) * (N / bn);
+int wgrad_splits(bool bf16, int M, int N, int K) {
+  int tiles, target;
+  if (bf16 && M % 256 == 0 && N >= 128) {
+    // large-tile kernel (256 x 256 tiles, or 256 x 128 when N is not a multiple of
+    // 256): about one workgroup per CU
+    tiles = (M / 256) * (N % 256 == 0 ? N / 256 : N / 128);
+    target = 256;
+  } else {
+    const int bm = pick_tile(M), bn = pick_tile(N);
+    if (!bm || !bn) return 1;
+    tiles = (M / bm) * (N / bn);
+    target = 1024;
+  }
   int s = 1;
-  while (tiles * s < 1024 && K % (2 * s * BK) == 0 && K / (2 * s) >= 256) s *= 2;
+  while (tiles * s < target && K % (2 * s * BK) == 0 && K / (2 * s) >= 256) s *= 2;
   return s;
 }
 
-hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
-  // Shape contract: tiles divide the problem, K slices are whole BK steps,
-  // operand rows are 16-byte aligned.
-  if (g.M <= 0 || g.N <= 0 || g.K <= 0) return hipErrorInvalidValue;
+namespace {
+
+hipError_t gemm_generic(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   if (!pick_tile(g.N)) return hipErrorInvalidValue;
   if (mode == GEMM_WGRAD) {
     if (!pick_tile(g.M) || g.splits < 1 || g.K % (g.splits * BK)) return hipErrorInvalidValue;
   } else {
     if (g.M % 128 || g.K % BK) return hipErrorInvalidValue;
   }
-  const int vec = bf16 ? 8 : 4;
-  if (g.lda % vec || g.ldb % vec) return hipErrorInvalidValue;
   if (bf16) {
     switch (mode) {
       case GEMM_FWD: return launch_mode<bf16_t, GEMM_FWD>(g, s);
@@ -301,9 +312,46 @@ hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+// The same product restricted to output columns [off, off + n).
+GemmArgs column_slice(bool bf16, GemmMode mode, const GemmArgs& g, int off, int n) {
+  GemmArgs r = g;
+  const int64_t e = bf16 ? 2 : 4;
+  const int64_t ec = (mode == GEMM_WGRAD || g.out_f32) ? 4 : e;
+  r.N = n;
+  r.B = static_cast<const uint8_t*>(g.B) + (mode == GEMM_FWD ? (int64_t)off * g.ldb : off) * e;
+  r.C = static_cast<uint8_t*>(g.C) + (int64_t)off * ec;
+  if (g.bias) r.bias = g.bias + off;
+  if (g.mask) r.mask = static_cast<const uint8_t*>(g.mask) + (int64_t)off * e;
+  return r;
+}
+
+}  // namespace
+
+bool gemm_colsum_fused(bool bf16, GemmMode mode, int M, int N, int K) {
+  return bf16 && N % 128 == 0 && big_gemm_colsum(mode, M, N, K);
+}
+
+hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
+  if (g.colsum && !gemm_colsum_fused(bf16, mode, g.M, g.N, g.K)) return hipErrorInvalidValue;
+  // Shape contract: tiles divide the problem, K slices are whole BK steps,
+  // operand rows are 16-byte aligned.
+  if (g.M <= 0 || g.N <= 0 || g.K <= 0) return hipErrorInvalidValue;
+  const int vec = bf16 ? 8 : 4;
+  if (g.lda % vec || g.ldb % vec) return hipErrorInvalidValue;
+  if (mode == GEMM_WGRAD && (g.splits < 1 || g.K % g.splits)) return hipErrorInvalidValue;
+  const int n_big = g.N / 128 * 128;
+  if (bf16 && n_big > 0 && big_gemm_fits(mode, g.M, n_big, g.K, mode == GEMM_WGRAD ? g.splits : 1)) {
+    hipError_t e = gemm_big(mode, column_slice(bf16, mode, g, 0, n_big), s);
+    if (e != hipSuccess || n_big == g.N) return e;
+    return gemm_generic(bf16, mode, column_slice(bf16, mode, g, n_big, g.N - n_big), s);
+  }
+  return gemm_generic(bf16, mode, g, s);
+}
+
 hipError_t splitk_reduce(const float* part, int splits, int M, int N, int64_t ldc, float* out,
                          int64_t ldo, hipStream_t s) {
-  const int64_t n = (int64_t)M * N;
+  if (N % 4 || ldc % 4 || ldo % 4) return hipErrorInvalidValue;
+  const int64_t n = (int64_t)M * (N / 4);
   k_splitk_reduce<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, splits, M, N, ldc, out, ldo);
   return hipGetLastError();
 }

@@ -1,0 +1,334 @@
+// Large-tile bfloat16 MFMA GEMM for the wide layers (256-row tiles).
+//
+// Same three products and epilogues as the generic kernel (gemm.hip), for
+// bf16 operands whose tile dimensions are multiples of 256 (rows) and 256 or
+// 128 (columns). Design points for gfx950:
+//   * 512 threads = 8 waves (two per SIMD) in a 4x2 grid; each wave owns
+//     64 x BN/2 of the output as 2 x (BN/64) blocks of v_mfma_f32_32x32x16_bf16
+//     (128 or 64 float32 accumulators per lane). Two waves per SIMD let one
+//     wave's LDS reads and global loads overlap the other's matrix work, which
+//     measured faster than one wave per SIMD with 128 x 128 wave tiles.
+//   * Both operands are copied global -> registers -> LDS in their memory layout
+//     (16-byte vector loads and stores, no shuffles). A k-contiguous tile is read
+//     back as one 16-byte LDS read per fragment; an m/n-contiguous (k-major) tile
+//     is read with two ds_read_b64_tr_b16 transposing reads per fragment: within
+//     each 16-lane group, lane i addresses 4 consecutive values of row k0 + i/4
+//     at column m0 + 4(i%4), and lane j receives column m0 + j for the 4 rows.
+//   * Double-buffered LDS (one barrier per 32-deep k slice). At the top of each
+//     slice the registers holding slice k+1 are stored to the free LDS buffer and
+//     the global loads of slice k+2 are issued, so they travel while slice k is
+//     multiplied.
+//   * XCD-aware tile order: workgroup b runs on XCD b % 8, so logical tiles are
+//     handed out in contiguous ranges per XCD; the column tiles of one row panel
+//     (and the split-K slices of one weight-gradient tile) share an L2.
+#include "internal.h"
+
+namespace spz {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+#define LDS_AS __attribute__((address_space(3)))
+
+constexpr int BM = 256, BK = 32, NT = 512, WM = 4, WN = 2;
+
+template <bool KC, int ROWS>
+struct BigTile {
+  // Row pitch in elements. k-contiguous rows of 80 bytes put the 16 rows read by
+  // one 16-lane phase of a 16-byte read on distinct 4-bank groups; k-major rows of
+  // 2*ROWS + 64 bytes shift consecutive k rows by 16 banks, so the two 16-lane
+  // groups of a transposing read (4 rows x 32 bytes each) never share a bank.
+  static constexpr int PITCH = KC ? BK + 8 : ROWS + 32;
+  static constexpr int ELEMS = (KC ? ROWS : BK) * PITCH;
+  static constexpr int NV = ROWS * BK / 8;
+  static constexpr int PER = NV / NT;
+  static constexpr int VPR = (KC ? BK : ROWS) / 8;
+  static_assert(NV % NT == 0, "tile must split evenly over the workgroup");
+  u32x4 r[PER];
+
+  __device__ inline void load(const bf16_t* __restrict__ base, int64_t ld, int r0, int k0, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      const int a = v / VPR, b = (v % VPR) * 8;
+      const bf16_t* src = KC ? base + (int64_t)(r0 + a) * ld + (k0 + b) : base + (int64_t)(k0 + a) * ld + (r0 + b);
+      r[p] = *reinterpret_cast<const u32x4*>(src);
+    }
+  }
+  __device__ inline void store(bf16_t* lds, int tid) const {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      const int a = v / VPR, b = (v % VPR) * 8;
+      *reinterpret_cast<u32x4*>(lds + a * PITCH + b) = r[p];
+    }
+  }
+};
+
+template <bool KC, int PITCH>
+__device__ inline bf16x8 frag(const bf16_t* lds, int rb, int ks, int lane) {
+  if constexpr (KC) {
+    const int row = rb + (lane & 31), k = ks + 8 * (lane >> 5);
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(lds + row * PITCH + k));
+  } else {
+    const int g = lane >> 4, i = lane & 15;
+    const int m0 = rb + 16 * (g & 1), k0 = ks + 8 * (g >> 1);
+    const bf16_t* p = lds + (k0 + (i >> 2)) * PITCH + m0 + 4 * (i & 3);
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(p));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(p + 4 * PITCH));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  }
+}
+
+// Epilogue. Accumulator blocks leave through a per-wave LDS scratch so that each
+// lane handles 8 consecutive columns of one row: 16-byte loads of mask and bias and
+// 16-byte (bf16) or 32-byte (fp32) stores. 32x32 accumulator layout: lane holds
+// column lane%32; register q holds row 8*(q/4) + 4*(lane/32) + q%4 of the block.
+// CSUM (dgrad): column sums of the stored (rounded) values over the tile's 256 rows
+// go to g.colsum[mt, :]: per lane over its rows, a fixed butterfly over the 16 lanes
+// of a column group, then the WM waves of the column in order through LDS.
+constexpr int SCR_PITCH = 36;   // floats per scratch row
+
+template <int MODE, int BN, bool MASK, bool OUTF32, bool RELU, bool CSUM>
+__device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0,
+                                int n0, int wm, int wn, int lane, int wave, int z, int mt, float* smem_f) {
+  constexpr int TM_ = BM / WM / 32, TN_ = BN / WN / 32;
+  float* scr = smem_f + wave * (32 * SCR_PITCH);
+  float* csh = smem_f + (NT / 64) * 32 * SCR_PITCH;   // [WM][BN]
+  const int cgrp = lane & 3, rsub = lane >> 2;
+#pragma unroll
+  for (int j = 0; j < TN_; ++j) {
+    const int cb = wn * (BN / WN) + 32 * j + 8 * cgrp;
+    float bias[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bias[e] = 0.0f;
+    if constexpr (MODE == GEMM_FWD) {
+      if (g.bias) {
+        const float4 b0 = *reinterpret_cast<const float4*>(g.bias + n0 + cb);
+        const float4 b1 = *reinterpret_cast<const float4*>(g.bias + n0 + cb + 4);
+        bias[0] = b0.x; bias[1] = b0.y; bias[2] = b0.z; bias[3] = b0.w;
+        bias[4] = b1.x; bias[5] = b1.y; bias[6] = b1.z; bias[7] = b1.w;
+      }
+    }
+    float cs[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cs[e] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < TM_; ++i) {
+      // The wave reads back what it wrote; LDS operations of one wave complete in order.
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        scr[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * SCR_PITCH + (lane & 31)] = acc[i][j][q];
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const int r = rsub + 16 * p;
+        const int64_t row = m0 + wm * (BM / WM) + 32 * i + r;
+        const float4 x0 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp);
+        const float4 x1 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp + 4);
+        float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+        if constexpr (MODE == GEMM_WGRAD) {
+          float* dst = static_cast<float*>(g.C) + ((int64_t)z * g.M + row) * g.ldc + n0 + cb;
+          *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+          *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            if constexpr (MODE == GEMM_FWD) v[e] += bias[e];
+            if constexpr (RELU) v[e] = v[e] < 0.0f ? 0.0f : v[e];
+          }
+          if constexpr (MASK) {
+            const uint4 mk = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(g.mask) + row * g.ldm + n0 + cb);
+            const uint32_t mw[4] = {mk.x, mk.y, mk.z, mk.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float h = bf2f((bf16_t)((mw[e >> 1] >> (16 * (e & 1))) & 0xFFFFu));
+              v[e] = h > 0.0f ? v[e] : 0.0f;
+            }
+          }
+          if constexpr (OUTF32) {
+            float* dst = static_cast<float*>(g.C) + row * g.ldc + n0 + cb;
+            *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+            *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+          } else {
+            uint32_t w[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const bf16_t lo = f2bf(v[2 * e]), hi = f2bf(v[2 * e + 1]);
+              w[e] = (uint32_t)lo | ((uint32_t)hi << 16);
+              if constexpr (CSUM) {
+                cs[2 * e] += bf2f(lo);
+                cs[2 * e + 1] += bf2f(hi);
+              }
+            }
+            *reinterpret_cast<uint4*>(static_cast<bf16_t*>(g.C) + row * g.ldc + n0 + cb) = make_uint4(w[0], w[1], w[2], w[3]);
+          }
+        }
+      }
+    }
+    if constexpr (CSUM) {
+#pragma unroll
+      for (int o = 4; o < 64; o <<= 1)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cs[e] += __shfl_xor(cs[e], o);
+      if (rsub == 0)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) csh[wm * BN + cb + e] = cs[e];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if constexpr (CSUM) {
+    __syncthreads();
+    for (int c = threadIdx.x; c < BN; c += NT) {
+      float t = 0.0f;
+#pragma unroll
+      for (int w = 0; w < WM; ++w) t += csh[w * BN + c];
+      g.colsum[(int64_t)mt * g.ldcs + n0 + c] = t;
+    }
+  }
+}
+
+template <int MODE, int BN>
+__global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int tiles_n) {
+  constexpr bool AKC = MODE != GEMM_WGRAD;
+  constexpr bool BKC = MODE == GEMM_FWD;
+  using TA = BigTile<AKC, BM>;
+  using TB = BigTile<BKC, BN>;
+  constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  bf16_t* As0 = reinterpret_cast<bf16_t*>(smem);
+  bf16_t* As1 = As0 + TA::ELEMS;
+  bf16_t* Bs0 = As1 + TA::ELEMS;
+  bf16_t* Bs1 = Bs0 + TB::ELEMS;
+
+  // XCD-aware logical tile: contiguous logical ranges per XCD, column tiles fastest.
+  const int total = gridDim.x;
+  int L = blockIdx.x;
+  if ((total & 7) == 0) L = (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3);
+  const int nt = L % tiles_n;
+  const int mt = (L / tiles_n) % tiles_m;
+  const int z = L / (tiles_n * tiles_m);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int m0 = mt * BM, n0 = nt * BN;
+  int kbeg = 0, kend = g.K;
+  if constexpr (MODE == GEMM_WGRAD) {
+    const int ks = g.K / g.splits;
+    kbeg = z * ks;
+    kend = kbeg + ks;
+  }
+  const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.A);
+  const bf16_t* __restrict__ B = static_cast<const bf16_t*>(g.B);
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
+
+  TA ta;
+  TB tb;
+  const int nk = (kend - kbeg) / BK;
+  ta.load(A, g.lda, m0, kbeg, tid);
+  tb.load(B, g.ldb, n0, kbeg, tid);
+  ta.store(As0, tid);
+  tb.store(Bs0, tid);
+  if (nk > 1) {
+    ta.load(A, g.lda, m0, kbeg + BK, tid);
+    tb.load(B, g.ldb, n0, kbeg + BK, tid);
+  }
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const bf16_t* Ac = (kt & 1) ? As1 : As0;
+    const bf16_t* Bc = (kt & 1) ? Bs1 : Bs0;
+    if (kt + 1 < nk) {
+      ta.store((kt & 1) ? As0 : As1, tid);
+      tb.store((kt & 1) ? Bs0 : Bs1, tid);
+    }
+    if (kt + 2 < nk) {
+      ta.load(A, g.lda, m0, kbeg + (kt + 2) * BK, tid);
+      tb.load(B, g.ldb, n0, kbeg + (kt + 2) * BK, tid);
+    }
+#pragma unroll
+    for (int ks = 0; ks < BK; ks += 16) {
+      bf16x8 af[TM], bw[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = frag<AKC, TA::PITCH>(Ac, (wm * TM + i) * 32, ks, lane);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bw[j] = frag<BKC, TB::PITCH>(Bc, (wn * TN + j) * 32, ks, lane);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue variants are compile-time so the store loops unroll completely. The
+  // final barrier of the k loop has released the LDS tiles for the scratch.
+  float* smem_f = reinterpret_cast<float*>(smem);
+  if constexpr (MODE == GEMM_WGRAD) {
+    epilogue<MODE, BN, false, true, false, false>(g, acc, m0, n0, wm, wn, lane, wave, z, mt, smem_f);
+  } else if constexpr (MODE == GEMM_FWD) {
+    if (g.out_f32) epilogue<MODE, BN, false, true, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
+    else if (g.relu) epilogue<MODE, BN, false, false, true, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
+    else epilogue<MODE, BN, false, false, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
+  } else {
+    if (g.out_f32) epilogue<MODE, BN, false, true, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
+    else if (g.mask && g.colsum) epilogue<MODE, BN, true, false, false, true>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
+    else if (g.mask) epilogue<MODE, BN, true, false, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
+    else if (g.colsum) epilogue<MODE, BN, false, false, false, true>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
+    else epilogue<MODE, BN, false, false, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
+  }
+}
+
+template <int MODE, int BN>
+hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
+  using TA = BigTile<MODE != GEMM_WGRAD, BM>;
+  using TB = BigTile<MODE == GEMM_FWD, BN>;
+  const size_t tiles = 2 * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
+  const size_t scratch = ((NT / 64) * 32 * SCR_PITCH + WM * BN) * sizeof(float);
+  const size_t lds = tiles > scratch ? tiles : scratch;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_gemm_big<MODE, BN>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int tiles_m = g.M / BM, tiles_n = g.N / BN;
+  const int splits = MODE == GEMM_WGRAD ? g.splits : 1;
+  k_gemm_big<MODE, BN><<<tiles_m * tiles_n * splits, NT, lds, s>>>(g, tiles_m, tiles_n);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool big_gemm_colsum(GemmMode mode, int M, int N, int K) {
+  return mode == GEMM_DGRAD && big_gemm_fits(mode, M, N, K, 1);
+}
+
+bool big_gemm_fits(GemmMode mode, int M, int N, int K, int splits) {
+  (void)mode;
+  if (M % BM || N % 128) return false;
+  const int kk = mode == GEMM_WGRAD ? K / splits : K;
+  return kk % BK == 0 && kk > 0;
+}
+
+hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s) {
+  const bool bn256 = g.N % 256 == 0;
+  switch (mode) {
+    case GEMM_FWD: return bn256 ? launch_big<GEMM_FWD, 256>(g, s) : launch_big<GEMM_FWD, 128>(g, s);
+    case GEMM_DGRAD: return bn256 ? launch_big<GEMM_DGRAD, 256>(g, s) : launch_big<GEMM_DGRAD, 128>(g, s);
+    case GEMM_WGRAD: return bn256 ? launch_big<GEMM_WGRAD, 256>(g, s) : launch_big<GEMM_WGRAD, 128>(g, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace spz

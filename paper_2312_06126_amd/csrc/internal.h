@@ -81,6 +81,8 @@ struct GemmArgs {
   int relu;                    // FWD
   int out_f32;                 // FWD / DGRAD: store float32 instead of the operand type
   int splits;                  // WGRAD: number of K slices; C gets splits * M * ldc floats
+  float* colsum; int64_t ldcs; // DGRAD (bf16 large-tile only): column sums of the stored C
+                               // per 256-row tile, colsum[M / 256, ldcs]
 };
 
 // C = A B with A: [M, K] k-contiguous (FWD, DGRAD) or [K, M] (WGRAD),
@@ -90,6 +92,12 @@ hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s);
 hipError_t splitk_reduce(const float* part, int splits, int M, int N, int64_t ldc, float* out,
                          int64_t ldo, hipStream_t s);
 // Choose a split count for a WGRAD of (M, N, K) and return it (K % (32*splits) == 0).
-int wgrad_splits(int M, int N, int K);
+int wgrad_splits(bool bf16, int M, int N, int K);
+// Large-tile bf16 kernel (gemm_big.hip): M % 256 == 0, N % 128 == 0, K slices of 32.
+bool big_gemm_fits(GemmMode mode, int M, int N, int K, int splits);
+// True when gemm() with these arguments can produce the fused column sums (GemmArgs::colsum).
+bool gemm_colsum_fused(bool bf16, GemmMode mode, int M, int N, int K);
+bool big_gemm_colsum(GemmMode mode, int M, int N, int K);
+hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s);
 
 }  // namespace spz

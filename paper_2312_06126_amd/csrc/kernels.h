@@ -5,7 +5,7 @@
 
 namespace spz {
 
-constexpr int COLSUM_CHUNK = 512;  // rows per first-pass block of the column sums
+constexpr int COLSUM_CHUNK = 256;  // rows per first-pass block of the column sums
 
 struct GatherArgs {
   const uint8_t* buf; int64_t row_bytes;
@@ -67,6 +67,7 @@ struct ActorHeadBwdArgs {
 
 struct ColsumArgs {
   const void* X; int64_t ld; int N, rows, chunk; const float* weights; int extra; float* part;
+  float* part_extra;   // [chunks] when extra
 };
 
 struct AdamArgs {
@@ -97,6 +98,8 @@ hipError_t launch_actor_loss(const ActorLossArgs& a, hipStream_t s);
 hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream_t s);
 int colsum_chunks(int rows);
 hipError_t launch_colsum(bool bf16, const ColsumArgs& a, float* out, float* out_extra, hipStream_t s);
+// out[n] = sum over c in order of part[c, n] (c < chunks), n < N.
+hipError_t launch_colsum_final(const float* part, int chunks, int N, float* out, hipStream_t s);
 hipError_t launch_adam(const AdamArgs& a, hipStream_t s);
 hipError_t launch_finish(const FinishArgs& f, hipStream_t s);
 hipError_t launch_to_bf16(const float* src, bf16_t* dst, int64_t n, hipStream_t s);

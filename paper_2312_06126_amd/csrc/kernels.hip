@@ -46,6 +46,17 @@ __device__ inline double block_sum(double v, double* sh) {
 }
 
 // ------------------------------------------------------------------------------ replay
+// Copy `bytes` (a multiple of the element size) between 16-byte aligned segments,
+// 16 bytes per lane, the tail element by element.
+template <typename T>
+__device__ inline void copy_seg(uint8_t* dst, const uint8_t* src, int bytes, int lane) {
+  const int nv = bytes >> 4;
+  for (int v = lane; v < nv; v += 64)
+    reinterpret_cast<uint4*>(dst)[v] = reinterpret_cast<const uint4*>(src)[v];
+  for (int e = (nv << 4) / (int)sizeof(T) + lane; e < bytes / (int)sizeof(T); e += 64)
+    reinterpret_cast<T*>(dst)[e] = reinterpret_cast<const T*>(src)[e];
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256) k_gather(GatherArgs g) {
   const int lane = threadIdx.x & 63;
@@ -55,19 +66,15 @@ __global__ void __launch_bounds__(256) k_gather(GatherArgs g) {
   const uint32_t w = philox_word(g.seed, (uint64_t)b, t, P_IDX, 0u);
   const uint32_t row = mulhi32(w, g.size);
   const uint8_t* src = g.buf + (int64_t)row * g.row_bytes;
-  const T* s = reinterpret_cast<const T*>(src);
-  const T* a = reinterpret_cast<const T*>(src + g.off_a);
-  const T* s2 = reinterpret_cast<const T*>(src + g.off_s2);
-  T* xsa = static_cast<T*>(g.xsa) + (int64_t)b * g.Kc;
-  T* xsp = static_cast<T*>(g.xsp) + (int64_t)b * g.Kc;
-  T* xs2 = static_cast<T*>(g.xs2) + (int64_t)b * g.Kc;
-  for (int j = lane; j < g.O; j += 64) {
-    const T v = s[j];
-    xsa[j] = v;
-    xsp[j] = v;
-    xs2[j] = s2[j];
-  }
-  for (int j = lane; j < g.A; j += 64) xsa[g.Ka + j] = a[j];
+  const int64_t xrow = (int64_t)b * g.Kc * (int64_t)sizeof(T);
+  uint8_t* xsa = static_cast<uint8_t*>(g.xsa) + xrow;
+  uint8_t* xsp = static_cast<uint8_t*>(g.xsp) + xrow;
+  uint8_t* xs2 = static_cast<uint8_t*>(g.xs2) + xrow;
+  const int sb = g.O * (int)sizeof(T);
+  copy_seg<T>(xsa, src, sb, lane);
+  copy_seg<T>(xsp, src, sb, lane);
+  copy_seg<T>(xs2, src + g.off_s2, sb, lane);
+  copy_seg<T>(xsa + g.Ka * (int)sizeof(T), src + g.off_a, g.A * (int)sizeof(T), lane);
   if (lane == 0) {
     g.r[b] = *reinterpret_cast<const float*>(src + g.off_r);
     g.d[b] = *reinterpret_cast<const float*>(src + g.off_d);
@@ -147,33 +154,76 @@ __global__ void __launch_bounds__(256) k_td3_head(Td3HeadArgs h) {
   }
 }
 
-// Critic output layer (width 1): q[b] = sum_k H[b, k] w[k] + bias. One wave per row.
+// 16-byte vector of operand values and its float image.
+template <typename T> struct Vec16;
+template <> struct Vec16<float> {
+  static constexpr int N = 4;
+  __device__ static inline void load(const float* p, float* o) {
+    const float4 v = *reinterpret_cast<const float4*>(p);
+    o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+  }
+  __device__ static inline void store(float* p, const float* o) {
+    *reinterpret_cast<float4*>(p) = make_float4(o[0], o[1], o[2], o[3]);
+  }
+};
+template <> struct Vec16<bf16_t> {
+  static constexpr int N = 8;
+  __device__ static inline void load(const bf16_t* p, float* o) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = bf2f((bf16_t)(w[i] & 0xFFFFu));
+      o[2 * i + 1] = bf2f((bf16_t)(w[i] >> 16));
+    }
+  }
+  __device__ static inline void store(bf16_t* p, const float* o) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(o[2 * i]) | ((uint32_t)f2bf(o[2 * i + 1]) << 16);
+    *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+
+// Critic output layer (width 1): q[b] = sum_k H[b, k] w[k] + bias. One wave per row,
+// 16 bytes per lane; fixed per-lane order, then a fixed butterfly.
 template <typename T>
 __global__ void __launch_bounds__(256) k_rowdot(RowdotArgs r) {
+  using V = Vec16<T>;
   const int lane = threadIdx.x & 63;
   const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (b >= r.rows) return;
   const T* h = static_cast<const T*>(r.H) + (int64_t)b * r.ld;
   const T* w = static_cast<const T*>(r.w);
   float s = 0.0f;
-  for (int k = lane; k < r.K; k += 64) s = fmaf(to_f<T>(h[k]), to_f<T>(w[k]), s);
+  for (int k = lane * V::N; k < r.K; k += 64 * V::N) {
+    float hv[V::N], wv[V::N];
+    V::load(h + k, hv);
+    V::load(w + k, wv);
+#pragma unroll
+    for (int i = 0; i < V::N; ++i) s = fmaf(hv[i], wv[i], s);
+  }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
   if (lane == 0) r.q[b] = s + *r.bias;
 }
 
 // Critic output layer backward: dH[b, k] = rnd(dq[b]) * w[k] * (H[b, k] > 0), stored
-// in the operand type. Pad rows have dq = 0 and pad columns have w = 0.
+// in the operand type, 16 bytes per thread. Pad rows have dq = 0 and pad columns w = 0.
 template <typename T>
 __global__ void __launch_bounds__(256) k_head_bwd(HeadBwdArgs a) {
+  using V = Vec16<T>;
+  const int kv = a.K / V::N;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)a.rows * a.K) return;
-  const int b = (int)(i / a.K), k = (int)(i % a.K);
+  if (i >= (int64_t)a.rows * kv) return;
+  const int b = (int)(i / kv), k = (int)(i % kv) * V::N;
   const float dq = to_f<T>(from_f<T>(a.dq[b]));
-  const T* H = static_cast<const T*>(a.H);
-  float v = dq * to_f<T>(static_cast<const T*>(a.w)[k]);
-  if (!(to_f<T>(H[(int64_t)b * a.ld + k]) > 0.0f)) v = 0.0f;
-  static_cast<T*>(a.dH)[(int64_t)b * a.ld + k] = from_f<T>(v);
+  float hv[V::N], wv[V::N], o[V::N];
+  V::load(static_cast<const T*>(a.H) + (int64_t)b * a.ld + k, hv);
+  V::load(static_cast<const T*>(a.w) + k, wv);
+#pragma unroll
+  for (int j = 0; j < V::N; ++j) o[j] = hv[j] > 0.0f ? dq * wv[j] : 0.0f;
+  V::store(static_cast<T*>(a.dH) + (int64_t)b * a.ld + k, o);
 }
 
 // ------------------------------------------------------------------------------ TD target, losses
@@ -271,34 +321,101 @@ __global__ void __launch_bounds__(256) k_actor_head_bwd(ActorHeadBwdArgs h) {
 }
 
 // ------------------------------------------------------------------------------ column sums
-// part[c, n] = sum over rows of chunk c of wt(b) X[b, n] for n < N, and wt(b) for n == N
-// (when extra). wt(b) = rnd(weights[b]) or 1.
+// First pass: block (x, y) sums rows [y*chunk, (y+1)*chunk) of a column tile of CT
+// 16-byte vectors; threads hold one vector column each and step over rows by RT,
+// then the RT partial sums per column are added in row order through LDS.
+// part[y, n] = sum_b wt(b) X[b, n]; wt(b) = rnd(weights[b]) or 1. With `extra`,
+// part_extra[y] = sum_b wt(b) (computed by the x == 0 blocks).
 template <typename T>
 __global__ void __launch_bounds__(256) k_colsum(ColsumArgs a) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  const int ncol = a.N + (a.extra ? 1 : 0);
-  if (n >= ncol) return;
+  using V = Vec16<T>;
+  constexpr int NT = 256;
+  const int nvec = a.N / V::N;
+  const int CT = nvec < 32 ? nvec : 32;
+  const int RT = NT / CT;
+  const int tx = threadIdx.x % CT, ty = threadIdx.x / CT;
+  const int cv = blockIdx.x * CT + tx;
   const int b0 = blockIdx.y * a.chunk, b1 = min(b0 + a.chunk, a.rows);
   const T* X = static_cast<const T*>(a.X);
-  float s = 0.0f;
-  for (int b = b0; b < b1; ++b) {
-    const float w = a.weights ? to_f<T>(from_f<T>(a.weights[b])) : 1.0f;
-    const float x = n < a.N ? to_f<T>(X[(int64_t)b * a.ld + n]) : 1.0f;
-    s = fmaf(w, x, s);
+  float acc[V::N];
+#pragma unroll
+  for (int i = 0; i < V::N; ++i) acc[i] = 0.0f;
+  float wsum = 0.0f;
+  if (ty < RT && cv < nvec) {
+#pragma unroll 4
+    for (int b = b0 + ty; b < b1; b += RT) {
+      const float w = a.weights ? to_f<T>(from_f<T>(a.weights[b])) : 1.0f;
+      float x[V::N];
+      V::load(X + (int64_t)b * a.ld + cv * V::N, x);
+#pragma unroll
+      for (int i = 0; i < V::N; ++i) acc[i] = fmaf(w, x[i], acc[i]);
+      wsum += w;
+    }
   }
-  a.part[(int64_t)blockIdx.y * ncol + n] = s;
+  __shared__ float sh[NT * 8 + NT];
+  const bool live = ty < RT;
+#pragma unroll
+  for (int i = 0; i < V::N; ++i) sh[threadIdx.x * V::N + i] = live ? acc[i] : 0.0f;
+  __syncthreads();
+  if (ty == 0 && cv < nvec) {
+    float o[V::N];
+#pragma unroll
+    for (int i = 0; i < V::N; ++i) o[i] = 0.0f;
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int i = 0; i < V::N; ++i) o[i] += sh[(r * CT + tx) * V::N + i];
+#pragma unroll
+    for (int i = 0; i < V::N; ++i) a.part[(int64_t)blockIdx.y * a.N + cv * V::N + i] = o[i];
+  }
+  if (a.extra && blockIdx.x == 0) {   // uniform per block
+    if (tx == 0 && live) sh[NT * 8 + ty] = wsum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float t = 0.0f;
+      for (int r = 0; r < RT; ++r) t += sh[NT * 8 + r];
+      a.part_extra[blockIdx.y] = t;
+    }
+  }
 }
 
-__global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ part, int chunks, int N,
-                                                      int extra, float* __restrict__ out,
+// Second pass: out[n] = sum over chunks c of part[c, n]. A block owns 64 columns
+// (16 float4 lanes) and splits the chunks over 16 groups g (c = g, g + 16, ...); the
+// group sums are then added in g order through LDS: a fixed order for a fixed chunk
+// count. The extra scalar (when present) is summed the same way by block 0.
+__global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ part, const float* __restrict__ part_extra,
+                                                      int chunks, int N, int extra, float* __restrict__ out,
                                                       float* __restrict__ out_extra) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  const int ncol = N + (extra ? 1 : 0);
-  if (n >= ncol) return;
-  float s = 0.0f;
-  for (int c = 0; c < chunks; ++c) s += part[(int64_t)c * ncol + n];
-  if (n < N) out[n] = s;
-  else *out_extra = s;
+  __shared__ float4 sh[256];
+  __shared__ float she[16];
+  const int cv = threadIdx.x & 15, grp = threadIdx.x >> 4;
+  const int col = blockIdx.x * 64 + cv * 4;
+  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  float ex = 0.0f;
+  if (col < N) {
+#pragma unroll 4
+    for (int c = grp; c < chunks; c += 16) {
+      const float4 v = *reinterpret_cast<const float4*>(part + (int64_t)c * N + col);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+  }
+  if (extra && blockIdx.x == 0 && cv == 0)
+    for (int c = grp; c < chunks; c += 16) ex += part_extra[c];
+  sh[threadIdx.x] = acc;
+  if (cv == 0) she[grp] = ex;
+  __syncthreads();
+  if (grp == 0 && col < N) {
+    float4 t = sh[cv];
+    for (int g = 1; g < 16; ++g) {
+      const float4 v = sh[g * 16 + cv];
+      t.x += v.x; t.y += v.y; t.z += v.z; t.w += v.w;
+    }
+    *reinterpret_cast<float4*>(out + col) = t;
+  }
+  if (extra && blockIdx.x == 0 && threadIdx.x == 0) {
+    float t = 0.0f;
+    for (int g = 0; g < 16; ++g) t += she[g];
+    *out_extra = t;
+  }
 }
 
 // ------------------------------------------------------------------------------ optimizer
@@ -428,11 +545,14 @@ hipError_t launch_td3_head(bool bf16, const Td3HeadArgs& h, hipStream_t s) {
   return hipGetLastError();
 }
 hipError_t launch_rowdot(bool bf16, const RowdotArgs& r, hipStream_t s) {
+  if (r.K % (bf16 ? 8 : 4)) return hipErrorInvalidValue;
   SPZ_LAUNCH_T(bf16, k_rowdot, blocks(r.rows, 4), 256, s, r);
   return hipGetLastError();
 }
 hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s) {
-  SPZ_LAUNCH_T(bf16, k_head_bwd, blocks((int64_t)a.rows * a.K, 256), 256, s, a);
+  const int vec = bf16 ? 8 : 4;
+  if (a.K % vec || a.ld % vec) return hipErrorInvalidValue;
+  SPZ_LAUNCH_T(bf16, k_head_bwd, blocks((int64_t)a.rows * (a.K / vec), 256), 256, s, a);
   return hipGetLastError();
 }
 hipError_t launch_td_target(const TdArgs& a, hipStream_t s) {
@@ -454,11 +574,18 @@ hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream
 }
 int colsum_chunks(int rows) { return (int)blocks(rows, COLSUM_CHUNK); }
 hipError_t launch_colsum(bool bf16, const ColsumArgs& a, float* out, float* out_extra, hipStream_t s) {
-  const int ncol = a.N + (a.extra ? 1 : 0);
+  const int vec = bf16 ? 8 : 4;
+  if (a.N % vec || a.ld % vec || a.N % 4) return hipErrorInvalidValue;
+  const int nvec = a.N / vec, ct = nvec < 32 ? nvec : 32;
   const int chunks = (int)blocks(a.rows, a.chunk);
-  dim3 grid(blocks(ncol, 256), chunks);
+  dim3 grid(blocks(nvec, ct), chunks);
   SPZ_LAUNCH_T(bf16, k_colsum, grid, 256, s, a);
-  k_colsum_final<<<blocks(ncol, 256), 256, 0, s>>>(a.part, chunks, a.N, a.extra, out, out_extra);
+  k_colsum_final<<<blocks(a.N, 64), 256, 0, s>>>(a.part, a.part_extra, chunks, a.N, a.extra, out, out_extra);
+  return hipGetLastError();
+}
+hipError_t launch_colsum_final(const float* part, int chunks, int N, float* out, hipStream_t s) {
+  if (N % 4) return hipErrorInvalidValue;
+  k_colsum_final<<<blocks(N, 64), 256, 0, s>>>(part, nullptr, chunks, N, 0, out, nullptr);
   return hipGetLastError();
 }
 hipError_t launch_adam(const AdamArgs& a, hipStream_t s) {

@@ -89,3 +89,54 @@ def per_tensor_rel(o, key, flat_gpu, flat_ref):
             worst = max(worst, rel(flat_gpu[off:off + n], flat_ref[off:off + n]))
             off += n
     return worst
+
+
+# ---------------------------------------------------------------- multi-step parameter parity
+# An Adam update m_hat / (sqrt(v_hat) + eps) changes by about delta / sqrt(v_hat)
+# when the gradient changes by delta. For an element whose whole gradient history
+# is tiny next to its tensor's typical gradient (at step 1: |g| itself, since the
+# first step is lr * sign(g)), the direction is set by rounding -- mostly by ReLU
+# decisions on pre-activations within float32 rounding of zero, which float32
+# and float64 can take differently. Such elements are identified from the
+# oracle's gradients alone (sqrt(v_hat) < AMBIGUOUS * rms(g) of the tensor at
+# some step), excluded from the norm comparison, counted, and checked against
+# the bound Adam puts on their motion.
+AMBIGUOUS = 3e-3
+
+
+def tensor_slices(o, key):
+    off, out = 0, []
+    for fi, fo in o.dims(key):
+        for n in (fi * fo, fo):
+            out.append(slice(off, off + n))
+            off += n
+    return out
+
+
+def ambiguous_elements(o, key, grad_history, beta2=0.999):
+    """Boolean mask over the flat layout of `key` (grad_history: flat oracle gradients per Adam step)."""
+    amb = np.zeros(o.param_count(key), bool)
+    v = np.zeros(o.param_count(key))
+    for t, gflat in enumerate(grad_history, start=1):
+        v = beta2 * v + (1.0 - beta2) * gflat * gflat
+        root_vhat = np.sqrt(v / (1.0 - beta2 ** t))
+        for sl in tensor_slices(o, key):
+            gt = gflat[sl]
+            rms = np.sqrt(np.mean(gt * gt))
+            amb[sl] |= (root_vhat[sl] < AMBIGUOUS * rms) & (root_vhat[sl] > 0.0)
+    return amb
+
+
+def check_param_parity(o, key, pg, pr, amb, tol, steps, lr, max_frac=0.05):
+    """Per-tensor rel L2 <= tol over unambiguous elements; ambiguous ones rare and bounded
+    (an Adam step moves an element by about lr at most; targets move less)."""
+    worst = 0.0
+    for sl in tensor_slices(o, key):
+        a, b, m = pg[sl].astype(np.float64), pr[sl], ~amb[sl]
+        if m.any():
+            worst = max(worst, rel(a[m], b[m]))
+        if (~m).any():
+            assert (~m).mean() <= max_frac, (key, (~m).mean())
+            assert np.all(np.abs(a[~m] - b[~m]) <= 2.0 * lr * steps + tol * np.abs(b[~m]) + 1e-12), key
+    assert worst <= tol, (key, worst)
+    return worst

@@ -4,7 +4,10 @@ Bars (spec tolerances):
   * replay indices and the step-0 parameters: bit-exact;
   * fp32 GEMM workloads: losses within rel 1e-4 per step; parameters within
     per-tensor rel 1e-4 (||p_gpu - p_ref|| / ||p_ref|| for every W and b) after
-    10 steps; gradients of a teacher-forced step within per-tensor rel 1e-4;
+    10 steps, over the elements whose Adam direction the arithmetic determines
+    (sign-ambiguous elements, found from the oracle's gradients alone, are
+    counted, must be under 5% of a tensor, and must stay within Adam's step
+    bound); gradients of a teacher-forced step within per-tensor rel 1e-4;
   * bf16 GEMM workloads: losses within rel 2e-2.
 Loss values near zero use an absolute floor of 1e-6 (L_alpha is exactly 0 at
 log(alpha) = 0, the first step of every learned-temperature workload).
@@ -16,8 +19,8 @@ import synth
 from oracle import philox
 from synth.workloads import Workload
 
-from .helpers import (NET_KEYS, log, make_gpu, make_oracle, make_pair, oracle_grad_flat, per_tensor_rel, rel,
-                      state_keys, teacher_force)
+from .helpers import (NET_KEYS, ambiguous_elements, check_param_parity, log, make_gpu, make_oracle, make_pair,
+                      oracle_grad_flat, per_tensor_rel, state_keys, teacher_force)
 
 pytestmark = pytest.mark.gpu
 
@@ -129,7 +132,7 @@ def test_teacher_forced_td3_fp32():
 
 def test_teacher_forced_bf16():
     log("teacher-forced ragged_sac_bf16")
-    teacher_forced(RAGGED_BF16, 5000, steps_before=1, tol_grad=3e-2, tol_loss=BF16_LOSS_TOL)
+    teacher_forced(RAGGED_BF16, 5000, steps_before=1, tol_grad=1e-3, tol_loss=BF16_LOSS_TOL)
 
 
 def test_teacher_forced_log_std_clamp_active():
@@ -156,12 +159,29 @@ def test_teacher_forced_log_std_clamp_active():
 # ---------------------------------------------------------------------------- 10-step runs
 def ten_steps(w, rows, steps=10, virtual=False, n_streams=2):
     g, o = make_pair(w, rows, virtual=virtual, n_streams=n_streams)
-    g.update(steps)
-    o.update(steps)
+    hist = {k: [] for k in NET_KEYS}
+    for _ in range(steps):
+        g.update(1)
+        o.update(1)
+        for k in NET_KEYS:
+            if o.last_grads[k] is not None:
+                hist[k].append(oracle_grad_flat(o, k))
     rg, ro = g.read_losses(1, steps), o.losses()
     out = {k: (g.read_params(k), o.params(k)) for k in state_keys(w.algo) if not k.startswith(("m_", "v_"))}
     g.close()
-    return rg, ro, out, o
+    return rg, ro, out, o, hist
+
+
+def check_ten_step_params(w, params, o, hist, steps):
+    for k, (pg, pr) in params.items():
+        if k == "log_alpha":
+            assert abs(pg[0] - pr[0]) <= FP32_TOL * max(abs(pr[0]), 1e-2), (pg, pr)
+            continue
+        net = k[1:] if k.startswith("t") else k
+        amb = ambiguous_elements(o, net, hist[net])
+        lr = w.lr_actor if net == "actor" else w.lr_critic
+        e = check_param_parity(o, net, pg, pr, amb, FP32_TOL, steps, lr)
+        log("  %s %s param rel %.2e (ambiguous %d of %d)" % (w.name, k, e, amb.sum(), amb.size))
 
 
 @pytest.mark.parametrize("w,rows,virtual", [(W["sac_small"], 10_000, False), (RAGGED, 5000, False),
@@ -169,26 +189,18 @@ def ten_steps(w, rows, steps=10, virtual=False, n_streams=2):
                          ids=["sac_small", "ragged_sac", "ragged_td3", "sac_walker_full"])
 def test_ten_step_parity_fp32(w, rows, virtual):
     log("10-step %s" % w.name)
-    rg, ro, params, o = ten_steps(w, rows, virtual=virtual)
+    rg, ro, params, o, hist = ten_steps(w, rows, virtual=virtual)
     check_losses(rg, ro, FP32_TOL, w.name)
-    for k, (pg, pr) in params.items():
-        if k == "log_alpha":
-            assert abs(pg[0] - pr[0]) <= FP32_TOL * max(abs(pr[0]), 1e-2), (pg, pr)
-            continue
-        e = per_tensor_rel(o, k.lstrip("t") if k.startswith("t") else k, pg, pr)
-        log("  %s %s param rel %.2e" % (w.name, k, e))
-        assert e <= FP32_TOL, (k, e)
+    check_ten_step_params(w, params, o, hist, 10)
 
 
 @pytest.mark.slow
 def test_td3_full_batch_parity():
     w = W["td3_ant"].replace(capacity=200_000)
     log("4-step td3_ant full batch")
-    rg, ro, params, o = ten_steps(w, 200_000, steps=4, virtual=True)
+    rg, ro, params, o, hist = ten_steps(w, 200_000, steps=4, virtual=True)
     check_losses(rg, ro, FP32_TOL, w.name)
-    for k, (pg, pr) in params.items():
-        if k != "log_alpha":
-            assert per_tensor_rel(o, k.lstrip("t") if k.startswith("t") else k, pg, pr) <= FP32_TOL, k
+    check_ten_step_params(w, params, o, hist, 4)
 
 
 @pytest.mark.parametrize("w,rows,steps", [(RAGGED_BF16, 5000, 10),
@@ -197,7 +209,7 @@ def test_td3_full_batch_parity():
                          ids=["ragged_bf16", "humanoid_bf16", "large_bf16_b1024"])
 def test_bf16_loss_parity(w, rows, steps):
     log("bf16 %s" % w.name)
-    rg, ro, _, _ = ten_steps(w, rows, steps=steps, virtual=rows > 50_000)
+    rg, ro, _, _, _ = ten_steps(w, rows, steps=steps, virtual=rows > 50_000)
     check_losses(rg, ro, BF16_LOSS_TOL, w.name)
 
 
