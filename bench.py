@@ -184,7 +184,7 @@ def main():
         out["roofline"] = roofline(stats, prec)
         out["kernels"] = [dict(name=s["name"], M=s["M"], N=s["N"], K=s["K"], launches=s["launches"],
                                avg_ms=round(s["avg_ms"], 5), total_ms=round(s["total_ms"], 3))
-                          for s in stats[:12]]
+                          for s in stats[:40]]
     if not args.no_cpu_baseline:
         progress("cpu baseline (oracle) at batch %d" % args.cpu_sample_batch)
         out["cpu_baseline"] = cpu_baseline(w, args.seed, args.data_seed, args.cpu_sample_batch)
