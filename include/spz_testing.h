@@ -26,6 +26,34 @@ int spzt_gemm(int32_t bf16, int32_t mode, int32_t M, int32_t N, int32_t K, int32
               int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc, const float* bias,
               const void* mask, int64_t ldm, int32_t relu, int32_t out_f32);
 
+/*
+ * Fused epilogues of the large-tile bf16 kernel (bf16 operands; the whole product
+ * must fit that kernel: M % 256 == 0, N % 128 == 0, K % 32 == 0; else SPZ_EINVAL).
+ * Bit c % 32 of word bits[(c / 32) * ldbits + r] is mask element (r, c).
+ *   mode 0: C = ReLU(A . B^T + bias) in bf16 (bias may be null);
+ *           bits_out (or null): bits of C > 0;
+ *           rdot_w [N] bf16 (or null): rdot_part[p * ldrd + r] = sum over columns c of
+ *             group p (spzt_rdot_cols(N) columns each) of C[r, c] * rdot_w[c];
+ *           no_store: C is not written (requires rdot_w).
+ *   mode 1: C = (A . B) * bit(r, c) in bf16 (bits required);
+ *           colsum (or null): colsum[t * ldcs + c] = sum of stored C[r, c] over the
+ *             256 rows r of row tile t.
+ * Synchronous.
+ */
+int spzt_gemm_fused(int32_t mode, int32_t M, int32_t N, int32_t K, const void* A, int64_t lda, const void* B,
+                    int64_t ldb, void* C, int64_t ldc, const float* bias, uint32_t* bits_out, const uint32_t* bits,
+                    int64_t ldbits, const void* rdot_w, float* rdot_part, int64_t ldrd, int32_t no_store,
+                    float* colsum, int64_t ldcs);
+/* Columns per row-dot partial of an N-column product. */
+int spzt_rdot_cols(int32_t N);
+/*
+ * Checks the device float32 -> bfloat16 rounding used by every kernel against an
+ * integer round-to-nearest-even over the float bit patterns [begin, begin + count)
+ * (begin + count <= 2^32); a NaN input must give a NaN. *mismatches receives the
+ * number of failing patterns.
+ */
+int spzt_bf16_round_check(uint64_t begin, uint64_t count, uint64_t* mismatches);
+
 #ifdef __cplusplus
 }
 #endif

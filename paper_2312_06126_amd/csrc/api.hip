@@ -85,6 +85,8 @@ struct spz_ctx {
   float *z2 = nullptr, *logp2 = nullptr, *qt1 = nullptr, *qt2 = nullptr, *y = nullptr;
   float *q1 = nullptr, *q2 = nullptr, *dq1 = nullptr, *dq2 = nullptr;
   std::vector<void*> hc[2];
+  std::vector<uint32_t*> bhc[2];     // ReLU masks of hc as bits (null where not fused)
+  float* c_rdot = nullptr;           // row-dot partials of the critic stream
   void* c_dz[2] = {nullptr, nullptr};
   float *c_wpart = nullptr, *c_cpart = nullptr, *c_cextra = nullptr;
   double* c_lpart = nullptr;
@@ -93,6 +95,8 @@ struct spz_ctx {
   float *z = nullptr, *th = nullptr, *se = nullptr, *lm = nullptr, *logp = nullptr;
   float *qp1 = nullptr, *qp2 = nullptr, *dqp1 = nullptr, *dqp2 = nullptr, *da1 = nullptr, *da2 = nullptr;
   std::vector<void*> hpc[2];
+  std::vector<uint32_t*> bha, bhpc[2];
+  float* a_rdot = nullptr;
   void* a_dz[2] = {nullptr, nullptr};
   void* dzh = nullptr;
   float *a_wpart = nullptr, *a_cpart = nullptr;
@@ -265,14 +269,23 @@ const void* wop(const spz_ctx* c, bool target, int64_t off) {
 }
 const float* wf(const spz_ctx* c, bool target, int64_t off) { return (target ? c->T : c->P) + off; }
 size_t es(const spz_ctx* c) { return c->bf16 ? 2 : 4; }
+double head_bwd_bytes(const spz_ctx* c, int K, const uint32_t* bits) {
+  return (double)c->Bp * K * es(c) + (bits ? c->Bp * K / 8.0 : (double)c->Bp * K * es(c));
+}
 const void* elem(const spz_ctx* c, const void* base, int64_t off) {
   return static_cast<const uint8_t*>(base) + off * (int64_t)es(c);
 }
 
 // Forward of net ni. X: [Bp, ldx] operand tensor (the first in_p(0) columns are read).
-// hid[l] receives hidden layer l; critic heads write q [Bp], the actor head z [Bp, out_p].
+// hid[l] receives hidden layer l and, where bits[l] is set, its ReLU mask as bits;
+// critic heads write q [Bp], the actor head z [Bp, out_p]. Where the large-tile
+// kernel covers the last hidden layer of a critic, the output layer is folded into
+// that product's epilogue (row-dot partials in rdot, summed in order afterwards);
+// the last hidden layer is then stored only when keep_last.
+bool fused_layer(const spz_ctx* c, const Lay& L) { return gemm_fused_ok(c->bf16, GEMM_FWD, c->Bp, L.out_p, L.in_p); }
+
 hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, void* const* hid,
-                   float* head, hipStream_t s) {
+                   uint32_t* const* bits, bool keep_last, float* rdot, float* head, hipStream_t s) {
   const Net& n = c->net[ni];
   const int nl = (int)n.L.size();
   const void* in = X;
@@ -289,13 +302,32 @@ hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, 
     g.B = wop(c, target, L.w); g.ldb = L.in_p;
     g.bias = wf(c, target, L.b);
     g.M = c->Bp; g.N = L.out_p; g.K = L.in_p;
+    bool folded = false;
     if (l == nl - 1) {
       g.C = head; g.ldc = L.out_p; g.relu = 0; g.out_f32 = 1;
     } else {
       g.C = hid[l]; g.ldc = L.out_p; g.relu = 1; g.out_f32 = 0;
+      if (bits && bits[l]) {
+        g.bits_out = bits[l];
+        g.ldbits = c->Bp;
+      }
+      if (ni != 0 && l == nl - 2 && fused_layer(c, L)) {
+        const Lay& H = n.L[nl - 1];
+        g.rdot_w = wop(c, target, H.w);
+        g.rdot_part = rdot;
+        g.ldrd = c->Bp;
+        g.no_store = keep_last ? 0 : 1;
+        folded = true;
+      }
     }
     HK(timed(c, "gemm_fwd", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
              [&] { return gemm(c->bf16, GEMM_FWD, g, s); }));
+    if (folded) {
+      const Lay& H = n.L[nl - 1];
+      RdotFinalArgs f{rdot, L.out_p / gemm_rdot_cols(L.out_p), c->Bp, c->Bp, wf(c, target, H.b), head};
+      return timed(c, "rdot_final", c->Bp, f.parts, 0, 0.0, 4.0 * c->Bp * (f.parts + 1), s,
+                   [&] { return launch_rdot_final(f, s); });
+    }
     in = g.C;
     ld = L.out_p;
   }
@@ -322,17 +354,24 @@ hipError_t wgrad(spz_ctx* c, const void* dz, int64_t lddz, const void* X, int64_
                [&] { return launch_colsum(c->bf16, cs, c->G + L.b, nullptr, s); });
 }
 
-// Input gradient through layer L: out[Bp, N] = (dz . W) masked by mask > 0. With
+// Input gradient through layer L: out[Bp, N] = (dz . W) masked by mask > 0 (or by
+// the mask bits when given). With
 // bias_out, also the column sums of the stored out (the bias gradient of the layer
 // below): fused into the product's epilogue where the large-tile kernel covers it.
 hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_t ldw, int N,
-                 const void* mask, void* out, int64_t ldo, bool out_f32, float* bias_out, float* cpart,
-                 hipStream_t s) {
+                 const void* mask, const uint32_t* bits, void* out, int64_t ldo, bool out_f32, float* bias_out,
+                 float* cpart, hipStream_t s) {
   GemmArgs g{};
   g.A = dz; g.lda = L.out_p;
   g.B = W; g.ldb = ldw;
   g.C = out; g.ldc = ldo; g.out_f32 = out_f32 ? 1 : 0;
-  g.mask = mask; g.ldm = ldo;
+  if (bits) {
+    g.bits = bits;
+    g.ldbits = c->Bp;
+  } else if (mask) {
+    g.mask = mask;
+    g.ldm = ldo;
+  }
   g.M = c->Bp; g.N = N; g.K = L.out_p;
   const bool fused = bias_out && gemm_colsum_fused(c->bf16, GEMM_DGRAD, g.M, g.N, g.K);
   if (fused) {
@@ -353,15 +392,15 @@ hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_
 // Critic ni in {1, 2}: weight and bias gradients of L = sum_b dq[b] q[b] given the
 // stored hidden activations hid of the forward on X.
 hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, void* const* hid,
-                           hipStream_t s) {
+                           uint32_t* const* bits, hipStream_t s) {
   const Net& n = c->net[ni];
   const int nl = (int)n.L.size();
   const Lay& H = n.L[nl - 1];
   ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, c->c_cpart, c->c_cextra};
   HK(timed(c, "colsum", c->Bp, H.in_p, 1, 0.0, (double)c->Bp * H.in_p * es(c), s,
            [&] { return launch_colsum(c->bf16, cs, c->G + H.w, c->G + H.b, s); }));
-  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp};
-  HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, 2.0 * c->Bp * H.in_p * es(c), s,
+  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp};
+  HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, head_bwd_bytes(c, H.in_p, bits[nl - 2]), s,
            [&] { return launch_head_bwd(c->bf16, hb, s); }));
   // dz of the last hidden layer comes from the head backward; its bias gradient is a
   // separate column sum. Every later dz comes from a dgrad that also produces its
@@ -373,8 +412,8 @@ hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, v
     const int64_t ldx = l == 0 ? c->Kc : L.in_p;
     HK(wgrad(c, c->c_dz[cur], L.out_p, Xl, ldx, L, c->c_wpart, c->c_cpart, l == nl - 2, s));
     if (l > 0) {
-      HK(dgrad(c, c->c_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], c->c_dz[cur ^ 1],
-               L.in_p, false, c->G + n.L[l - 1].b, c->c_cpart, s));
+      HK(dgrad(c, c->c_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], bits[l - 1],
+               c->c_dz[cur ^ 1], L.in_p, false, c->G + n.L[l - 1].b, c->c_cpart, s));
       cur ^= 1;
     }
   }
@@ -382,23 +421,23 @@ hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, v
 }
 
 // Gradient of sum_b dq[b] Q_ni(s, a)[b] with respect to the action block, into da [Bp, Ap].
-hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* hid, float* da,
-                              hipStream_t s) {
+hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* hid, uint32_t* const* bits,
+                              float* da, hipStream_t s) {
   const Net& n = c->net[ni];
   const int nl = (int)n.L.size();
   const Lay& H = n.L[nl - 1];
-  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->a_dz[0], H.in_p, H.in_p, c->Bp};
-  HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, 2.0 * c->Bp * H.in_p * es(c), s,
+  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->a_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp};
+  HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, head_bwd_bytes(c, H.in_p, bits[nl - 2]), s,
            [&] { return launch_head_bwd(c->bf16, hb, s); }));
   int cur = 0;
   for (int l = nl - 2; l >= 1; --l) {
     const Lay& L = n.L[l];
-    HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], c->a_dz[cur ^ 1],
-             L.in_p, false, nullptr, nullptr, s));
+    HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], bits[l - 1],
+             c->a_dz[cur ^ 1], L.in_p, false, nullptr, nullptr, s));
     cur ^= 1;
   }
   const Lay& L0 = n.L[0];
-  return dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, c->Ap, nullptr, da,
+  return dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, c->Ap, nullptr, nullptr, da,
                c->Ap, true, nullptr, nullptr, s);
 }
 
@@ -413,8 +452,8 @@ hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
     const int64_t ldx = l == 0 ? c->Kc : L.in_p;
     HK(wgrad(c, cur, L.out_p, Xl, ldx, L, c->a_wpart, c->a_cpart, l == nl - 1, s));
     if (l > 0) {
-      HK(dgrad(c, cur, L, wop(c, false, L.w), L.in_p, L.in_p, c->ha[l - 1], c->a_dz[nxt], L.in_p, false,
-               c->G + n.L[l - 1].b, c->a_cpart, s));
+      HK(dgrad(c, cur, L, wop(c, false, L.w), L.in_p, L.in_p, c->ha[l - 1], c->bha[l - 1], c->a_dz[nxt],
+               L.in_p, false, c->G + n.L[l - 1].b, c->a_cpart, s));
       cur = c->a_dz[nxt];
       nxt ^= 1;
     }
@@ -430,27 +469,27 @@ hipError_t critic_part(spz_ctx* c, hipStream_t s) {
   const int pa = c->net[0].L.back().out_p;
   const spz_hparams& hp = c->hp;
   if (!c->td3) {
-    HK(forward(c, 0, false, c->xs2, c->Kc, c->scratch.data(), c->z2, s));
+    HK(forward(c, 0, false, c->xs2, c->Kc, c->scratch.data(), nullptr, true, nullptr, c->z2, s));
     SacHeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_TGT, hp.log_std_min, hp.log_std_max,
                   c->xs2, c->Kc, c->Ka, c->logp2, nullptr, nullptr, nullptr};
     HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, h, s); }));
   } else {
-    HK(forward(c, 0, true, c->xs2, c->Kc, c->scratch.data(), c->z2, s));
+    HK(forward(c, 0, true, c->xs2, c->Kc, c->scratch.data(), nullptr, true, nullptr, c->z2, s));
     Td3HeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, 1, hp.policy_noise, hp.noise_clip,
                   c->xs2, c->Kc, c->Ka, nullptr};
     HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
-  HK(forward(c, 1, true, c->xs2, c->Kc, c->scratch.data(), c->qt1, s));
-  HK(forward(c, 2, true, c->xs2, c->Kc, c->scratch.data(), c->qt2, s));
+  HK(forward(c, 1, true, c->xs2, c->Kc, c->scratch.data(), nullptr, false, c->c_rdot, c->qt1, s));
+  HK(forward(c, 2, true, c->xs2, c->Kc, c->scratch.data(), nullptr, false, c->c_rdot, c->qt2, s));
   TdArgs td{c->qt1, c->qt2, c->r, c->d, c->td3 ? nullptr : c->logp2, log_alpha_ptr(c), c->y, hp.gamma,
             c->B, c->Bp};
   HK(timed(c, "td_target", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_td_target(td, s); }));
-  HK(forward(c, 1, false, c->xsa, c->Kc, c->hc[0].data(), c->q1, s));
-  HK(forward(c, 2, false, c->xsa, c->Kc, c->hc[1].data(), c->q2, s));
+  HK(forward(c, 1, false, c->xsa, c->Kc, c->hc[0].data(), c->bhc[0].data(), true, c->c_rdot, c->q1, s));
+  HK(forward(c, 2, false, c->xsa, c->Kc, c->hc[1].data(), c->bhc[1].data(), true, c->c_rdot, c->q2, s));
   CriticLossArgs cl{c->q1, c->q2, c->y, c->dq1, c->dq2, c->c_lpart, c->B, c->Bp};
   HK(timed(c, "critic_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_critic_loss(cl, s); }));
-  HK(critic_backward(c, 1, c->dq1, c->xsa, c->hc[0].data(), s));
-  HK(critic_backward(c, 2, c->dq2, c->xsa, c->hc[1].data(), s));
+  HK(critic_backward(c, 1, c->dq1, c->xsa, c->hc[0].data(), c->bhc[0].data(), s));
+  HK(critic_backward(c, 2, c->dq2, c->xsa, c->hc[1].data(), c->bhc[1].data(), s));
   return hipSuccess;
 }
 
@@ -459,7 +498,7 @@ hipError_t critic_part(spz_ctx* c, hipStream_t s) {
 hipError_t actor_part(spz_ctx* c, hipStream_t s) {
   const int pa = c->net[0].L.back().out_p;
   const spz_hparams& hp = c->hp;
-  HK(forward(c, 0, false, c->xsa, c->Kc, c->ha.data(), c->z, s));
+  HK(forward(c, 0, false, c->xsa, c->Kc, c->ha.data(), c->bha.data(), true, nullptr, c->z, s));
   if (!c->td3) {
     SacHeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_POL, hp.log_std_min, hp.log_std_max,
                   c->xsp, c->Kc, c->Ka, c->logp, c->th, c->se, c->lm};
@@ -468,13 +507,14 @@ hipError_t actor_part(spz_ctx* c, hipStream_t s) {
     Td3HeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, 0, 0.0f, 0.0f, c->xsp, c->Kc, c->Ka, c->th};
     HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
-  HK(forward(c, 1, false, c->xsp, c->Kc, c->hpc[0].data(), c->qp1, s));
-  if (!c->td3) HK(forward(c, 2, false, c->xsp, c->Kc, c->hpc[1].data(), c->qp2, s));
+  HK(forward(c, 1, false, c->xsp, c->Kc, c->hpc[0].data(), c->bhpc[0].data(), false, c->a_rdot, c->qp1, s));
+  if (!c->td3)
+    HK(forward(c, 2, false, c->xsp, c->Kc, c->hpc[1].data(), c->bhpc[1].data(), false, c->a_rdot, c->qp2, s));
   ActorLossArgs al{c->qp1, c->td3 ? nullptr : c->qp2, c->logp, log_alpha_ptr(c), c->dqp1,
                    c->td3 ? nullptr : c->dqp2, c->a_lpart, c->B, c->Bp};
   HK(timed(c, "actor_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_actor_loss(al, s); }));
-  HK(critic_action_grad(c, 1, c->dqp1, c->hpc[0].data(), c->da1, s));
-  if (!c->td3) HK(critic_action_grad(c, 2, c->dqp2, c->hpc[1].data(), c->da2, s));
+  HK(critic_action_grad(c, 1, c->dqp1, c->hpc[0].data(), c->bhpc[0].data(), c->da1, s));
+  if (!c->td3) HK(critic_action_grad(c, 2, c->dqp2, c->hpc[1].data(), c->bhpc[1].data(), c->da2, s));
   ActorHeadBwdArgs hb{c->da1, c->td3 ? nullptr : c->da2, c->Ap, c->th, c->se, c->lm, log_alpha_ptr(c),
                       c->dzh, pa, c->A, c->B, c->td3 ? 0 : 1};
   HK(timed(c, "actor_head_bwd", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_actor_head_bwd(c->bf16, hb, s); }));
@@ -612,6 +652,30 @@ int setup(spz_ctx* c) {
   for (int l = 0; l < nh; ++l) {
     CK(dalloc(c, &c->ha[l], (size_t)Bp * pad32(c->hidden[l]) * e));
     c->scratch[l] = c->cs_h[l & 1];
+  }
+  // ReLU masks as bits where the large-tile kernel produces and consumes them (the
+  // same condition holds for every product that reads a layer's mask), and the
+  // row-dot partials of the folded critic output layers.
+  for (int i = 0; i < 2; ++i) {
+    c->bhc[i].assign(nh, nullptr);
+    c->bhpc[i].assign(nh, nullptr);
+  }
+  c->bha.assign(nh, nullptr);
+  int rd_parts = 0;
+  for (int l = 0; l < nh; ++l) {
+    const int w = pad32(c->hidden[l]);
+    if (!gemm_fused_ok(c->bf16, GEMM_FWD, (int)Bp, w, 32)) continue;
+    const size_t bb = (size_t)Bp * (w / 32) * 4;
+    for (int i = 0; i < 2; ++i) {
+      CK(dalloc_t(c, &c->bhc[i][l], bb));
+      CK(dalloc_t(c, &c->bhpc[i][l], bb));
+    }
+    CK(dalloc_t(c, &c->bha[l], bb));
+    if (l == nh - 1) rd_parts = w / gemm_rdot_cols(w);
+  }
+  if (rd_parts) {
+    CK(dalloc_t(c, &c->c_rdot, (size_t)rd_parts * Bp * 4));
+    CK(dalloc_t(c, &c->a_rdot, (size_t)rd_parts * Bp * 4));
   }
   // reduction workspaces
   int64_t wmax = 0, cmax = 0;

@@ -331,8 +331,23 @@ bool gemm_colsum_fused(bool bf16, GemmMode mode, int M, int N, int K) {
   return bf16 && N % 128 == 0 && big_gemm_colsum(mode, M, N, K);
 }
 
+bool gemm_fused_ok(bool bf16, GemmMode mode, int M, int N, int K) {
+  return bf16 && N % 128 == 0 && big_gemm_fits(mode, M, N, K, 1);
+}
+
 hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   if (g.colsum && !gemm_colsum_fused(bf16, mode, g.M, g.N, g.K)) return hipErrorInvalidValue;
+  // Epilogue features of the large-tile kernel only: the whole product must run there.
+  const bool fused = g.bits_out || g.bits || g.rdot_w || g.no_store;
+  if (fused) {
+    if (mode == GEMM_WGRAD || !gemm_fused_ok(bf16, mode, g.M, g.N, g.K)) return hipErrorInvalidValue;
+    if ((g.bits_out || g.bits) && (g.ldbits < g.M || ((uintptr_t)(g.bits_out ? (const void*)g.bits_out : g.bits) & 3)))
+      return hipErrorInvalidValue;
+    if (g.rdot_w && (!g.rdot_part || g.ldrd < g.M || ((uintptr_t)g.rdot_w & 15))) return hipErrorInvalidValue;
+    if (g.no_store && !g.rdot_w) return hipErrorInvalidValue;
+    if (g.bits && g.mask) return hipErrorInvalidValue;
+    if (!big_epilogue_supported(mode, epilogue_flags(mode, g))) return hipErrorInvalidValue;
+  }
   // Shape contract: tiles divide the problem, K slices are whole BK steps,
   // operand rows are 16-byte aligned.
   if (g.M <= 0 || g.N <= 0 || g.K <= 0) return hipErrorInvalidValue;
@@ -340,7 +355,8 @@ hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   if (g.lda % vec || g.ldb % vec) return hipErrorInvalidValue;
   if (mode == GEMM_WGRAD && (g.splits < 1 || g.K % g.splits)) return hipErrorInvalidValue;
   const int n_big = g.N / 128 * 128;
-  if (bf16 && n_big > 0 && big_gemm_fits(mode, g.M, n_big, g.K, mode == GEMM_WGRAD ? g.splits : 1)) {
+  if (bf16 && n_big > 0 && big_gemm_fits(mode, g.M, n_big, g.K, mode == GEMM_WGRAD ? g.splits : 1) &&
+      big_epilogue_supported(mode, epilogue_flags(mode, g))) {
     hipError_t e = gemm_big(mode, column_slice(bf16, mode, g, 0, n_big), s);
     if (e != hipSuccess || n_big == g.N) return e;
     return gemm_generic(bf16, mode, column_slice(bf16, mode, g, n_big, g.N - n_big), s);

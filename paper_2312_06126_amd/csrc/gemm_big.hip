@@ -87,99 +87,156 @@ __device__ inline bf16x8 frag(const bf16_t* lds, int rb, int ks, int lane) {
 // lane handles 8 consecutive columns of one row: 16-byte loads of mask and bias and
 // 16-byte (bf16) or 32-byte (fp32) stores. 32x32 accumulator layout: lane holds
 // column lane%32; register q holds row 8*(q/4) + 4*(lane/32) + q%4 of the block.
-// CSUM (dgrad): column sums of the stored (rounded) values over the tile's 256 rows
-// go to g.colsum[mt, :]: per lane over its rows, a fixed butterfly over the 16 lanes
-// of a column group, then the WM waves of the column in order through LDS.
+// The four lanes 4r..4r+3 hold the 32 columns of one row of a 32x32 block.
+//   CSUM (dgrad): column sums of the stored (rounded) values over the tile's 256
+//     rows go to g.colsum[mt, :]: per lane over its rows, a fixed butterfly over the
+//     16 lanes of a column group, then the WM waves of the column in order via LDS.
+//   BITS_OUT (fwd): one bit per stored value (> 0), 32 columns per word, words of
+//     one 32-column block stored row-contiguously.
+//   BITS (dgrad): the same bits as the mask.
+//   RDOT (fwd): per row, the dot product of the stored values of the wave's
+//     BN/WN columns with rdot_w, one partial per (column tile, wave column).
+//   NOSTORE (fwd): C itself is not written.
 constexpr int SCR_PITCH = 36;   // floats per scratch row
 
-template <int MODE, int BN, bool MASK, bool OUTF32, bool RELU, bool CSUM>
+// One 32x32 accumulator block (i, j) of the wave: cs accumulates the column sums of
+// the lane's 8 columns, rd[p] the row dots of the lane's rows r and r + 16.
+template <int MODE, int BN, int F>
+__device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int j, int m0, int n0, int wm, int wn,
+                                 int lane, int z, float* scr, float (&cs)[8], float (&rd)[2]) {
+  constexpr int WCOLS = BN / WN;
+  constexpr bool OUTF32 = F & EPI_F32, RELU = F & EPI_RELU, MASK = F & EPI_MASK, BITS = F & EPI_BITS;
+  constexpr bool BITS_OUT = F & EPI_BITS_OUT, CSUM = F & EPI_CSUM, RDOT = F & EPI_RDOT;
+  constexpr bool STORE = !(F & EPI_NOSTORE);
+  const int cgrp = lane & 3, rsub = lane >> 2;
+  const int cw = wn * WCOLS + 32 * j;   // first column of the 32-column block in the tile
+  const int cb = cw + 8 * cgrp;
+  float bias[8];
+  uint32_t ww[4] = {0u, 0u, 0u, 0u};   // rdot_w of the lane's 8 columns, packed bf16
+#pragma unroll
+  for (int e = 0; e < 8; ++e) bias[e] = 0.0f;
+  if constexpr (MODE == GEMM_FWD) {
+    if (g.bias) {
+      const float4 b0 = *reinterpret_cast<const float4*>(g.bias + n0 + cb);
+      const float4 b1 = *reinterpret_cast<const float4*>(g.bias + n0 + cb + 4);
+      bias[0] = b0.x; bias[1] = b0.y; bias[2] = b0.z; bias[3] = b0.w;
+      bias[4] = b1.x; bias[5] = b1.y; bias[6] = b1.z; bias[7] = b1.w;
+    }
+  }
+  if constexpr (RDOT) {
+    const uint4 w4 = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(g.rdot_w) + n0 + cb);
+    ww[0] = w4.x; ww[1] = w4.y; ww[2] = w4.z; ww[3] = w4.w;
+  }
+  // The wave reads back what it wrote; LDS operations of one wave complete in order.
+#pragma unroll
+  for (int q = 0; q < 16; ++q)
+    scr[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * SCR_PITCH + (lane & 31)] = a[q];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int r = rsub + 16 * p;
+    const int64_t row = m0 + wm * (BM / WM) + 32 * i + r;
+    const float4 x0 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp);
+    const float4 x1 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp + 4);
+    float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+    if constexpr (MODE == GEMM_WGRAD) {
+      float* dst = static_cast<float*>(g.C) + ((int64_t)z * g.M + row) * g.ldc + n0 + cb;
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      continue;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if constexpr (MODE == GEMM_FWD) v[e] += bias[e];
+      if constexpr (RELU) v[e] = v[e] < 0.0f ? 0.0f : v[e];
+    }
+    if constexpr (MASK) {
+      const uint4 mk = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(g.mask) + row * g.ldm + n0 + cb);
+      const uint32_t mw[4] = {mk.x, mk.y, mk.z, mk.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float h = bf2f((bf16_t)((mw[e >> 1] >> (16 * (e & 1))) & 0xFFFFu));
+        v[e] = h > 0.0f ? v[e] : 0.0f;
+      }
+    }
+    if constexpr (BITS) {
+      const uint32_t wd = g.bits[(int64_t)((n0 + cw) >> 5) * g.ldbits + row] >> (8 * cgrp);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (wd >> e) & 1u ? v[e] : 0.0f;
+    }
+    if constexpr (OUTF32) {
+      float* dst = static_cast<float*>(g.C) + row * g.ldc + n0 + cb;
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+    } else {
+      uint32_t w[4], bt = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        w[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
+        const float hl = __uint_as_float(w[e] << 16), hh = __uint_as_float(w[e] & 0xFFFF0000u);
+        if constexpr (CSUM) {
+          cs[2 * e] += hl;
+          cs[2 * e + 1] += hh;
+        }
+        if constexpr (RDOT) {
+          rd[p] = fmaf(hl, __uint_as_float(ww[e] << 16), rd[p]);
+          rd[p] = fmaf(hh, __uint_as_float(ww[e] & 0xFFFF0000u), rd[p]);
+        }
+        if constexpr (BITS_OUT) bt |= (hl > 0.0f ? 1u : 0u) << (2 * e) | (hh > 0.0f ? 1u : 0u) << (2 * e + 1);
+      }
+      if constexpr (BITS_OUT) {
+        bt <<= 8 * cgrp;
+        bt |= __shfl_xor(bt, 1);
+        bt |= __shfl_xor(bt, 2);
+        if (cgrp == 0) g.bits_out[(int64_t)((n0 + cw) >> 5) * g.ldbits + row] = bt;
+      }
+      if constexpr (STORE)
+        *reinterpret_cast<uint4*>(static_cast<bf16_t*>(g.C) + row * g.ldc + n0 + cb) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+}
+
+// Epilogue. Accumulator blocks leave through a per-wave LDS scratch so that each
+// lane handles 8 consecutive columns of one row: 16-byte loads of mask and bias and
+// 16-byte (bf16) or 32-byte (fp32) stores. 32x32 accumulator layout: lane holds
+// column lane%32; register q holds row 8*(q/4) + 4*(lane/32) + q%4 of the block.
+// The four lanes 4r..4r+3 hold the 32 columns of one row of a 32x32 block.
+//   CSUM (dgrad): column sums of the stored (rounded) values over the tile's 256
+//     rows go to g.colsum[mt, :]: per lane over its rows, a fixed butterfly over the
+//     16 lanes of a column group, then the WM waves of the column in order via LDS.
+//   BITS_OUT (fwd): one bit per stored value (> 0), 32 columns per word, words of
+//     one 32-column block stored row-contiguously.
+//   BITS (dgrad): the same bits as the mask.
+//   RDOT (fwd): per row, the dot product of the stored values of the wave's
+//     BN/WN columns with rdot_w, one partial per (column tile, wave column).
+//   NOSTORE (fwd): C itself is not written.
+// Blocks go column-block-major when column sums accumulate over row blocks and
+// row-block-major otherwise, so that only the running sums of one block row or
+// column stay live.
+template <int MODE, int BN, int F>
 __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0,
                                 int n0, int wm, int wn, int lane, int wave, int z, int mt, float* smem_f) {
-  constexpr int TM_ = BM / WM / 32, TN_ = BN / WN / 32;
+  constexpr int TM_ = BM / WM / 32, TN_ = BN / WN / 32, WCOLS = BN / WN;
   float* scr = smem_f + wave * (32 * SCR_PITCH);
   float* csh = smem_f + (NT / 64) * 32 * SCR_PITCH;   // [WM][BN]
   const int cgrp = lane & 3, rsub = lane >> 2;
+  if constexpr ((F & EPI_CSUM) != 0) {
 #pragma unroll
-  for (int j = 0; j < TN_; ++j) {
-    const int cb = wn * (BN / WN) + 32 * j + 8 * cgrp;
-    float bias[8];
+    for (int j = 0; j < TN_; ++j) {
+      float cs[8], rd[2];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) bias[e] = 0.0f;
-    if constexpr (MODE == GEMM_FWD) {
-      if (g.bias) {
-        const float4 b0 = *reinterpret_cast<const float4*>(g.bias + n0 + cb);
-        const float4 b1 = *reinterpret_cast<const float4*>(g.bias + n0 + cb + 4);
-        bias[0] = b0.x; bias[1] = b0.y; bias[2] = b0.z; bias[3] = b0.w;
-        bias[4] = b1.x; bias[5] = b1.y; bias[6] = b1.z; bias[7] = b1.w;
-      }
-    }
-    float cs[8];
+      for (int e = 0; e < 8; ++e) cs[e] = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) cs[e] = 0.0f;
-#pragma unroll
-    for (int i = 0; i < TM_; ++i) {
-      // The wave reads back what it wrote; LDS operations of one wave complete in order.
-#pragma unroll
-      for (int q = 0; q < 16; ++q)
-        scr[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * SCR_PITCH + (lane & 31)] = acc[i][j][q];
-#pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const int r = rsub + 16 * p;
-        const int64_t row = m0 + wm * (BM / WM) + 32 * i + r;
-        const float4 x0 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp);
-        const float4 x1 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp + 4);
-        float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-        if constexpr (MODE == GEMM_WGRAD) {
-          float* dst = static_cast<float*>(g.C) + ((int64_t)z * g.M + row) * g.ldc + n0 + cb;
-          *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
-          *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            if constexpr (MODE == GEMM_FWD) v[e] += bias[e];
-            if constexpr (RELU) v[e] = v[e] < 0.0f ? 0.0f : v[e];
-          }
-          if constexpr (MASK) {
-            const uint4 mk = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(g.mask) + row * g.ldm + n0 + cb);
-            const uint32_t mw[4] = {mk.x, mk.y, mk.z, mk.w};
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const float h = bf2f((bf16_t)((mw[e >> 1] >> (16 * (e & 1))) & 0xFFFFu));
-              v[e] = h > 0.0f ? v[e] : 0.0f;
-            }
-          }
-          if constexpr (OUTF32) {
-            float* dst = static_cast<float*>(g.C) + row * g.ldc + n0 + cb;
-            *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
-            *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
-          } else {
-            uint32_t w[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const bf16_t lo = f2bf(v[2 * e]), hi = f2bf(v[2 * e + 1]);
-              w[e] = (uint32_t)lo | ((uint32_t)hi << 16);
-              if constexpr (CSUM) {
-                cs[2 * e] += bf2f(lo);
-                cs[2 * e + 1] += bf2f(hi);
-              }
-            }
-            *reinterpret_cast<uint4*>(static_cast<bf16_t*>(g.C) + row * g.ldc + n0 + cb) = make_uint4(w[0], w[1], w[2], w[3]);
-          }
-        }
-      }
-    }
-    if constexpr (CSUM) {
+      for (int i = 0; i < TM_; ++i)
+        epi_block<MODE, BN, F>(g, acc[i][j], i, j, m0, n0, wm, wn, lane, z, scr, cs, rd);
 #pragma unroll
       for (int o = 4; o < 64; o <<= 1)
 #pragma unroll
         for (int e = 0; e < 8; ++e) cs[e] += __shfl_xor(cs[e], o);
       if (rsub == 0)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) csh[wm * BN + cb + e] = cs[e];
+        for (int e = 0; e < 8; ++e) csh[wm * BN + wn * WCOLS + 32 * j + 8 * cgrp + e] = cs[e];
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  if constexpr (CSUM) {
     __syncthreads();
     for (int c = threadIdx.x; c < BN; c += NT) {
       float t = 0.0f;
@@ -187,10 +244,36 @@ __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM /
       for (int w = 0; w < WM; ++w) t += csh[w * BN + c];
       g.colsum[(int64_t)mt * g.ldcs + n0 + c] = t;
     }
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM_; ++i) {
+      float cs[8], rd[2] = {0.0f, 0.0f};
+#pragma unroll
+      for (int j = 0; j < TN_; ++j) {
+        epi_block<MODE, BN, F>(g, acc[i][j], i, j, m0, n0, wm, wn, lane, z, scr, cs, rd);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // Compiler-only fence: the bias and weight loads of the next block row are
+      // issued again instead of being kept live in registers from this one.
+      asm volatile("" ::: "memory");
+      if constexpr ((F & EPI_RDOT) != 0) {
+        const int part = (n0 + wn * WCOLS) / WCOLS;
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          float t = rd[p];
+          t += __shfl_xor(t, 1);
+          t += __shfl_xor(t, 2);
+          if (cgrp == 0) g.rdot_part[(int64_t)part * g.ldrd + m0 + wm * (BM / WM) + 32 * i + rsub + 16 * p] = t;
+        }
+      }
+    }
   }
 }
 
-template <int MODE, int BN>
+// One kernel per (product, column tile, epilogue variant): a runtime switch over the
+// variants inside one kernel let common code move above the switch and raised the
+// register pressure of every variant to the point of spilling.
+template <int MODE, int BN, int F>
 __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int tiles_n) {
   constexpr bool AKC = MODE != GEMM_WGRAD;
   constexpr bool BKC = MODE == GEMM_FWD;
@@ -272,24 +355,11 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
 
   // Epilogue variants are compile-time so the store loops unroll completely. The
   // final barrier of the k loop has released the LDS tiles for the scratch.
-  float* smem_f = reinterpret_cast<float*>(smem);
-  if constexpr (MODE == GEMM_WGRAD) {
-    epilogue<MODE, BN, false, true, false, false>(g, acc, m0, n0, wm, wn, lane, wave, z, mt, smem_f);
-  } else if constexpr (MODE == GEMM_FWD) {
-    if (g.out_f32) epilogue<MODE, BN, false, true, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
-    else if (g.relu) epilogue<MODE, BN, false, false, true, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
-    else epilogue<MODE, BN, false, false, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
-  } else {
-    if (g.out_f32) epilogue<MODE, BN, false, true, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
-    else if (g.mask && g.colsum) epilogue<MODE, BN, true, false, false, true>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
-    else if (g.mask) epilogue<MODE, BN, true, false, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
-    else if (g.colsum) epilogue<MODE, BN, false, false, false, true>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
-    else epilogue<MODE, BN, false, false, false, false>(g, acc, m0, n0, wm, wn, lane, wave, 0, mt, smem_f);
-  }
+  epilogue<MODE, BN, F>(g, acc, m0, n0, wm, wn, lane, wave, z, mt, reinterpret_cast<float*>(smem));
 }
 
-template <int MODE, int BN>
-hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
+template <int MODE, int BN, int F>
+hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
   using TA = BigTile<MODE != GEMM_WGRAD, BM>;
   using TB = BigTile<MODE == GEMM_FWD, BN>;
   const size_t tiles = 2 * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
@@ -297,18 +367,74 @@ hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
   const size_t lds = tiles > scratch ? tiles : scratch;
   static bool attr = false;
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_gemm_big<MODE, BN>,
+    hipError_t e = hipFuncSetAttribute((const void*)k_gemm_big<MODE, BN, F>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int tiles_m = g.M / BM, tiles_n = g.N / BN;
   const int splits = MODE == GEMM_WGRAD ? g.splits : 1;
-  k_gemm_big<MODE, BN><<<tiles_m * tiles_n * splits, NT, lds, s>>>(g, tiles_m, tiles_n);
+  k_gemm_big<MODE, BN, F><<<tiles_m * tiles_n * splits, NT, lds, s>>>(g, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
+template <int MODE, int BN>
+hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
+#define SPZ_CASE(F) \
+  case (F): return launch_big_f<MODE, BN, (F)>(g, s)
+  if constexpr (MODE == GEMM_WGRAD) {
+    return launch_big_f<MODE, BN, EPI_F32>(g, s);
+  } else if constexpr (MODE == GEMM_FWD) {
+    switch (epilogue_flags((GemmMode)MODE, g)) {
+      SPZ_CASE(EPI_F32);
+      SPZ_CASE(0);
+      SPZ_CASE(EPI_RELU);
+      SPZ_CASE(EPI_RELU | EPI_BITS_OUT);
+      SPZ_CASE(EPI_RELU | EPI_RDOT);
+      SPZ_CASE(EPI_RELU | EPI_RDOT | EPI_NOSTORE);
+      SPZ_CASE(EPI_RELU | EPI_BITS_OUT | EPI_RDOT);
+      SPZ_CASE(EPI_RELU | EPI_BITS_OUT | EPI_RDOT | EPI_NOSTORE);
+    }
+  } else {
+    switch (epilogue_flags((GemmMode)MODE, g)) {
+      SPZ_CASE(EPI_F32);
+      SPZ_CASE(0);
+      SPZ_CASE(EPI_MASK);
+      SPZ_CASE(EPI_MASK | EPI_CSUM);
+      SPZ_CASE(EPI_CSUM);
+      SPZ_CASE(EPI_BITS);
+      SPZ_CASE(EPI_BITS | EPI_CSUM);
+    }
+  }
+#undef SPZ_CASE
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
+
+int gemm_rdot_cols(int N) { return (N % 256 == 0 ? 256 : 128) / WN; }
+
+bool big_epilogue_supported(GemmMode mode, int f) {
+  switch (mode) {
+    case GEMM_WGRAD: return f == EPI_F32;
+    case GEMM_FWD:
+      switch (f) {
+        case EPI_F32: case 0: case EPI_RELU: case EPI_RELU | EPI_BITS_OUT: case EPI_RELU | EPI_RDOT:
+        case EPI_RELU | EPI_RDOT | EPI_NOSTORE: case EPI_RELU | EPI_BITS_OUT | EPI_RDOT:
+        case EPI_RELU | EPI_BITS_OUT | EPI_RDOT | EPI_NOSTORE:
+          return true;
+      }
+      return false;
+    case GEMM_DGRAD:
+      switch (f) {
+        case EPI_F32: case 0: case EPI_MASK: case EPI_MASK | EPI_CSUM: case EPI_CSUM: case EPI_BITS:
+        case EPI_BITS | EPI_CSUM:
+          return true;
+      }
+      return false;
+  }
+  return false;
+}
 
 bool big_gemm_colsum(GemmMode mode, int M, int N, int K) {
   return mode == GEMM_DGRAD && big_gemm_fits(mode, M, N, K, 1);

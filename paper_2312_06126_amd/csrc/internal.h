@@ -20,13 +20,30 @@ __host__ __device__ inline float bf2f(bf16_t h) {
   return v.f;
 }
 
-// float32 -> bfloat16, round to nearest, ties to even; NaN stays NaN.
+// float32 -> bfloat16, round to nearest, ties to even (subnormals kept); NaN stays
+// NaN. On the device this is the hardware conversion (v_cvt_pk_bf16_f32).
 __host__ __device__ inline bf16_t f2bf(float f) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_bit_cast(bf16_t, (__bf16)f);
+#else
   union { uint32_t u; float f; } v;
   v.f = f;
   if ((v.u & 0x7F800000u) == 0x7F800000u && (v.u & 0x007FFFFFu)) return (bf16_t)0x7FC0;
   uint32_t r = v.u + 0x7FFFu + ((v.u >> 16) & 1u);
   return (bf16_t)(r >> 16);
+#endif
+}
+
+// Two values rounded as f2bf, lo in the low half (one instruction on the device).
+__host__ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+#else
+  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+#endif
 }
 
 template <typename T> __host__ __device__ inline float to_f(T x);
@@ -83,7 +100,38 @@ struct GemmArgs {
   int splits;                  // WGRAD: number of K slices; C gets splits * M * ldc floats
   float* colsum; int64_t ldcs; // DGRAD (bf16 large-tile only): column sums of the stored C
                                // per 256-row tile, colsum[M / 256, ldcs]
+  // Large-tile bf16 epilogue features (the whole product must run on that kernel,
+  // see gemm_fused_ok). Bit c % 32 of word bits[(c / 32) * ldbits + r] is element
+  // (r, c) of a ReLU mask.
+  uint32_t* bits_out;          // FWD with relu: mask of the stored C (C[r, c] > 0)
+  const uint32_t* bits;        // DGRAD: C *= mask bit (instead of mask)
+  int64_t ldbits;
+  const void* rdot_w;          // FWD with relu: rdot_part[p, r] = sum over the p-th group of
+  float* rdot_part;            // gemm_rdot_cols(N) columns c of stored C[r, c] * rdot_w[c]
+  int64_t ldrd;
+  int no_store;                // FWD with rdot_w: C is not written
 };
+
+enum EpilogueFlag : int {
+  EPI_F32 = 1, EPI_RELU = 2, EPI_MASK = 4, EPI_BITS = 8, EPI_BITS_OUT = 16, EPI_CSUM = 32,
+  EPI_RDOT = 64, EPI_NOSTORE = 128
+};
+
+__host__ __device__ inline int epilogue_flags(GemmMode mode, const GemmArgs& g) {
+  if (mode == GEMM_WGRAD) return EPI_F32;
+  int f = g.out_f32 ? EPI_F32 : 0;
+  if (mode == GEMM_FWD) {
+    if (g.relu) f |= EPI_RELU;
+    if (g.bits_out) f |= EPI_BITS_OUT;
+    if (g.rdot_w) f |= EPI_RDOT;
+    if (g.no_store) f |= EPI_NOSTORE;
+  } else {
+    if (g.mask) f |= EPI_MASK;
+    if (g.bits) f |= EPI_BITS;
+    if (g.colsum) f |= EPI_CSUM;
+  }
+  return f;
+}
 
 // C = A B with A: [M, K] k-contiguous (FWD, DGRAD) or [K, M] (WGRAD),
 // B: [N, K] (FWD) or [K, N] (DGRAD, WGRAD). Returns a hipError_t.
@@ -99,5 +147,12 @@ bool big_gemm_fits(GemmMode mode, int M, int N, int K, int splits);
 bool gemm_colsum_fused(bool bf16, GemmMode mode, int M, int N, int K);
 bool big_gemm_colsum(GemmMode mode, int M, int N, int K);
 hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s);
+// True when a product of this shape runs entirely on the large-tile kernel, so that
+// bits_out / bits / rdot_w / no_store / colsum may be used.
+bool gemm_fused_ok(bool bf16, GemmMode mode, int M, int N, int K);
+// Columns per row-dot partial for an N-column product (N / gemm_rdot_cols partials).
+int gemm_rdot_cols(int N);
+// True when the large-tile kernel has an epilogue for these flags.
+bool big_epilogue_supported(GemmMode mode, int flags);
 
 }  // namespace spz

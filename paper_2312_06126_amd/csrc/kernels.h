@@ -46,6 +46,14 @@ struct RowdotArgs {
 
 struct HeadBwdArgs {
   const float* dq; const void* w; const void* H; void* dH; int64_t ld; int K, rows;
+  // When set (bf16, K % 32 == 0), the ReLU mask comes from these bits instead of H:
+  // bit k % 32 of bits[(k / 32) * ldbits + b].
+  const uint32_t* bits; int64_t ldbits;
+};
+
+// q[r] = bias + sum over p < parts in order of part[p * ld + r], r < rows.
+struct RdotFinalArgs {
+  const float* part; int parts; int64_t ld; int rows; const float* bias; float* q;
 };
 
 struct TdArgs {
@@ -91,6 +99,7 @@ hipError_t launch_sac_head(bool bf16, const SacHeadArgs& h, hipStream_t s);
 hipError_t launch_td3_head(bool bf16, const Td3HeadArgs& h, hipStream_t s);
 hipError_t launch_rowdot(bool bf16, const RowdotArgs& r, hipStream_t s);
 hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s);
+hipError_t launch_rdot_final(const RdotFinalArgs& a, hipStream_t s);
 hipError_t launch_td_target(const TdArgs& a, hipStream_t s);
 int loss_blocks(int Bp);
 hipError_t launch_critic_loss(const CriticLossArgs& a, hipStream_t s);

@@ -226,6 +226,48 @@ __global__ void __launch_bounds__(256) k_head_bwd(HeadBwdArgs a) {
   V::store(static_cast<T*>(a.dH) + (int64_t)b * a.ld + k, o);
 }
 
+// The same with the mask read from bits. A block covers HB_ROWS rows: their words
+// (K / 32 per row, stored row-contiguously per 32-column block) are staged in LDS
+// with coalesced loads, then each thread writes 16-byte pieces of the rows in order.
+constexpr int HB_ROWS = 64;
+__global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
+  extern __shared__ uint32_t wsh[];   // [K / 32][HB_ROWS]
+  const int nw = a.K / 32, kv = a.K / 8;
+  const int r0 = blockIdx.x * HB_ROWS;
+  for (int t = threadIdx.x; t < nw * HB_ROWS; t += blockDim.x) {
+    const int wc = t / HB_ROWS, r = t % HB_ROWS;
+    wsh[t] = r0 + r < a.rows ? a.bits[(int64_t)wc * a.ldbits + r0 + r] : 0u;
+  }
+  __syncthreads();
+  const bf16_t* w = static_cast<const bf16_t*>(a.w);
+  for (int t = threadIdx.x; t < HB_ROWS * kv; t += blockDim.x) {
+    const int r = t / kv, k = (t % kv) * 8;
+    const int b = r0 + r;
+    if (b >= a.rows) break;
+    const float dq = bf2f(f2bf(a.dq[b]));
+    const uint32_t wd = wsh[(k >> 5) * HB_ROWS + r] >> (k & 31);
+    const uint4 w4 = *reinterpret_cast<const uint4*>(w + k);
+    const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float w0 = bf2f((bf16_t)(ww[e] & 0xFFFFu)), w1 = bf2f((bf16_t)(ww[e] >> 16));
+      const float v0 = (wd >> (2 * e)) & 1u ? dq * w0 : 0.0f;
+      const float v1 = (wd >> (2 * e + 1)) & 1u ? dq * w1 : 0.0f;
+      o[e] = (uint32_t)f2bf(v0) | ((uint32_t)f2bf(v1) << 16);
+    }
+    *reinterpret_cast<uint4*>(static_cast<bf16_t*>(a.dH) + (int64_t)b * a.ld + k) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+__global__ void __launch_bounds__(256) k_rdot_final(RdotFinalArgs a) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= a.rows) return;
+  float s = 0.0f;
+  for (int p = 0; p < a.parts; ++p) s += a.part[(int64_t)p * a.ld + r];
+  a.q[r] = s + *a.bias;
+}
+
 // ------------------------------------------------------------------------------ TD target, losses
 __global__ void __launch_bounds__(256) k_td_target(TdArgs a) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
@@ -552,7 +594,19 @@ hipError_t launch_rowdot(bool bf16, const RowdotArgs& r, hipStream_t s) {
 hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s) {
   const int vec = bf16 ? 8 : 4;
   if (a.K % vec || a.ld % vec) return hipErrorInvalidValue;
+  if (a.bits) {
+    if (!bf16 || a.K % 32 || a.ldbits < a.rows) return hipErrorInvalidValue;
+    const size_t lds = (size_t)(a.K / 32) * HB_ROWS * 4;
+    if (lds > 64 * 1024) return hipErrorInvalidValue;
+    k_head_bwd_bits<<<blocks(a.rows, HB_ROWS), 256, lds, s>>>(a);
+    return hipGetLastError();
+  }
   SPZ_LAUNCH_T(bf16, k_head_bwd, blocks((int64_t)a.rows * (a.K / vec), 256), 256, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_rdot_final(const RdotFinalArgs& a, hipStream_t s) {
+  if (a.parts < 1 || a.ld < a.rows) return hipErrorInvalidValue;
+  k_rdot_final<<<blocks(a.rows, 256), 256, 0, s>>>(a);
   return hipGetLastError();
 }
 hipError_t launch_td_target(const TdArgs& a, hipStream_t s) {

@@ -25,3 +25,82 @@ extern "C" int spzt_gemm(int32_t bf16, int32_t mode, int32_t M, int32_t N, int32
   if (e == hipErrorInvalidValue) return SPZ_EINVAL;
   return e == hipSuccess ? SPZ_OK : SPZ_EHIP;
 }
+
+extern "C" int spzt_gemm_fused(int32_t mode, int32_t M, int32_t N, int32_t K, const void* A, int64_t lda,
+                               const void* B, int64_t ldb, void* C, int64_t ldc, const float* bias,
+                               uint32_t* bits_out, const uint32_t* bits, int64_t ldbits, const void* rdot_w,
+                               float* rdot_part, int64_t ldrd, int32_t no_store, float* colsum, int64_t ldcs) {
+  if ((mode != GEMM_FWD && mode != GEMM_DGRAD) || !A || !B || !C) return SPZ_EINVAL;
+  if (mode == GEMM_DGRAD && !bits) return SPZ_EINVAL;
+  GemmArgs g{};
+  g.A = A; g.lda = lda; g.B = B; g.ldb = ldb; g.C = C; g.ldc = ldc;
+  g.M = M; g.N = N; g.K = K;
+  if (mode == GEMM_FWD) {
+    g.bias = bias; g.relu = 1;
+    g.bits_out = bits_out;
+    g.rdot_w = rdot_w; g.rdot_part = rdot_part; g.ldrd = ldrd;
+    g.no_store = no_store;
+  } else {
+    g.bits = bits;
+    g.colsum = colsum; g.ldcs = ldcs;
+  }
+  g.ldbits = ldbits;
+  if (!gemm_fused_ok(true, (GemmMode)mode, M, N, K)) return SPZ_EINVAL;
+  hipError_t e = gemm(true, (GemmMode)mode, g, nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e == hipErrorInvalidValue) return SPZ_EINVAL;
+  return e == hipSuccess ? SPZ_OK : SPZ_EHIP;
+}
+
+extern "C" int spzt_rdot_cols(int32_t N) { return gemm_rdot_cols(N); }
+
+// Rounding check of the device float32 -> bfloat16 conversion against an integer
+// round-to-nearest-even written out here: every input bit pattern in
+// [begin, begin + count) must give the same 16 bits, except that a NaN input only
+// has to give a NaN.
+namespace {
+__device__ inline uint32_t rne_bf16_ref(uint32_t u) {
+  const uint32_t mant = u & 0xFFFFu, keep = u >> 16;
+  const bool up = mant > 0x8000u || (mant == 0x8000u && (keep & 1u));
+  return (keep + (up ? 1u : 0u)) & 0xFFFFu;
+}
+
+__global__ void k_round_check(uint64_t begin, uint64_t count, unsigned long long* bad) {
+  const uint64_t base = begin + ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) * 16;
+  unsigned n = 0;
+  for (int t = 0; t < 16; ++t) {
+    const uint64_t x = base + t;
+    if (x >= begin + count) break;
+    const uint32_t u = (uint32_t)x;
+    const float f = __uint_as_float(u);
+    const uint32_t hw = f2bf(f);
+    const uint32_t pk = pack_bf16x2(f, -f);
+    const bool nan = (u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu);
+    if (nan) {
+      const bool ok = (hw & 0x7F80u) == 0x7F80u && (hw & 0x7Fu) && (pk & 0x7F80u) == 0x7F80u && (pk & 0x7Fu);
+      n += ok ? 0 : 1;
+    } else {
+      const uint32_t ref = rne_bf16_ref(u), refn = rne_bf16_ref(u ^ 0x80000000u);
+      n += (hw != ref || (pk & 0xFFFFu) != ref || (pk >> 16) != refn) ? 1 : 0;
+    }
+  }
+  if (n) atomicAdd(bad, (unsigned long long)n);
+}
+}  // namespace
+
+extern "C" int spzt_bf16_round_check(uint64_t begin, uint64_t count, uint64_t* mismatches) {
+  if (!mismatches || count == 0 || begin + count > (1ull << 32)) return SPZ_EINVAL;
+  unsigned long long* d = nullptr;
+  if (hipMalloc(&d, sizeof(*d)) != hipSuccess) return SPZ_ENOMEM;
+  hipError_t e = hipMemset(d, 0, sizeof(*d));
+  const uint64_t threads = (count + 15) / 16;
+  if (e == hipSuccess) {
+    k_round_check<<<(unsigned)((threads + 255) / 256), 256>>>(begin, count, d);
+    e = hipGetLastError();
+  }
+  unsigned long long h = 0;
+  if (e == hipSuccess) e = hipMemcpy(&h, d, sizeof(h), hipMemcpyDeviceToHost);
+  (void)hipFree(d);
+  *mismatches = h;
+  return e == hipSuccess ? SPZ_OK : SPZ_EHIP;
+}

@@ -112,3 +112,144 @@ def test_rejects_bad_shapes(env):
     torch, f = env
     d = torch.zeros(1024, device="cuda")
     assert f(1, 0, 100, 64, 64, 1, d.data_ptr(), 64, d.data_ptr(), 64, d.data_ptr(), 64, None, None, 0, 0, 1) != 0
+
+
+# ----------------------------------------------------------------------------- fused epilogues
+@pytest.fixture(scope="module")
+def fused(env):
+    torch, _ = env
+    from paper_2312_06126_amd import spz
+    lib = spz.load()
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    f = lib.spzt_gemm_fused
+    f.argtypes = [I32, I32, I32, I32, P, I64, P, I64, P, I64, P, P, P, I64, P, P, I64, I32, P, I64]
+    f.restype = ctypes.c_int
+    lib.spzt_rdot_cols.argtypes = [I32]
+    lib.spzt_rdot_cols.restype = ctypes.c_int
+    return torch, f, lib.spzt_rdot_cols
+
+
+def unpack_bits(words, M, N):
+    """words [N/32, M] uint32 -> bool [M, N]: bit c % 32 of word (c / 32, r)."""
+    w = words.astype(np.uint64)
+    cols = [((w[c // 32] >> np.uint64(c % 32)) & np.uint64(1)).astype(bool) for c in range(N)]
+    return np.stack(cols, axis=1)
+
+
+def dev_ptr(t):
+    return t.data_ptr() if t is not None else None
+
+
+@pytest.mark.parametrize("M,N,K", [(512, 512, 96), (256, 384, 64), (768, 1024, 416)])
+@pytest.mark.parametrize("bits,rdot,no_store", [(True, False, False), (False, True, False), (False, True, True),
+                                                (True, True, False), (True, True, True)])
+def test_forward_fused_epilogue(fused, M, N, K, bits, rdot, no_store):
+    """ReLU forward with mask bits / row dots: C matches the plain product (one
+    bf16 ulp), the bits are exactly C > 0 of the stored C, and the row-dot partials
+    are the column-group sums of stored C times w (float32 accumulation)."""
+    torch, f, rdot_cols = fused
+    rng = np.random.default_rng(M + N + K)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    B = rng.standard_normal((N, K)).astype(np.float32)
+    bias = rng.standard_normal(N).astype(np.float32)
+    w = rng.standard_normal(N).astype(np.float32)
+    dA, dB = to_dev(torch, A, True), to_dev(torch, B, True)
+    dbias = torch.from_numpy(bias).cuda()
+    dw = to_dev(torch, w, True)
+    dC = torch.full((M, N), 7.0, dtype=torch.bfloat16, device="cuda")
+    dbits = torch.zeros((N // 32, M), dtype=torch.int32, device="cuda") if bits else None
+    cols = rdot_cols(N)
+    parts = N // cols
+    dpart = torch.zeros((parts, M), dtype=torch.float32, device="cuda") if rdot else None
+    rc = f(0, M, N, K, dA.data_ptr(), K, dB.data_ptr(), K, dC.data_ptr(), N, dbias.data_ptr(), dev_ptr(dbits), None,
+           M, dev_ptr(dw) if rdot else None, dev_ptr(dpart), M, int(no_store), None, 0)
+    assert rc == 0, rc
+    ref = np.maximum(rounded(torch, A, True) @ rounded(torch, B, True).T + bias, 0.0)
+    ref_b = rounded(torch, ref, True)
+    got = dC.to(torch.float64).cpu().numpy()
+    if no_store:
+        assert np.all(got == 7.0)
+        # the stored values the epilogue used are not visible: compare the row dots
+        # with the reference product instead (bf16 ulp-level differences allowed)
+        cval = ref_b
+    else:
+        ulp = np.abs(ref_b) * 2.0 ** -7 + 1e-30
+        assert np.all(np.abs(got - ref_b) <= 2 * ulp + 1e-6)
+        cval = got
+    if bits:
+        words = dbits.cpu().numpy().view(np.uint32)
+        mask = unpack_bits(words, M, N)
+        if no_store:
+            # sign decisions near zero may differ from the float64 reference
+            assert (mask != (ref_b > 0)).mean() < 1e-3
+        else:
+            assert np.array_equal(mask, got > 0)
+    if rdot:
+        wr = rounded(torch, w, True)
+        part = dpart.cpu().numpy().astype(np.float64)
+        want = np.stack([(cval[:, p * cols:(p + 1) * cols] * wr[p * cols:(p + 1) * cols]).sum(1)
+                         for p in range(parts)])
+        scale = np.abs(cval[:, :]).max() * np.abs(wr).max() * cols
+        tol = 1e-5 if not no_store else 2.0 ** -7
+        assert np.abs(part - want).max() <= tol * scale, np.abs(part - want).max() / scale
+
+
+@pytest.mark.parametrize("M,N,K", [(512, 512, 64), (256, 1024, 1024), (512, 384, 96)])
+@pytest.mark.parametrize("colsum", [False, True])
+def test_dgrad_bits_equal_mask(env, fused, M, N, K, colsum):
+    """A dgrad masked by bits is bit-identical to the same dgrad masked by a bf16
+    tensor with the same sign pattern; the fused column sums are those of the
+    stored result over each 256-row tile."""
+    torch, gemm = env
+    _, f, _ = fused
+    rng = np.random.default_rng(M * 7 + N + K)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    B = rng.standard_normal((K, N)).astype(np.float32)
+    pos = rng.uniform(size=(M, N)) < 0.5
+    mask = np.where(pos, rng.uniform(0.1, 2.0, size=(M, N)), -rng.uniform(0.0, 2.0, size=(M, N))).astype(np.float32)
+    words = np.zeros((N // 32, M), dtype=np.uint32)
+    for c in range(N):
+        words[c // 32] |= (pos[:, c].astype(np.uint32) << np.uint32(c % 32))
+    dA, dB = to_dev(torch, A, True), to_dev(torch, B, True)
+    dmask = to_dev(torch, mask, True)
+    dbits = torch.from_numpy(words.view(np.int32)).cuda()
+    dC1 = torch.zeros((M, N), dtype=torch.bfloat16, device="cuda")
+    dC2 = torch.zeros((M, N), dtype=torch.bfloat16, device="cuda")
+    dcs = torch.zeros((M // 256, N), dtype=torch.float32, device="cuda") if colsum else None
+    rc = gemm(1, 1, M, N, K, 1, dA.data_ptr(), K, dB.data_ptr(), N, dC1.data_ptr(), N, None, dmask.data_ptr(), N, 0, 0)
+    assert rc == 0
+    rc = f(1, M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, dC2.data_ptr(), N, None, None, dbits.data_ptr(), M,
+           None, None, 0, 0, dev_ptr(dcs), N)
+    assert rc == 0
+    assert torch.equal(dC1.view(torch.int16), dC2.view(torch.int16))
+    if colsum:
+        c = dC2.to(torch.float64).cpu().numpy().reshape(M // 256, 256, N).sum(1)
+        got = dcs.cpu().numpy()
+        assert np.abs(got - c).max() <= 1e-5 * np.abs(c).max() + 1e-6
+
+
+def test_fused_rejects_bad_use(fused):
+    """Fused epilogues need the whole product on the large-tile kernel."""
+    torch, f, _ = fused
+    d = torch.zeros(1 << 20, device="cuda")
+    p = d.data_ptr()
+    # N not a multiple of 128
+    assert f(0, 256, 96, 64, p, 64, p, 64, p, 96, None, p, None, 256, None, None, 0, 0, None, 0) != 0
+    # no_store without a row dot
+    assert f(0, 256, 128, 64, p, 64, p, 64, p, 128, None, p, None, 256, None, None, 0, 1, None, 0) != 0
+    # dgrad without bits
+    assert f(1, 256, 128, 64, p, 64, p, 128, p, 128, None, None, None, 256, None, None, 0, 0, None, 0) != 0
+    # bits leading dimension shorter than M
+    assert f(0, 512, 128, 64, p, 64, p, 64, p, 128, None, p, None, 256, None, None, 0, 0, None, 0) != 0
+
+
+def test_bf16_rounding_exhaustive(env):
+    """The device float32 -> bf16 conversion (hardware instruction) rounds every
+    float32 bit pattern to nearest-even exactly as the integer definition does."""
+    from paper_2312_06126_amd import spz
+    lib = spz.load()
+    lib.spzt_bf16_round_check.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.POINTER(ctypes.c_uint64)]
+    lib.spzt_bf16_round_check.restype = ctypes.c_int
+    bad = ctypes.c_uint64(0)
+    assert lib.spzt_bf16_round_check(0, 1 << 32, ctypes.byref(bad)) == 0
+    assert bad.value == 0, bad.value

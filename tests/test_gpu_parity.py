@@ -31,6 +31,12 @@ RAGGED_TD3 = Workload("ragged_td3", "td3", 13, 5, (100, 70), 1000, 5000, "fp32",
                       alpha_init=0.0)
 RAGGED_BF16 = RAGGED.replace(name="ragged_sac_bf16", prec="bf16", zero_mod=10, obs_dim=45)
 DEEP = Workload("deep_sac", "sac", 29, 3, (96, 64, 160), 600, 3000, "fp32", 10, target_entropy=-3.0)
+# bf16 shapes on the large-tile kernel with every fused epilogue (ReLU masks as bits,
+# critic output layer folded into the last hidden product): 256- and 128-wide
+# column tiles, a ragged batch (500 of 512 rows) and a three-layer variant.
+FUSED_BF16 = RAGGED_BF16.replace(name="fused_sac_bf16", hidden=(256, 128), batch=500)
+FUSED_BF16_DEEP = RAGGED_BF16.replace(name="fused_sac_bf16_deep", hidden=(128, 256, 384), batch=768)
+FUSED_TD3_BF16 = RAGGED_TD3.replace(name="fused_td3_bf16", prec="bf16", zero_mod=10, hidden=(256, 256), batch=256)
 
 FP32_TOL = 1e-4
 BF16_LOSS_TOL = 2e-2
@@ -135,6 +141,13 @@ def test_teacher_forced_bf16():
     teacher_forced(RAGGED_BF16, 5000, steps_before=1, tol_grad=1e-3, tol_loss=BF16_LOSS_TOL)
 
 
+@pytest.mark.parametrize("w,n_steps", [(FUSED_BF16, 1), (FUSED_BF16_DEEP, 1), (FUSED_TD3_BF16, 2)],
+                         ids=lambda x: getattr(x, "name", str(x)))
+def test_teacher_forced_bf16_fused(w, n_steps):
+    log("teacher-forced %s" % w.name)
+    teacher_forced(w, 5000, steps_before=1, tol_grad=1e-3, tol_loss=BF16_LOSS_TOL, n_steps=n_steps)
+
+
 def test_teacher_forced_log_std_clamp_active():
     """Push the log-std head beyond both clamp bounds through write_params."""
     w = RAGGED
@@ -203,10 +216,10 @@ def test_td3_full_batch_parity():
     check_ten_step_params(w, params, o, hist, 4)
 
 
-@pytest.mark.parametrize("w,rows,steps", [(RAGGED_BF16, 5000, 10),
+@pytest.mark.parametrize("w,rows,steps", [(RAGGED_BF16, 5000, 10), (FUSED_BF16, 5000, 10),
                                           (W["sac_humanoid_bf16"].replace(capacity=100_000), 100_000, 4),
                                           (W["sac_large_bf16"].replace(batch=1024, capacity=20_000), 20_000, 3)],
-                         ids=["ragged_bf16", "humanoid_bf16", "large_bf16_b1024"])
+                         ids=["ragged_bf16", "fused_bf16", "humanoid_bf16", "large_bf16_b1024"])
 def test_bf16_loss_parity(w, rows, steps):
     log("bf16 %s" % w.name)
     rg, ro, _, _, _ = ten_steps(w, rows, steps=steps, virtual=rows > 50_000)
