@@ -14,10 +14,14 @@
 //     is read with two ds_read_b64_tr_b16 transposing reads per fragment: within
 //     each 16-lane group, lane i addresses 4 consecutive values of row k0 + i/4
 //     at column m0 + 4(i%4), and lane j receives column m0 + j for the 4 rows.
-//   * Double-buffered LDS (one barrier per 32-deep k slice). At the top of each
-//     slice the registers holding slice k+1 are stored to the free LDS buffer and
-//     the global loads of slice k+2 are issued, so they travel while slice k is
-//     multiplied.
+//   * Three LDS stages of one 32-deep k slice each, one barrier per slice. In
+//     slice k: the registers holding slice k+2 go to the stage freed by slice k-1,
+//     the global loads of slice k+3 are issued, the first 16-deep half of slice k
+//     is multiplied while the fragments of its second half are read, the barrier
+//     publishes slice k+1, and the second half is multiplied while the fragments
+//     of slice k+1's first half are read. The matrix cores never wait for an LDS
+//     read after the barrier, and the barrier sits between two runs of MFMAs.
+//     Instruction groups are interleaved explicitly (one LDS access per MFMA).
 //   * XCD-aware tile order: workgroup b runs on XCD b % 8, so logical tiles are
 //     handed out in contiguous ranges per XCD; the column tiles of one row panel
 //     (and the split-K slices of one weight-gradient tile) share an L2.
@@ -33,7 +37,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 #define LDS_AS __attribute__((address_space(3)))
 
-constexpr int BM = 256, BK = 32, NT = 512, WM = 4, WN = 2;
+constexpr int BM = 256, BK = 32, NT = 512, WM = 4, WN = 2, STAGES = 3;
 
 template <bool KC, int ROWS>
 struct BigTile {
@@ -280,11 +284,9 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   using TA = BigTile<AKC, BM>;
   using TB = BigTile<BKC, BN>;
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
+  constexpr int SE = TA::ELEMS + TB::ELEMS;   // elements per stage: A tile then B tile
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  bf16_t* As0 = reinterpret_cast<bf16_t*>(smem);
-  bf16_t* As1 = As0 + TA::ELEMS;
-  bf16_t* Bs0 = As1 + TA::ELEMS;
-  bf16_t* Bs1 = Bs0 + TB::ELEMS;
+  bf16_t* S = reinterpret_cast<bf16_t*>(smem);
 
   // XCD-aware logical tile: contiguous logical ranges per XCD, column tiles fastest.
   const int total = gridDim.x;
@@ -317,44 +319,90 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   TA ta;
   TB tb;
   const int nk = (kend - kbeg) / BK;
+  // Prologue: slices 0 and 1 in stages 0 and 1, slice 2 in registers.
   ta.load(A, g.lda, m0, kbeg, tid);
   tb.load(B, g.ldb, n0, kbeg, tid);
-  ta.store(As0, tid);
-  tb.store(Bs0, tid);
+  ta.store(S, tid);
+  tb.store(S + TA::ELEMS, tid);
   if (nk > 1) {
     ta.load(A, g.lda, m0, kbeg + BK, tid);
     tb.load(B, g.ldb, n0, kbeg + BK, tid);
+    ta.store(S + SE, tid);
+    tb.store(S + SE + TA::ELEMS, tid);
+  }
+  if (nk > 2) {
+    ta.load(A, g.lda, m0, kbeg + 2 * BK, tid);
+    tb.load(B, g.ldb, n0, kbeg + 2 * BK, tid);
   }
   __syncthreads();
+  bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) fa0[i] = frag<AKC, TA::PITCH>(S, (wm * TM + i) * 32, 0, lane);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) fb0[j] = frag<BKC, TB::PITCH>(S + TA::ELEMS, (wn * TN + j) * 32, 0, lane);
+  // LDS read / write and global load instruction counts of one slice, for the
+  // interleave pattern (a transposing fragment read is two instructions).
+  constexpr int NR = (AKC ? TM : 2 * TM) + (BKC ? TN : 2 * TN);
+  constexpr int NW = TA::PER + TB::PER;
+  int sc = 0;   // stage of slice kt
   for (int kt = 0; kt < nk; ++kt) {
-    const bf16_t* Ac = (kt & 1) ? As1 : As0;
-    const bf16_t* Bc = (kt & 1) ? Bs1 : Bs0;
-    if (kt + 1 < nk) {
-      ta.store((kt & 1) ? As0 : As1, tid);
-      tb.store((kt & 1) ? Bs0 : Bs1, tid);
-    }
+    const int s1 = sc == STAGES - 1 ? 0 : sc + 1;   // stage of slice kt + 1
+    const int s2 = s1 == STAGES - 1 ? 0 : s1 + 1;   // stage of slice kt + 2 (= that of kt - 1)
+    const bf16_t* Sc = S + sc * SE;
     if (kt + 2 < nk) {
-      ta.load(A, g.lda, m0, kbeg + (kt + 2) * BK, tid);
-      tb.load(B, g.ldb, n0, kbeg + (kt + 2) * BK, tid);
+      ta.store(S + s2 * SE, tid);
+      tb.store(S + s2 * SE + TA::ELEMS, tid);
+    }
+    if (kt + 3 < nk) {
+      ta.load(A, g.lda, m0, kbeg + (kt + 3) * BK, tid);
+      tb.load(B, g.ldb, n0, kbeg + (kt + 3) * BK, tid);
     }
 #pragma unroll
-    for (int ks = 0; ks < BK; ks += 16) {
-      bf16x8 af[TM], bw[TN];
+    for (int i = 0; i < TM; ++i) fa1[i] = frag<AKC, TA::PITCH>(Sc, (wm * TM + i) * 32, 16, lane);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) af[i] = frag<AKC, TA::PITCH>(Ac, (wm * TM + i) * 32, ks, lane);
+    for (int j = 0; j < TN; ++j) fb1[j] = frag<BKC, TB::PITCH>(Sc + TA::ELEMS, (wn * TN + j) * 32, 16, lane);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) bw[j] = frag<BKC, TB::PITCH>(Bc, (wn * TN + j) * 32, ks, lane);
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa0[i], fb0[j], acc[i][j], 0, 0, 0);
+    // sched_group_barrier masks: 0x008 MFMA, 0x020 global load, 0x100 LDS read, 0x200 LDS write.
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);
+    for (int t = 0; t < NW; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
+#pragma unroll
+    for (int t = 0; t < NW; ++t) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+#pragma unroll
+    for (int t = 0; t < NR; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+    // Publishes slice kt + 1 (stored one slice earlier) and retires every wave's
+    // reads of slice kt - 1, whose stage the next slice overwrites.
     __syncthreads();
+    if (kt + 1 < nk) {
+      const bf16_t* Sn = S + s1 * SE;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) fa0[i] = frag<AKC, TA::PITCH>(Sn, (wm * TM + i) * 32, 0, lane);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) fb0[j] = frag<BKC, TB::PITCH>(Sn + TA::ELEMS, (wn * TN + j) * 32, 0, lane);
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa1[i], fb1[j], acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NR; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+    sc = s1;
   }
-
-  // Epilogue variants are compile-time so the store loops unroll completely. The
-  // final barrier of the k loop has released the LDS tiles for the scratch.
+  // The barrier of the last slice came after every wave's last LDS read, so the
+  // epilogue may reuse LDS as scratch.
   epilogue<MODE, BN, F>(g, acc, m0, n0, wm, wn, lane, wave, z, mt, reinterpret_cast<float*>(smem));
 }
 
@@ -362,7 +410,7 @@ template <int MODE, int BN, int F>
 hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
   using TA = BigTile<MODE != GEMM_WGRAD, BM>;
   using TB = BigTile<MODE == GEMM_FWD, BN>;
-  const size_t tiles = 2 * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
+  const size_t tiles = STAGES * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
   const size_t scratch = ((NT / 64) * 32 * SCR_PITCH + WM * BN) * sizeof(float);
   const size_t lds = tiles > scratch ? tiles : scratch;
   static bool attr = false;

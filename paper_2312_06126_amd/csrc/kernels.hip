@@ -107,51 +107,60 @@ __global__ void __launch_bounds__(256) k_pack_rows(PackArgs p) {
 // SAC head: z = [mu | l] -> a = tanh(mu + exp(clip(l)) eps) written into the action
 // columns of x, and the tanh-Gaussian log-density (overflow-free form of
 // log(1 - tanh^2 u) = 2 (ln 2 - u - softplus(-2u))). Optional cache for backward.
+// One thread per (row, action) element, so that loads and stores of consecutive
+// threads are contiguous; a block covers HEAD_ROWS rows and adds each row's
+// per-action terms in action order through LDS.
+constexpr int HEAD_ROWS = 64;
 template <typename T>
 __global__ void __launch_bounds__(256) k_sac_head(SacHeadArgs h) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= h.B) return;
+  extern __shared__ float lterm[];   // [HEAD_ROWS][A]
+  const int r0 = blockIdx.x * HEAD_ROWS;
+  const int rows = min(HEAD_ROWS, h.B - r0);
+  const int n = rows * h.A;
   const uint32_t t = (uint32_t)(*h.step + 1);
-  const float* z = h.z + (int64_t)b * h.ldz;
-  T* x = static_cast<T*>(h.x) + (int64_t)b * h.ldx + h.xoff;
-  float lp = 0.0f;
-  for (int j = 0; j < h.A; ++j) {
-    const float eps = normal_at(h.seed, (uint64_t)b * h.A + j, t, h.purpose);
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int r = e / h.A, j = e - r * h.A;
+    const int b = r0 + r;
+    const float* z = h.z + (int64_t)b * h.ldz;
+    const float eps = normal_at(h.seed, (uint64_t)r0 * h.A + e, t, h.purpose);
     const float mu = z[j], l = z[h.A + j];
     const float lc = fminf(fmaxf(l, h.lmin), h.lmax);
     const float sig = expf(lc);
     const float u = mu + sig * eps;
     const float a = tanhf(u);
-    x[j] = from_f<T>(a);
-    lp += -0.5f * eps * eps - lc - HALF_LN_2PI_F - 2.0f * (LN2F - u - softplusf(-2.0f * u));
+    static_cast<T*>(h.x)[(int64_t)b * h.ldx + h.xoff + j] = from_f<T>(a);
+    lterm[e] = -0.5f * eps * eps - lc - HALF_LN_2PI_F - 2.0f * (LN2F - u - softplusf(-2.0f * u));
     if (h.th) {
-      const int64_t c = (int64_t)b * h.A + j;
+      const int64_t c = (int64_t)r0 * h.A + e;
       h.th[c] = a;
       h.se[c] = sig * eps;
       h.lm[c] = (l >= h.lmin && l <= h.lmax) ? 1.0f : 0.0f;
     }
   }
-  h.logp[b] = lp;
+  __syncthreads();
+  if ((int)threadIdx.x < rows) {
+    float lp = 0.0f;
+    for (int j = 0; j < h.A; ++j) lp += lterm[threadIdx.x * h.A + j];
+    h.logp[r0 + threadIdx.x] = lp;
+  }
 }
 
 // TD3 heads. Target: a' = clip(tanh z + clip(noise * eps, -c, c), -1, 1). Policy: a = tanh z.
+// One thread per (row, action) element.
 template <typename T>
 __global__ void __launch_bounds__(256) k_td3_head(Td3HeadArgs h) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= h.B) return;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (int64_t)h.B * h.A) return;
+  const int b = (int)(e / h.A), j = (int)(e - (int64_t)b * h.A);
   const uint32_t t = (uint32_t)(*h.step + 1);
-  const float* z = h.z + (int64_t)b * h.ldz;
-  T* x = static_cast<T*>(h.x) + (int64_t)b * h.ldx + h.xoff;
-  for (int j = 0; j < h.A; ++j) {
-    float a = tanhf(z[j]);
-    if (h.smooth) {
-      const float eps = normal_at(h.seed, (uint64_t)b * h.A + j, t, P_NOISE_TGT);
-      const float nz = fminf(fmaxf(h.noise * eps, -h.clip), h.clip);
-      a = fminf(fmaxf(a + nz, -1.0f), 1.0f);
-    }
-    x[j] = from_f<T>(a);
-    if (h.th) h.th[(int64_t)b * h.A + j] = a;
+  float a = tanhf(h.z[(int64_t)b * h.ldz + j]);
+  if (h.smooth) {
+    const float eps = normal_at(h.seed, (uint64_t)e, t, P_NOISE_TGT);
+    const float nz = fminf(fmaxf(h.noise * eps, -h.clip), h.clip);
+    a = fminf(fmaxf(a + nz, -1.0f), 1.0f);
   }
+  static_cast<T*>(h.x)[(int64_t)b * h.ldx + h.xoff + j] = from_f<T>(a);
+  if (h.th) h.th[e] = a;
 }
 
 // 16-byte vector of operand values and its float image.
@@ -344,22 +353,20 @@ __global__ void __launch_bounds__(256) k_actor_loss(ActorLossArgs a) {
 // d l = (g_u sigma eps - alpha/B) * [lmin <= l <= lmax]. TD3: dz = da (1 - a^2).
 template <typename T>
 __global__ void __launch_bounds__(256) k_actor_head_bwd(ActorHeadBwdArgs h) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= h.B) return;
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // (row, action) element
+  if (c >= (int64_t)h.B * h.A) return;
+  const int b = (int)(c / h.A), j = (int)(c - (int64_t)b * h.A);
   T* dz = static_cast<T*>(h.dz) + (int64_t)b * h.ldz;
   const float aB = h.sac ? expf(*h.log_alpha) / (float)h.B : 0.0f;
-  for (int j = 0; j < h.A; ++j) {
-    const int64_t c = (int64_t)b * h.A + j;
-    float da = h.da1[(int64_t)b * h.ldda + j];
-    if (h.da2) da += h.da2[(int64_t)b * h.ldda + j];
-    const float a = h.th[c];
-    float gu = da * (1.0f - a * a);
-    if (h.sac) {
-      gu += aB * 2.0f * a;
-      dz[h.A + j] = from_f<T>((gu * h.se[c] - aB) * h.lm[c]);
-    }
-    dz[j] = from_f<T>(gu);
+  float da = h.da1[(int64_t)b * h.ldda + j];
+  if (h.da2) da += h.da2[(int64_t)b * h.ldda + j];
+  const float a = h.th[c];
+  float gu = da * (1.0f - a * a);
+  if (h.sac) {
+    gu += aB * 2.0f * a;
+    dz[h.A + j] = from_f<T>((gu * h.se[c] - aB) * h.lm[c]);
   }
+  dz[j] = from_f<T>(gu);
 }
 
 // ------------------------------------------------------------------------------ column sums
@@ -579,11 +586,14 @@ hipError_t launch_pack(bool bf16, const PackArgs& p, hipStream_t s) {
   return hipGetLastError();
 }
 hipError_t launch_sac_head(bool bf16, const SacHeadArgs& h, hipStream_t s) {
-  SPZ_LAUNCH_T(bf16, k_sac_head, blocks(h.B, 256), 256, s, h);
+  if (h.A < 1 || h.A > 256) return hipErrorInvalidValue;
+  const size_t lds = (size_t)HEAD_ROWS * h.A * sizeof(float);
+  if (bf16) k_sac_head<bf16_t><<<blocks(h.B, HEAD_ROWS), 256, lds, s>>>(h);
+  else k_sac_head<float><<<blocks(h.B, HEAD_ROWS), 256, lds, s>>>(h);
   return hipGetLastError();
 }
 hipError_t launch_td3_head(bool bf16, const Td3HeadArgs& h, hipStream_t s) {
-  SPZ_LAUNCH_T(bf16, k_td3_head, blocks(h.B, 256), 256, s, h);
+  SPZ_LAUNCH_T(bf16, k_td3_head, blocks((int64_t)h.B * h.A, 256), 256, s, h);
   return hipGetLastError();
 }
 hipError_t launch_rowdot(bool bf16, const RowdotArgs& r, hipStream_t s) {
@@ -623,7 +633,7 @@ hipError_t launch_actor_loss(const ActorLossArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream_t s) {
-  SPZ_LAUNCH_T(bf16, k_actor_head_bwd, blocks(h.B, 256), 256, s, h);
+  SPZ_LAUNCH_T(bf16, k_actor_head_bwd, blocks((int64_t)h.B * h.A, 256), 256, s, h);
   return hipGetLastError();
 }
 int colsum_chunks(int rows) { return (int)blocks(rows, COLSUM_CHUNK); }
