@@ -34,6 +34,10 @@ METRIC = "actor-critic update frames/sec (batch rows/s) at 1 MI355X; MFMA util %
 PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense matrix peaks
 PEAK_HBM_GBS = 8000.0
 GEMMS = ("gemm_fwd", "gemm_dgrad", "gemm_wgrad")
+# Measured HBM traffic of the dominant kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
+# scaled by a plain copy of known size), valid while the kernel sources hash the same.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_fwd_1024_sac_large_bf16_traffic.txt")
+KERNEL_SOURCES = ("gemm_big.hip", "gemm.hip", "internal.h")
 
 
 def progress(msg: str):
@@ -56,6 +60,32 @@ def fill_ring(g, w, data_seed: int, rows: int):
             progress("ring %d / %d rows (%.1fs)" % (r0 + n, rows, time.time() - t0))
 
 
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2312_06126_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str):
+    """Bytes per launch from the committed counter summary, or None when there is
+    none for this kernel or the kernel sources changed since it was taken."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as fh:
+            for line in fh:
+                if ":" in line and not line.startswith("#"):
+                    k, v = line.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("kernel") != kernel or kv.get("source_sha256") != kernel_source_hash():
+            return None
+        return float(kv["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def roofline(stats, prec: str):
     """The dominant kernel (largest total time) against its MI355X roofline."""
     top = stats[0]
@@ -69,12 +99,40 @@ def roofline(stats, prec: str):
         peak = PEAK_HBM_GBS
         r = dict(bound="hbm", achieved=round(achieved, 1), peak=peak, unit="GB/s")
     r["frac"] = round(achieved / peak, 4)
-    r["traffic"] = None
     r["kernel"] = "%s M=%d N=%d K=%d" % (top["name"], top["M"], top["N"], top["K"])
+    r["traffic"] = measured_traffic(r["kernel"])
     r["avg_launch_ms"] = round(top["avg_ms"], 5)
     r["launches"] = top["launches"]
     r["per_launch"] = top["flops"] if top["name"] in GEMMS else top["bytes"]
     return r
+
+
+def sweep(w, args, stream, steps: int = 100):
+    """Frame rate at the geometric batch sizes 16384 .. the workload's batch; the knee
+    is the smallest batch within 5% of the best frame rate."""
+    import torch
+    from paper_2312_06126_amd import Spz
+    out = []
+    b = 16384
+    while b <= w.batch:
+        wb = w.replace(batch=b)
+        g = Spz(wb.obs_dim, wb.act_dim, wb.hidden, wb.batch, wb.hparams(), args.seed, n_streams=args.streams)
+        fill_ring(g, wb, args.data_seed, wb.capacity)
+        g.update(args.warmup, stream)
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        g.update(steps, stream)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / steps
+        g.close()
+        out.append(dict(batch=b, ms_per_step=round(ms, 4), value=round(frames_per_second(b, steps, ms * steps / 1e3), 1)))
+        progress("sweep batch %d: %.3f ms/step" % (b, ms))
+        b *= 2
+    best = max(r["value"] for r in out)
+    knee = min(r["batch"] for r in out if r["value"] >= 0.95 * best)
+    return dict(points=out, knee_batch=knee, steps=steps)
 
 
 def cpu_baseline(w, seed: int, data_seed: int, sample_batch: int):
@@ -105,7 +163,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="sac_large_bf16")
     ap.add_argument("--batch", type=int, default=None, help="override the workload batch")
-    ap.add_argument("--streams", type=int, default=2, choices=(1, 2))
+    ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
+                    help="2 runs the actor and critic halves on concurrent streams (per-kernel event "
+                         "durations then overlap, so the roofline is taken from 1-stream runs)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="also time the batch sizes 16384..131072 of the workload and report the knee")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--data-seed", type=int, default=0)
     ap.add_argument("--cpu-sample-batch", type=int, default=16384)
@@ -170,7 +232,8 @@ def main():
                            act_dim=w.act_dim, hidden=list(w.hidden), replay_rows=w.capacity,
                            gemm_operands=prec, accumulate="fp32", master_weights="fp32",
                            streams=args.streams, seed=args.seed, data_seed=args.data_seed,
-                           parallelism="single GPU; actor and critic on concurrent streams"),
+                           parallelism="single GPU; " + ("actor and critic on concurrent streams"
+                                                         if args.streams == 2 else "one stream")),
                losses_finite=finite)
     if stats:
         gemm_ms = sum(s["total_ms"] for s in stats if s["name"] in GEMMS)
@@ -185,6 +248,8 @@ def main():
         out["kernels"] = [dict(name=s["name"], M=s["M"], N=s["N"], K=s["K"], launches=s["launches"],
                                avg_ms=round(s["avg_ms"], 5), total_ms=round(s["total_ms"], 3))
                           for s in stats[:40]]
+    if args.sweep:
+        out["sweep"] = sweep(w, args, stream)
     if not args.no_cpu_baseline:
         progress("cpu baseline (oracle) at batch %d" % args.cpu_sample_batch)
         out["cpu_baseline"] = cpu_baseline(w, args.seed, args.data_seed, args.cpu_sample_batch)
