@@ -106,11 +106,25 @@ typedef struct spz_hparams {
   int32_t policy_delay;           /* TD3: actor and targets every policy_delay steps */
   int32_t device;                 /* HIP device ordinal                            */
   int32_t n_streams;              /* 2: actor and critic on concurrent streams; 1: one stream */
+  int32_t ordering;               /* SPZ_ORDER_SNAPSHOT | SPZ_ORDER_SEQUENTIAL (below)     */
 } spz_hparams;
+
+/* Update ordering within a step.
+ * SPZ_ORDER_SNAPSHOT: every loss of step t reads the parameters of the start of
+ *   step t and all Adam / Polyak writes follow both gradients: the actor and the
+ *   critics are updated independently (Section 3.2.2); the two halves may run on
+ *   concurrent streams.
+ * SPZ_ORDER_SEQUENTIAL: the critics take their Adam step (and Polyak) first and
+ *   the actor loss of the same step is taken through the updated critics, as in
+ *   the published SAC and TD3 algorithms; the temperature uses the step-start
+ *   actor sample and alpha. Runs on one stream whatever n_streams says. */
+#define SPZ_ORDER_SNAPSHOT 0
+#define SPZ_ORDER_SEQUENTIAL 1
 
 /* Defaults: SAC, fp32, capacity 1e6, gamma 0.99, tau 0.005, lr 3e-4, Adam
  * (0.9, 0.999, 1e-8), alpha_init 1, learned alpha, target_entropy 0, log-std
- * clamp [-20, 2], TD3 noise 0.2 clipped to 0.5, delay 2, device 0, 2 streams. */
+ * clamp [-20, 2], TD3 noise 0.2 clipped to 0.5, delay 2, device 0, 2 streams,
+ * snapshot ordering. */
 void spz_hparams_default(spz_hparams* hp);
 
 /* Create a learner. obs_dim, act_dim >= 1; hidden[0..n_hidden) >= 1 with

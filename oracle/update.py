@@ -30,6 +30,11 @@ Readings taken where the paper is silent (each is also stated where used):
     tbar <- (1 - tau) * tbar + tau * theta after Adam, every step (SAC) or on
     delayed steps only (TD3, together with the target actor).
   * TD3's delayed step fires when the global step k satisfies k % delay == 0.
+  * Ordering "sequential" (hp["ordering"], default "snapshot"): the order of the
+    published SAC and TD3 algorithms instead. The critics take their Adam step
+    first and the actor loss of the same step is taken through the updated
+    critics; the temperature loss still uses the step-start actor sample and
+    alpha, and the target networks move after both updates as above.
 """
 from __future__ import annotations
 
@@ -118,6 +123,7 @@ class Oracle:
         self.hp = dict(hp)
         self.seed = int(seed)
         self.algo = hp["algo"]
+        self.sequential = hp.get("ordering", "snapshot") == "sequential"
         self.rnd = round_bf16 if hp["gemm_prec"] == "bf16" else identity
         self.dims_actor = layer_dims("actor", obs_dim, act_dim, hidden, self.algo)
         self.dims_critic = layer_dims("critic", obs_dim, act_dim, hidden, self.algo)
@@ -260,7 +266,7 @@ class Oracle:
         return lq, out
 
     def _critic_action_grad(self, s, a_pi, dq_by_net):
-        """dL/da for L = sum_i <dq_i, Q_i(s, a)>, critics held at their step-start values."""
+        """dL/da for L = sum_i <dq_i, Q_i(s, a)> at the current critic parameters (held fixed)."""
         rnd = self.rnd
         x = np.concatenate([s, a_pi], axis=1)
         da = np.zeros_like(a_pi)
@@ -283,7 +289,8 @@ class Oracle:
 
     def sac_actor(self, s, eps_pol, alpha):
         """Actor loss and gradient: reparameterised sample on s, twin-Q minimum at the
-        step-start critics. Returns (L_pi, actor grads, policy dict)."""
+        current critics (step-start under snapshot ordering, updated under sequential).
+        Returns (L_pi, actor grads, policy dict)."""
         hp, B, A, rnd = self.hp, self.B, self.A, self.rnd
         lmin, lmax = hp["log_std_min"], hp["log_std_max"]
         z, xs_a = forward(self.net["actor"], s, rnd)
@@ -317,7 +324,7 @@ class Oracle:
         return r + hp["gamma"] * (1.0 - d) * np.minimum(qt1, qt2), a2
 
     def td3_actor(self, s):
-        """Deterministic policy gradient through Q1 at the step-start critic."""
+        """Deterministic policy gradient through Q1 at the current critic."""
         B, rnd = self.B, self.rnd
         z, xs_a = forward(self.net["actor"], s, rnd)
         ap = np.tanh(z)
@@ -341,6 +348,8 @@ class Oracle:
 
         y, _ = self.sac_target(s2, r, d, eps_tgt, alpha)
         lq, cg = self._critic_grads(s, a, y)
+        if self.sequential:
+            self._step_critics(cg)
         lpi, ag, pol = self.sac_actor(s, eps_pol, alpha)
         mean_lp_h = float(np.mean(pol["logp"] + hp["target_entropy"]))
         l_alpha = -log_alpha * mean_lp_h
@@ -348,8 +357,9 @@ class Oracle:
         self.last_grads = {"actor": ag, "critic1": cg["critic1"], "critic2": cg["critic2"],
                            "log_alpha": g_alpha, "y": y, "logp": pol["logp"]}
 
-        # Optimizer writes happen after both gradients exist (snapshot semantics).
-        self._step_critics(cg)
+        # Snapshot semantics: optimizer writes happen after both gradients exist.
+        if not self.sequential:
+            self._step_critics(cg)
         self.opt_actor.step(_tensors(self.net["actor"]), _tensors(ag), self.m["actor"], self.v["actor"])
         if hp["learn_alpha"]:
             self.opt_alpha.step([self.log_alpha], [np.array([g_alpha])], self.m["log_alpha"],
@@ -371,10 +381,13 @@ class Oracle:
         y, _ = self.td3_target(s2, r, d, eps_tgt)
         lq, cg = self._critic_grads(s, a, y)
         actor_step = (k % hp["policy_delay"]) == 0
+        if self.sequential:
+            self._step_critics(cg)
         lpi, ag = self.td3_actor(s) if actor_step else (0.0, None)
         self.last_grads = {"actor": ag, "critic1": cg["critic1"], "critic2": cg["critic2"], "y": y}
 
-        self._step_critics(cg)
+        if not self.sequential:
+            self._step_critics(cg)
         if actor_step:
             self.opt_actor.step(_tensors(self.net["actor"]), _tensors(ag), self.m["actor"], self.v["actor"])
             for key in ("critic1", "critic2", "actor"):

@@ -22,6 +22,8 @@
 //   actor stream:  actor forward on s, critics on (s, a~), actor loss, critic
 //                  input-gradient to the action, head backward, actor backward
 //   s0: join -> finish (loss record, temperature gradient, step counter) -> Adam + Polyak
+// Sequential ordering (the published algorithms' order) runs everything on s0 and
+// moves the critics' Adam + Polyak between the critic part and the actor part.
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
@@ -521,9 +523,41 @@ hipError_t actor_part(spz_ctx* c, hipStream_t s) {
   return actor_backward(c, s);
 }
 
+// Adam (+ Polyak) over the parameter arena. critics / actor select the optimizer
+// ranges of this launch; step_add is 1 when the step counter has not been advanced
+// by k_finish yet.
+hipError_t adam(spz_ctx* c, bool critics, bool actor_step, bool actor, int step_add, hipStream_t s) {
+  const Net& an = c->net[0];
+  AdamArgs a{};
+  a.P = c->P; a.M = c->M; a.V = c->V; a.T = c->T; a.G = c->G; a.Pb = c->Pb; a.Tb = c->Tb;
+  a.n = c->n_arena;
+  a.a0 = an.off; a.a1 = an.end;
+  a.c0 = c->net[1].off; a.c1 = c->net[2].end;
+  a.la = c->la;
+  a.do_critic = critics ? 1 : 0;
+  a.do_actor = (actor && actor_step) ? 1 : 0;
+  a.do_alpha = (actor && !c->td3 && c->hp.learn_alpha) ? 1 : 0;
+  a.polyak_critic = (critics && (!c->td3 || actor_step)) ? 1 : 0;
+  a.polyak_actor = (actor && c->td3 && actor_step) ? 1 : 0;
+  a.td3 = c->td3 ? 1 : 0;
+  a.delay = c->hp.policy_delay;
+  a.lr_a = c->hp.lr_actor; a.lr_c = c->hp.lr_critic; a.lr_al = c->hp.lr_alpha;
+  a.b1 = c->hp.beta1; a.b2 = c->hp.beta2; a.eps = c->hp.eps; a.tau = c->hp.tau;
+  a.step = c->d_step;
+  a.step_add = step_add;
+  const double n_crit = (double)(c->net[2].end - c->net[1].off);
+  const double n_act = (double)(an.end - an.off);
+  const double n_adam = (critics ? n_crit : 0.0) + (a.do_actor ? n_act : 0.0) + (a.do_alpha ? 1.0 : 0.0);
+  const double n_pol = (a.polyak_critic ? n_crit : 0.0) + (a.polyak_actor ? n_act : 0.0);
+  const double bytes = 28.0 * n_adam + 8.0 * n_pol + (c->bf16 ? 2.0 * (n_adam + n_pol) : 0.0);
+  return timed(c, "adam_polyak", (int)c->n_arena, 0, (critics ? 2 : 0) + (actor ? 1 : 0), 0.0, bytes, s,
+               [&] { return launch_adam(a, s); });
+}
+
 int enqueue_step(spz_ctx* c, hipStream_t s0) {
   const int64_t t = c->h_step + 1;
   const bool actor_step = !c->td3 || (t % c->hp.policy_delay == 0);
+  const bool sequential = c->hp.ordering == SPZ_ORDER_SEQUENTIAL;
   GatherArgs g{c->buf, c->row_bytes, c->off_a, c->off_s2, c->off_r, c->off_d, c->O, c->A, c->Ka, c->Kc,
                c->B, c->seed, (uint32_t)c->size, c->d_step, c->xsa, c->xs2, c->xsp, c->r, c->d, c->idx};
   {
@@ -532,7 +566,7 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
     CK(timed(c, "gather", c->B, c->O, c->A, 0.0, bytes, s0, [&] { return launch_gather(c->bf16, g, s0); }));
   }
   hipStream_t sc = s0, sa = s0;
-  const bool two = c->hp.n_streams == 2;
+  const bool two = c->hp.n_streams == 2 && !sequential;
   if (two) {
     CK(hipEventRecord(c->ev_fork, s0));
     CK(hipStreamWaitEvent(c->sc, c->ev_fork, 0));
@@ -541,6 +575,9 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
     sa = c->sa;
   }
   CK(critic_part(c, sc));
+  // Sequential ordering: the critics step (and their targets move) before the
+  // actor's loss is taken through them.
+  if (sequential) CK(adam(c, true, actor_step, false, 1, s0));
   if (actor_step) CK(actor_part(c, sa));
   if (two) {
     CK(hipEventRecord(c->ev_c, sc));
@@ -554,30 +591,7 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
                actor_step ? 1 : 0, c->hp.learn_alpha, c->hp.target_entropy, log_alpha_ptr(c),
                c->td3 ? nullptr : c->G + c->la, c->rec, c->rec_cap, c->d_step};
   CK(timed(c, "finish", 0, 0, 0, 0.0, 0.0, s0, [&] { return launch_finish(f, s0); }));
-  const Net& an = c->net[0];
-  AdamArgs a{};
-  a.P = c->P; a.M = c->M; a.V = c->V; a.T = c->T; a.G = c->G; a.Pb = c->Pb; a.Tb = c->Tb;
-  a.n = c->n_arena;
-  a.a0 = an.off; a.a1 = an.end;
-  a.c0 = c->net[1].off; a.c1 = c->net[2].end;
-  a.la = c->la;
-  a.do_actor = actor_step ? 1 : 0;
-  a.do_alpha = (!c->td3 && c->hp.learn_alpha) ? 1 : 0;
-  a.polyak_critic = (!c->td3 || actor_step) ? 1 : 0;
-  a.polyak_actor = (c->td3 && actor_step) ? 1 : 0;
-  a.td3 = c->td3 ? 1 : 0;
-  a.delay = c->hp.policy_delay;
-  a.lr_a = c->hp.lr_actor; a.lr_c = c->hp.lr_critic; a.lr_al = c->hp.lr_alpha;
-  a.b1 = c->hp.beta1; a.b2 = c->hp.beta2; a.eps = c->hp.eps; a.tau = c->hp.tau;
-  a.step = c->d_step;
-  {
-    const double n_adam = (double)(c->net[2].end - c->net[1].off) + (actor_step ? (double)(an.end - an.off) : 0.0) +
-                          (a.do_alpha ? 1.0 : 0.0);
-    const double n_pol = (a.polyak_critic ? (double)(c->net[2].end - c->net[1].off) : 0.0) +
-                         (a.polyak_actor ? (double)(an.end - an.off) : 0.0);
-    const double bytes = 28.0 * n_adam + 8.0 * n_pol + (c->bf16 ? 2.0 * (n_adam + n_pol) : 0.0);
-    CK(timed(c, "adam_polyak", (int)c->n_arena, 0, actor_step ? 1 : 0, 0.0, bytes, s0, [&] { return launch_adam(a, s0); }));
-  }
+  CK(adam(c, !sequential, actor_step, true, 0, s0));
   c->h_step = t;
   return SPZ_OK;
 }
@@ -788,6 +802,7 @@ void spz_hparams_default(spz_hparams* hp) {
   hp->policy_delay = 2;
   hp->device = 0;
   hp->n_streams = 2;
+  hp->ordering = SPZ_ORDER_SNAPSHOT;
 }
 
 spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int32_t n_hidden, int32_t batch,
@@ -807,7 +822,8 @@ spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int
       (hp->gemm_prec != SPZ_PREC_FP32 && hp->gemm_prec != SPZ_PREC_BF16) || hp->capacity < 1 ||
       hp->capacity > 0xFFFFFFFFll || !(hp->tau >= 0.0f && hp->tau <= 1.0f) ||
       (hp->algo == SPZ_ALGO_SAC && !(hp->alpha_init > 0.0f)) || hp->policy_delay < 1 ||
-      (hp->n_streams != 1 && hp->n_streams != 2) || !(hp->log_std_min <= hp->log_std_max)) {
+      (hp->n_streams != 1 && hp->n_streams != 2) || !(hp->log_std_min <= hp->log_std_max) ||
+      (hp->ordering != SPZ_ORDER_SNAPSHOT && hp->ordering != SPZ_ORDER_SEQUENTIAL)) {
     set_err(nullptr, SPZ_EINVAL, "spz_create: invalid hyper-parameters");
     return nullptr;
   }

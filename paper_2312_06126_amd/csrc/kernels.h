@@ -81,9 +81,10 @@ struct ColsumArgs {
 struct AdamArgs {
   float *P, *M, *V, *T; const float* G; bf16_t *Pb, *Tb;
   int64_t n, a0, a1, c0, c1, la;
-  int do_actor, do_alpha, polyak_critic, polyak_actor, td3, delay;
+  int do_actor, do_critic, do_alpha, polyak_critic, polyak_actor, td3, delay;
   float lr_a, lr_c, lr_al, b1, b2, eps, tau;
   const int64_t* step;
+  int step_add;   // the step being completed is *step + step_add (1 before k_finish ran)
 };
 
 struct FinishArgs {

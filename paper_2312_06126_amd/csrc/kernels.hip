@@ -474,9 +474,9 @@ __global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ 
 __global__ void __launch_bounds__(256) k_adam_polyak(AdamArgs a) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n) return;
-  const int64_t t = *a.step;
+  const int64_t t = *a.step + a.step_add;
   const bool in_actor = i >= a.a0 && i < a.a1;
-  const bool in_critic = i >= a.c0 && i < a.c1;
+  const bool in_critic = i >= a.c0 && i < a.c1 && a.do_critic;
   const bool is_alpha = i == a.la;
   float lr;
   int64_t tt;

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspz.so")
 SPZ_OK, SPZ_EINVAL, SPZ_ENOMEM, SPZ_EEMPTY, SPZ_ESIZE, SPZ_EHIP = 0, -1, -2, -3, -4, -5
 ALGOS = {"sac": 0, "td3": 1}
 PRECS = {"fp32": 0, "bf16": 1}
+ORDERINGS = {"snapshot": 0, "sequential": 1}
 SELECTORS = {
     "actor": 0, "critic1": 1, "critic2": 2, "tcritic1": 3, "tcritic2": 4, "tactor": 5, "log_alpha": 6,
     "m_actor": 7, "m_critic1": 8, "m_critic2": 9, "m_log_alpha": 10,
@@ -44,7 +45,8 @@ class Hparams(ctypes.Structure):
                 ("learn_alpha", ctypes.c_int32), ("target_entropy", ctypes.c_float),
                 ("log_std_min", ctypes.c_float), ("log_std_max", ctypes.c_float),
                 ("policy_noise", ctypes.c_float), ("noise_clip", ctypes.c_float),
-                ("policy_delay", ctypes.c_int32), ("device", ctypes.c_int32), ("n_streams", ctypes.c_int32)]
+                ("policy_delay", ctypes.c_int32), ("device", ctypes.c_int32), ("n_streams", ctypes.c_int32),
+                ("ordering", ctypes.c_int32)]
 
 
 class KernelStat(ctypes.Structure):
@@ -109,6 +111,8 @@ def make_hparams(d: dict, device: int = 0, n_streams: int = 2) -> Hparams:
             v = PRECS[v]
         elif k == "learn_alpha":
             v = int(bool(v))
+        elif k == "ordering":
+            v = ORDERINGS[v]
         setattr(hp, k, v)
     hp.device = device
     hp.n_streams = n_streams

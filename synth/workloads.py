@@ -43,6 +43,7 @@ class Workload:
     policy_noise: float = 0.2
     noise_clip: float = 0.5
     policy_delay: int = 2
+    ordering: str = "snapshot"  # "snapshot" | "sequential" (update order within a step)
 
     def hparams(self) -> dict:
         """Hyper-parameters as a plain dict (the key names of the C struct spz_hparams)."""
@@ -52,7 +53,7 @@ class Workload:
                     alpha_init=self.alpha_init, learn_alpha=self.learn_alpha,
                     target_entropy=self.target_entropy, log_std_min=self.log_std_min,
                     log_std_max=self.log_std_max, policy_noise=self.policy_noise,
-                    noise_clip=self.noise_clip, policy_delay=self.policy_delay)
+                    noise_clip=self.noise_clip, policy_delay=self.policy_delay, ordering=self.ordering)
 
     def replace(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)

@@ -38,6 +38,11 @@ FUSED_BF16 = RAGGED_BF16.replace(name="fused_sac_bf16", hidden=(256, 128), batch
 FUSED_BF16_DEEP = RAGGED_BF16.replace(name="fused_sac_bf16_deep", hidden=(128, 256, 384), batch=768)
 FUSED_TD3_BF16 = RAGGED_TD3.replace(name="fused_td3_bf16", prec="bf16", zero_mod=10, hidden=(256, 256), batch=256)
 
+# Sequential update ordering (critics step first, the actor sees the updated critics).
+SEQ_SAC = RAGGED.replace(name="ragged_sac_seq", ordering="sequential")
+SEQ_TD3 = RAGGED_TD3.replace(name="ragged_td3_seq", ordering="sequential")
+SEQ_BF16 = FUSED_BF16.replace(name="fused_sac_bf16_seq", ordering="sequential")
+
 FP32_TOL = 1e-4
 BF16_LOSS_TOL = 2e-2
 
@@ -148,6 +153,14 @@ def test_teacher_forced_bf16_fused(w, n_steps):
     teacher_forced(w, 5000, steps_before=1, tol_grad=1e-3, tol_loss=BF16_LOSS_TOL, n_steps=n_steps)
 
 
+@pytest.mark.parametrize("w,n_steps,tol", [(SEQ_SAC, 2, FP32_TOL), (SEQ_TD3, 2, FP32_TOL), (SEQ_BF16, 1, 1e-3)],
+                         ids=["sac_fp32", "td3_fp32", "sac_bf16_fused"])
+def test_teacher_forced_sequential(w, n_steps, tol):
+    log("teacher-forced %s" % w.name)
+    teacher_forced(w, 5000, steps_before=1, tol_grad=tol, tol_loss=FP32_TOL if tol == FP32_TOL else BF16_LOSS_TOL,
+                   n_steps=n_steps)
+
+
 def test_teacher_forced_log_std_clamp_active():
     """Push the log-std head beyond both clamp bounds through write_params."""
     w = RAGGED
@@ -207,6 +220,14 @@ def test_ten_step_parity_fp32(w, rows, virtual):
     check_ten_step_params(w, params, o, hist, 10)
 
 
+@pytest.mark.parametrize("w", [SEQ_SAC, SEQ_TD3], ids=["sac", "td3"])
+def test_ten_step_parity_sequential(w):
+    log("10-step %s" % w.name)
+    rg, ro, params, o, hist = ten_steps(w, 5000)
+    check_losses(rg, ro, FP32_TOL, w.name)
+    check_ten_step_params(w, params, o, hist, 10)
+
+
 @pytest.mark.slow
 def test_td3_full_batch_parity():
     w = W["td3_ant"].replace(capacity=200_000)
@@ -243,6 +264,21 @@ def test_stream_and_chunk_invariance_bit_exact():
     for r in runs[1:]:
         for k in r:
             assert np.array_equal(r[k], runs[0][k]), k
+
+
+def test_sequential_runs_on_one_stream_and_differs_from_snapshot():
+    """The sequential ordering ignores the second stream (bit-identical runs) and
+    moves the actor differently from the snapshot ordering."""
+    runs = []
+    for w, n_streams in ((SEQ_SAC, 2), (SEQ_SAC, 1), (RAGGED, 1)):
+        g = make_gpu(w, n_streams=n_streams)
+        g.buffer_push(*synth.workload_rows(w, 0, 5000, 0))
+        g.update(3)
+        runs.append({k: g.read_params(k) for k in ("actor", "critic1", "log_alpha")})
+        g.close()
+    for k in runs[0]:
+        assert np.array_equal(runs[0][k], runs[1][k]), k
+    assert not np.array_equal(runs[0]["actor"], runs[2]["actor"])
 
 
 def test_tau_one_targets_equal_online_bit_exact():

@@ -273,6 +273,70 @@ def test_snapshot_semantics_actor_reads_step_start_critic():
     assert np.array_equal(idx, philox.indices(o.seed, 1, B, 40))
 
 
+def test_sequential_with_frozen_critics_equals_snapshot():
+    """With lr_critic = 0 the critics' Adam step leaves them unchanged, so the two
+    update orderings must agree bit for bit over several steps (SAC and TD3)."""
+    for algo in ("sac", "td3"):
+        a = _filled(algo, lr_critic=0.0)
+        b = _filled(algo, lr_critic=0.0, ordering="sequential")
+        a.update(4)
+        b.update(4)
+        keys = ["actor", "critic1", "critic2", "tcritic1", "tcritic2"] + (["tactor"] if algo == "td3" else [])
+        for k in keys:
+            assert np.array_equal(a.params(k), b.params(k)), (algo, k)
+        assert np.array_equal(a.losses(), b.losses()), algo
+
+
+def test_sequential_sac_actor_reads_updated_critics():
+    """Sequential ordering: the critic side of the step is the snapshot one, and the
+    actor loss and gradient are the snapshot formulas evaluated at the critics after
+    this step's critic update (and differ from the step-start ones)."""
+    o = _filled(ordering="sequential")
+    start = copy.deepcopy(o)
+    twin = _filled()
+    o.update(1)
+    twin.update(1)
+    for k in ("critic1", "critic2", "tcritic1", "tcritic2"):
+        assert np.array_equal(o.params(k), twin.params(k)), k
+    assert o.losses()[0, U.REC_LQ] == twin.losses()[0, U.REC_LQ]
+    s = o.last_batch[0]
+    eps = philox.normals(o.seed, 1, philox.PURPOSE_NOISE_POL, B * A).reshape(B, A)
+    ref = copy.deepcopy(start)
+    for k in ("critic1", "critic2"):
+        ref.set_params(k, o.params(k))
+    lpi_new, ag_new, pol = ref.sac_actor(s, eps, HP["alpha_init"])
+    lpi_old, _, _ = start.sac_actor(s, eps, HP["alpha_init"])
+    assert np.isclose(o.losses()[0, U.REC_LPI], lpi_new, rtol=1e-14)
+    assert abs(lpi_new - lpi_old) > 1e-9 * abs(lpi_old)
+    for l, (gw, gb) in enumerate(ag_new):
+        np.testing.assert_allclose(o.last_grads["actor"][l][0], gw, rtol=1e-13, atol=1e-300)
+        np.testing.assert_allclose(o.last_grads["actor"][l][1], gb, rtol=1e-13, atol=1e-300)
+    # the temperature still sees the step-start actor sample
+    assert np.isclose(o.losses()[0, U.REC_LOGPI], np.mean(pol["logp"]), rtol=1e-14)
+    assert o.losses()[0, U.REC_LOGPI] == twin.losses()[0, U.REC_LOGPI]
+
+
+def test_sequential_td3_actor_reads_updated_critic():
+    """TD3: on the delayed step the actor gradient goes through the critic after that
+    step's critic update; on the other steps only the critics move, as in snapshot."""
+    o = _filled("td3", ordering="sequential")
+    o.update(1)
+    start = copy.deepcopy(o)
+    o.update(1)                       # step 2: critic update, then actor update
+    s = o.last_batch[0]
+    ref = copy.deepcopy(start)
+    ref.t = 2
+    for k in ("critic1", "critic2"):
+        ref.set_params(k, o.params(k))
+    lpi_new, ag_new = ref.td3_actor(s)
+    lpi_old, _ = start.td3_actor(s)
+    assert np.isclose(o.losses()[1, U.REC_LPI], lpi_new, rtol=1e-14)
+    assert abs(lpi_new - lpi_old) > 1e-9 * abs(lpi_old)
+    for l, (gw, gb) in enumerate(ag_new):
+        np.testing.assert_allclose(o.last_grads["actor"][l][0], gw, rtol=1e-13, atol=1e-300)
+    assert o.opt_actor.t == 1 and o.opt_critic.t == 2
+
+
 def test_step_zero_params_are_the_fanin_init():
     o = tiny()
     w0 = o.net["critic2"][0][0]
