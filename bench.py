@@ -168,6 +168,9 @@ def main():
                          "durations then overlap, so the roofline is taken from 1-stream runs)")
     ap.add_argument("--sweep", action="store_true",
                     help="also time the batch sizes 16384..131072 of the workload and report the knee")
+    ap.add_argument("--autotune", action="store_true",
+                    help="also run the library's adaptive batch-size controller (spz_autotune_batch) "
+                         "from batch 16384 on a context created with the workload's batch")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--data-seed", type=int, default=0)
     ap.add_argument("--cpu-sample-batch", type=int, default=16384)
@@ -250,6 +253,14 @@ def main():
                           for s in stats[:40]]
     if args.sweep:
         out["sweep"] = sweep(w, args, stream)
+    if args.autotune:
+        g = Spz(w.obs_dim, w.act_dim, w.hidden, w.batch, w.hparams(), args.seed, n_streams=args.streams)
+        fill_ring(g, w, args.data_seed, w.capacity)
+        chosen, probes = g.autotune_batch(min(16384, w.batch), 50, 0.05, stream)
+        g.close()
+        out["autotune"] = dict(chosen_batch=chosen, probe_steps=50, tolerance=0.05,
+                               probes=[dict(batch=b, value=round(r, 1)) for b, r in probes])
+        progress("autotune chose batch %d from %s" % (chosen, probes))
     if not args.no_cpu_baseline:
         progress("cpu baseline (oracle) at batch %d" % args.cpu_sample_batch)
         out["cpu_baseline"] = cpu_baseline(w, args.seed, args.data_seed, args.cpu_sample_batch)

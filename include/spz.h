@@ -165,6 +165,32 @@ int spz_update(spz_ctx* ctx, int32_t n_steps, void* hip_stream);
 /* Wait for all work the context enqueued. */
 int spz_synchronize(spz_ctx* ctx);
 
+/* Batch size of subsequent updates (the paper's adaptive batch size, Sections
+ * 3.2.1 and 3.4). 1 <= batch <= the batch given to spz_create, which sizes every
+ * batch buffer. Waits for the context's outstanding work. A row's replay index
+ * and noise depend only on (seed, step, row), so a context set to `batch`
+ * computes what a context created with `batch` computes. Errors: SPZ_EINVAL. */
+int spz_set_batch(spz_ctx* ctx, int32_t batch);
+
+/* Current batch size (SPZ_EINVAL for NULL). */
+int32_t spz_batch(const spz_ctx* ctx);
+
+/* Adaptive batch size (Section 3.4: geometric enumeration, stopping where the
+ * update frame rate saturates). Probes batch sizes b_min, 2 b_min, 4 b_min, ...
+ * (the last one capped at the created batch): at each, one untimed update step,
+ * then probe_steps timed steps on hip_stream (events); frame rate = batch x steps
+ * / seconds. Stops after the first probe that is below (1 + tolerance) x the best
+ * rate so far, or at the created batch, then sets the batch to the smallest probed
+ * size within (1 - tolerance) of the best rate and returns it in *chosen. The
+ * probes are real update steps: they advance the step counter and the networks.
+ * batches / frames_per_s (host, max_probes entries, may be NULL when max_probes
+ * is 0) receive the probes in order; *n_probes (may be NULL) their number.
+ * Synchronous. Errors: SPZ_EINVAL (b_min outside [1, created batch],
+ * probe_steps < 1, tolerance outside [0, 1)), SPZ_EEMPTY, SPZ_EHIP. */
+int spz_autotune_batch(spz_ctx* ctx, int32_t b_min, int32_t probe_steps, float tolerance, void* hip_stream,
+                       int32_t* chosen, int32_t* batches, float* frames_per_s, int32_t max_probes,
+                       int32_t* n_probes);
+
 /* Number of update steps enqueued so far (the step counter t of the last step). */
 int64_t spz_step(const spz_ctx* ctx);
 

@@ -229,6 +229,13 @@ class Oracle:
         return count(self.dims(key))
 
     # ---------------------------------------------------------------- the step
+    def set_batch(self, batch: int):
+        """Batch size of the following steps; a row's index and noise depend only on
+        (seed, step, row), so this equals a learner created with that batch."""
+        if batch < 1:
+            raise ValueError("batch must be >= 1")
+        self.B = int(batch)
+
     def update(self, n_steps: int):
         if self.size == 0:
             raise RuntimeError("replay buffer is empty")

@@ -57,6 +57,8 @@ inline int64_t align16(int64_t x) { return (x + 15) / 16 * 16; }
 struct spz_ctx {
   // configuration
   int O = 0, A = 0, B = 0, Bp = 0, Ka = 0, Ap = 0, Kc = 0;
+  int Bmax = 0, Bpmax = 0;   // batch given to spz_create: sizes every batch buffer
+  int64_t wpart_cap = 0;     // floats of each split-K partial buffer
   std::vector<int> hidden;
   spz_hparams hp{};
   uint64_t seed = 0;
@@ -701,6 +703,7 @@ int setup(spz_ctx* c) {
   // column-sum partials: first-pass chunks of the standalone kernel, or one row per
   // 256-row tile of a fused dgrad epilogue
   const int chunks = std::max(colsum_chunks((int)Bp), (int)(Bp / 256));
+  c->wpart_cap = wmax;
   CK(dalloc_t(c, &c->c_wpart, (size_t)wmax * 4));
   CK(dalloc_t(c, &c->a_wpart, (size_t)wmax * 4));
   CK(dalloc_t(c, &c->c_cpart, (size_t)chunks * cmax * 4));
@@ -838,6 +841,8 @@ spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int
   c->A = act_dim;
   c->B = batch;
   c->Bp = (batch + 255) / 256 * 256;
+  c->Bmax = c->B;
+  c->Bpmax = c->Bp;
   c->hidden.assign(hidden, hidden + n_hidden);
   c->hp = *hp;
   c->seed = seed;
@@ -914,6 +919,90 @@ int spz_update(spz_ctx* c, int32_t n_steps, void* hip_stream) {
     if (rc) return rc;
   }
   return SPZ_OK;
+}
+
+int spz_set_batch(spz_ctx* c, int32_t batch) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_set_batch: NULL context");
+  if (batch < 1 || batch > c->Bmax) return set_err(c, SPZ_EINVAL, "spz_set_batch: batch out of [1, created batch]");
+  const int Bp = (batch + 255) / 256 * 256;
+  for (int ni = 0; ni < 3; ++ni)
+    for (const Lay& L : c->net[ni].L)
+      if ((int64_t)wgrad_splits(c->bf16, L.out_p, L.in_p, Bp) * L.out_p * L.in_p > c->wpart_cap)
+        return set_err(c, SPZ_EINVAL, "spz_set_batch: split-K workspace too small for this batch");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  // Rows [batch, Bp) of the batch operands and of the actor head gradient must be
+  // zero (pad rows carry no gradient); a larger earlier batch may have left data there.
+  if (Bp > batch) {
+    const size_t e = es(c);
+    const size_t pad = (size_t)(Bp - batch);
+    for (void* x : {c->xsa, c->xs2, c->xsp})
+      CK(hipMemset(static_cast<uint8_t*>(x) + (size_t)batch * c->Kc * e, 0, pad * c->Kc * e));
+    const int pa = c->net[0].L.back().out_p;
+    CK(hipMemset(static_cast<uint8_t*>(c->dzh) + (size_t)batch * pa * e, 0, pad * pa * e));
+  }
+  c->B = batch;
+  c->Bp = Bp;
+  return SPZ_OK;
+}
+
+int32_t spz_batch(const spz_ctx* c) { return c ? c->B : SPZ_EINVAL; }
+
+int spz_autotune_batch(spz_ctx* c, int32_t b_min, int32_t probe_steps, float tolerance, void* hip_stream,
+                       int32_t* chosen, int32_t* batches, float* frames_per_s, int32_t max_probes,
+                       int32_t* n_probes) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_autotune_batch: NULL context");
+  if (b_min < 1 || b_min > c->Bmax || probe_steps < 1 || !(tolerance >= 0.0f && tolerance < 1.0f) || !chosen ||
+      max_probes < 0 || (max_probes > 0 && (!batches || !frames_per_s)))
+    return set_err(c, SPZ_EINVAL, "spz_autotune_batch: invalid arguments");
+  if (c->size == 0) return set_err(c, SPZ_EEMPTY, "spz_autotune_batch: replay buffer is empty");
+  CK(hipSetDevice(c->hp.device));
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  CK(hipEventCreate(&e0));
+  if (hipEventCreate(&e1) != hipSuccess) {
+    (void)hipEventDestroy(e0);
+    return set_err(c, SPZ_EHIP, "spz_autotune_batch: hipEventCreate failed");
+  }
+  std::vector<std::pair<int, double>> probes;
+  int rc = SPZ_OK;
+  double best = 0.0;
+  for (int64_t b = b_min;; b *= 2) {
+    const int bb = (int)std::min<int64_t>(b, c->Bmax);
+    if ((rc = spz_set_batch(c, bb))) break;
+    // one untimed step at the new size (first launches of new kernel shapes), then the probe
+    if ((rc = spz_update(c, 1, s))) break;
+    if (hipEventRecord(e0, s) != hipSuccess) { rc = set_err(c, SPZ_EHIP, "spz_autotune_batch: event"); break; }
+    if ((rc = spz_update(c, probe_steps, s))) break;
+    float ms = 0.0f;
+    if (hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+        hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+      rc = set_err(c, SPZ_EHIP, "spz_autotune_batch: event timing failed");
+      break;
+    }
+    const double rate = (double)bb * probe_steps / (ms * 1e-3);
+    probes.emplace_back(bb, rate);
+    // The frame rate is concave in the batch size: once doubling it gains less than
+    // the tolerance, larger batches only lower the update frequency.
+    const bool saturated = best > 0.0 && rate < best * (1.0 + tolerance);
+    best = std::max(best, rate);
+    if (saturated || bb == c->Bmax) break;
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (rc) return rc;
+  int pick = probes.back().first;
+  for (const auto& pr : probes)
+    if (pr.second >= best * (1.0 - tolerance)) { pick = pr.first; break; }
+  const int n = (int)probes.size();
+  for (int i = 0; i < n && i < max_probes; ++i) {
+    batches[i] = probes[i].first;
+    frames_per_s[i] = (float)probes[i].second;
+  }
+  if (n_probes) *n_probes = n;
+  *chosen = pick;
+  return spz_set_batch(c, pick);
 }
 
 int spz_synchronize(spz_ctx* c) {

@@ -28,7 +28,7 @@ REC_WIDTH = 8
 EXPORTS = ["spz_hparams_default", "spz_create", "spz_destroy", "spz_buffer_push", "spz_buffer_size",
            "spz_update", "spz_synchronize", "spz_step", "spz_set_step", "spz_param_count",
            "spz_read_params", "spz_write_params", "spz_read_losses", "spz_debug_read", "spz_last_error",
-           "spz_profile_enable", "spz_profile_read"]
+           "spz_profile_enable", "spz_profile_read", "spz_set_batch", "spz_batch", "spz_autotune_batch"]
 
 
 class SpzError(RuntimeError):
@@ -76,6 +76,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "spz_buffer_size": (ctypes.c_int64, [P]),
         "spz_update": (ctypes.c_int, [P, ctypes.c_int32, P]),
         "spz_synchronize": (ctypes.c_int, [P]),
+        "spz_set_batch": (ctypes.c_int, [P, ctypes.c_int32]),
+        "spz_batch": (ctypes.c_int32, [P]),
+        "spz_autotune_batch": (ctypes.c_int, [P, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, P,
+                                              ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
+                                              ctypes.POINTER(ctypes.c_float), ctypes.c_int32,
+                                              ctypes.POINTER(ctypes.c_int32)]),
         "spz_step": (ctypes.c_int64, [P]),
         "spz_set_step": (ctypes.c_int, [P, ctypes.c_int64]),
         "spz_param_count": (ctypes.c_int64, [P, ctypes.c_int32]),
@@ -173,6 +179,21 @@ class Spz:
 
     def synchronize(self):
         self._check(self.lib.spz_synchronize(self.ctx))
+
+    def set_batch(self, batch: int):
+        self._check(self.lib.spz_set_batch(self.ctx, int(batch)))
+        self.batch = int(self.lib.spz_batch(self.ctx))
+
+    def autotune_batch(self, b_min: int, probe_steps: int, tolerance: float = 0.05, stream=None, max_probes: int = 32):
+        """Adaptive batch size; returns (chosen, [(batch, frames/s), ...])."""
+        chosen = ctypes.c_int32(0)
+        n = ctypes.c_int32(0)
+        bs = (ctypes.c_int32 * max_probes)()
+        fr = (ctypes.c_float * max_probes)()
+        self._check(self.lib.spz_autotune_batch(self.ctx, b_min, probe_steps, tolerance, _stream_handle(stream),
+                                                ctypes.byref(chosen), bs, fr, max_probes, ctypes.byref(n)))
+        self.batch = int(self.lib.spz_batch(self.ctx))
+        return int(chosen.value), [(int(bs[i]), float(fr[i])) for i in range(min(n.value, max_probes))]
 
     def step(self) -> int:
         return int(self.lib.spz_step(self.ctx))

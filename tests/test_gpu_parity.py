@@ -281,6 +281,75 @@ def test_sequential_runs_on_one_stream_and_differs_from_snapshot():
     assert not np.array_equal(runs[0]["actor"], runs[2]["actor"])
 
 
+@pytest.mark.parametrize("w,created", [(RAGGED.replace(batch=600), 1000), (FUSED_BF16, 1000)],
+                         ids=["fp32", "bf16_fused"])
+def test_set_batch_equals_created_batch_bit_exact(w, created):
+    """A context created with a larger batch and set to w.batch computes exactly
+    what a context created with w.batch computes."""
+    log("set_batch %s" % w.name)
+    out = []
+    for b in (created, w.batch):
+        g = make_gpu(w.replace(batch=b))
+        g.buffer_push(*synth.workload_rows(w, 0, 5000, 0))
+        if b != w.batch:
+            g.set_batch(w.batch)
+        assert g.batch == w.batch
+        g.update(3)
+        out.append({k: g.read_params(k) for k in ("actor", "critic1", "tcritic2", "log_alpha")})
+        out[-1]["rec"] = g.read_losses(1, 3)
+        out[-1]["idx"] = g.debug_indices()
+        g.close()
+    for k in out[0]:
+        assert np.array_equal(out[0][k], out[1][k]), k
+
+
+def test_batch_changes_mid_run_parity():
+    """Grow and shrink the batch between steps; the oracle follows the same sizes
+    (rows past the batch left by a larger earlier batch must not leak in)."""
+    w = RAGGED.replace(batch=1000)
+    log("batch changes %s" % w.name)
+    g, o = make_pair(w, 5000)
+    hist = {k: [] for k in NET_KEYS}
+    for b, n in ((1000, 2), (300, 2), (777, 1), (1000, 1), (40, 2)):
+        g.set_batch(b)
+        o.set_batch(b)
+        for _ in range(n):
+            g.update(1)
+            o.update(1)
+            assert np.array_equal(g.debug_indices(), o.last_idx.astype(np.int32))
+            for k in NET_KEYS:
+                hist[k].append(oracle_grad_flat(o, k))
+    check_losses(g.read_losses(1, o.t), o.losses(), FP32_TOL, w.name)
+    params = {k: (g.read_params(k), o.params(k)) for k in state_keys(w.algo) if not k.startswith(("m_", "v_"))}
+    check_ten_step_params(w, params, o, hist, o.t)
+    g.close()
+
+
+def test_autotune_batch_probes_geometrically():
+    """The controller probes b_min * 2^k up to the created batch (stopping at
+    saturation), picks one of the probed sizes, sets it, and its probes are real
+    update steps."""
+    from paper_2312_06126_amd.spz import SpzError
+    w = RAGGED.replace(batch=4096, capacity=20000)
+    g = make_gpu(w, n_streams=1)
+    g.buffer_push(*synth.workload_rows(w, 0, 20000, 0))
+    chosen, probes = g.autotune_batch(256, 3, 0.05)
+    log("autotune probes %s chosen %d" % (probes, chosen))
+    sizes = [b for b, _ in probes]
+    assert sizes[0] == 256
+    assert all(sizes[i + 1] == min(2 * sizes[i], 4096) for i in range(len(sizes) - 1))
+    assert chosen in sizes and g.batch == chosen
+    assert all(r > 0 for _, r in probes)
+    assert g.step() == 4 * len(probes)
+    rec = g.read_losses(1, g.step())
+    assert np.all(rec[:, 6] == 0)
+    with pytest.raises(SpzError):
+        g.autotune_batch(8192, 3, 0.05)
+    with pytest.raises(SpzError):
+        g.set_batch(4097)
+    g.close()
+
+
 def test_tau_one_targets_equal_online_bit_exact():
     w = RAGGED.replace(tau=1.0)
     g = make_gpu(w)

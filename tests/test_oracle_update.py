@@ -337,6 +337,21 @@ def test_sequential_td3_actor_reads_updated_critic():
     assert o.opt_actor.t == 1 and o.opt_critic.t == 2
 
 
+def test_set_batch_equals_created_batch():
+    """An oracle created with batch 5 and set to 3 equals one created with batch 3:
+    indices and noise of a row depend only on (seed, step, row)."""
+    a = _filled()
+    a.set_batch(3)
+    b = Oracle(O, A, H, 3, dict(HP), seed=11)
+    b.push(*[np.asarray(x) for x in (a.buf_obs[:40], a.buf_act[:40], a.buf_rew[:40], a.buf_done[:40],
+                                     a.buf_nobs[:40])])
+    a.update(3)
+    b.update(3)
+    assert np.array_equal(a.losses(), b.losses())
+    for k in ("actor", "critic1", "tcritic2", "log_alpha"):
+        assert np.array_equal(a.params(k), b.params(k)), k
+
+
 def test_step_zero_params_are_the_fanin_init():
     o = tiny()
     w0 = o.net["critic2"][0][0]
