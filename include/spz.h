@@ -46,6 +46,7 @@ typedef struct spz_ctx spz_ctx;
 #define SPZ_EEMPTY (-3) /* spz_update on an empty replay buffer                          */
 #define SPZ_ESIZE (-4)  /* caller's array length does not match the requested object     */
 #define SPZ_EHIP (-5)   /* a HIP runtime call failed (message has the HIP error string)  */
+#define SPZ_EIO (-6)    /* checkpoint file not writable / readable, or not this learner's */
 
 /* Algorithms and GEMM operand precisions. */
 #define SPZ_ALGO_SAC 0
@@ -164,6 +165,19 @@ int spz_update(spz_ctx* ctx, int32_t n_steps, void* hip_stream);
 
 /* Wait for all work the context enqueued. */
 int spz_synchronize(spz_ctx* ctx);
+
+/* Checkpoints (the paper publishes weights through files, Section 3.3.1). A file
+ * holds the whole learner state: online and target parameters, Adam moments,
+ * log(alpha), the step counter, the Philox seed, the loss records and, with
+ * SPZ_CKPT_RING, the replay ring with its write pointer and fill level. Loading it
+ * into a context with the same dimensions, algorithm and GEMM precision (and ring
+ * capacity, if the ring is in the file) continues bit-exactly where the saved one
+ * stood. Hyper-parameters (rates, tau, ...) and the batch size are the loading
+ * context's own. Both calls wait for the context's outstanding work.
+ * Errors: SPZ_EINVAL (NULL), SPZ_EIO (file or mismatch), SPZ_EHIP, SPZ_ENOMEM. */
+#define SPZ_CKPT_RING 1
+int spz_save(spz_ctx* ctx, const char* path, int32_t flags);
+int spz_load(spz_ctx* ctx, const char* path);
 
 /* Batch size of subsequent updates (the paper's adaptive batch size, Sections
  * 3.2.1 and 3.4). 1 <= batch <= the batch given to spz_create, which sizes every

@@ -921,6 +921,130 @@ int spz_update(spz_ctx* c, int32_t n_steps, void* hip_stream) {
   return SPZ_OK;
 }
 
+// ---------------------------------------------------------------------------- checkpoints
+namespace {
+
+struct CkptHeader {
+  char magic[8];
+  uint32_t version, flags;
+  int32_t O, A, n_hidden, hidden[8], algo, prec, pad_;
+  int64_t capacity, n_arena, row_bytes, rec_cap;
+  uint64_t seed;
+  int64_t step, ring_ptr, ring_size;
+};
+constexpr char CKPT_MAGIC[8] = {'S', 'P', 'Z', 'C', 'K', 'P', 'T', '1'};
+constexpr size_t CKPT_CHUNK = (size_t)64 << 20;
+
+// Device <-> file through a host bounce buffer, in chunks.
+int dev_to_file(spz_ctx* c, FILE* f, const void* dev, size_t bytes, std::vector<uint8_t>& tmp) {
+  for (size_t o = 0; o < bytes; o += CKPT_CHUNK) {
+    const size_t n = std::min(CKPT_CHUNK, bytes - o);
+    CK(hipMemcpy(tmp.data(), static_cast<const uint8_t*>(dev) + o, n, hipMemcpyDeviceToHost));
+    if (fwrite(tmp.data(), 1, n, f) != n) return set_err(c, SPZ_EIO, "spz_save: write failed");
+  }
+  return SPZ_OK;
+}
+int file_to_dev(spz_ctx* c, FILE* f, void* dev, size_t bytes, std::vector<uint8_t>& tmp) {
+  for (size_t o = 0; o < bytes; o += CKPT_CHUNK) {
+    const size_t n = std::min(CKPT_CHUNK, bytes - o);
+    if (fread(tmp.data(), 1, n, f) != n) return set_err(c, SPZ_EIO, "spz_load: file truncated");
+    CK(hipMemcpy(static_cast<uint8_t*>(dev) + o, tmp.data(), n, hipMemcpyHostToDevice));
+  }
+  return SPZ_OK;
+}
+
+void fill_header(const spz_ctx* c, CkptHeader& h) {
+  memset(&h, 0, sizeof(h));
+  memcpy(h.magic, CKPT_MAGIC, 8);
+  h.version = 1;
+  h.O = c->O;
+  h.A = c->A;
+  h.n_hidden = (int32_t)c->hidden.size();
+  for (size_t i = 0; i < c->hidden.size() && i < 8; ++i) h.hidden[i] = c->hidden[i];
+  h.algo = c->hp.algo;
+  h.prec = c->hp.gemm_prec;
+  h.capacity = c->cap;
+  h.n_arena = c->n_arena;
+  h.row_bytes = c->row_bytes;
+  h.rec_cap = c->rec_cap;
+}
+
+struct FileCloser {
+  FILE* f;
+  ~FileCloser() { if (f) fclose(f); }
+};
+
+}  // namespace
+
+int spz_save(spz_ctx* c, const char* path, int32_t flags) {
+  if (!c || !path) return set_err(c, SPZ_EINVAL, "spz_save: NULL argument");
+  if (flags & ~SPZ_CKPT_RING) return set_err(c, SPZ_EINVAL, "spz_save: unknown flags");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  CkptHeader h;
+  fill_header(c, h);
+  h.flags = (uint32_t)flags;
+  h.seed = c->seed;
+  h.step = c->h_step;
+  h.ring_ptr = c->ptr;
+  h.ring_size = c->size;
+  FileCloser fc{fopen(path, "wb")};
+  if (!fc.f) return set_err(c, SPZ_EIO, std::string("spz_save: cannot open ") + path);
+  if (fwrite(&h, sizeof(h), 1, fc.f) != 1) return set_err(c, SPZ_EIO, "spz_save: write failed");
+  std::vector<uint8_t> tmp;
+  try { tmp.resize(CKPT_CHUNK); } catch (...) { return set_err(c, SPZ_ENOMEM, "spz_save: host buffer"); }
+  const size_t ab = (size_t)c->n_arena * 4;
+  for (const float* a : {c->P, c->T, c->M, c->V})
+    if ((rc = dev_to_file(c, fc.f, a, ab, tmp))) return rc;
+  if ((rc = dev_to_file(c, fc.f, c->rec, (size_t)c->rec_cap * SPZ_REC_WIDTH * 4, tmp))) return rc;
+  if (flags & SPZ_CKPT_RING)
+    if ((rc = dev_to_file(c, fc.f, c->buf, (size_t)(c->row_bytes * c->cap), tmp))) return rc;
+  if (fflush(fc.f) != 0) return set_err(c, SPZ_EIO, "spz_save: flush failed");
+  return SPZ_OK;
+}
+
+int spz_load(spz_ctx* c, const char* path) {
+  if (!c || !path) return set_err(c, SPZ_EINVAL, "spz_load: NULL argument");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  FileCloser fc{fopen(path, "rb")};
+  if (!fc.f) return set_err(c, SPZ_EIO, std::string("spz_load: cannot open ") + path);
+  CkptHeader h, mine;
+  if (fread(&h, sizeof(h), 1, fc.f) != 1 || memcmp(h.magic, CKPT_MAGIC, 8) || h.version != 1)
+    return set_err(c, SPZ_EIO, "spz_load: not a checkpoint of this library");
+  fill_header(c, mine);
+  const bool ring = h.flags & SPZ_CKPT_RING;
+  if (h.O != mine.O || h.A != mine.A || h.n_hidden != mine.n_hidden ||
+      memcmp(h.hidden, mine.hidden, sizeof(h.hidden)) || h.algo != mine.algo || h.prec != mine.prec ||
+      h.n_arena != mine.n_arena || h.rec_cap != mine.rec_cap ||
+      (ring && (h.capacity != mine.capacity || h.row_bytes != mine.row_bytes)) || h.step < 0 ||
+      h.ring_size < 0 || h.ring_size > h.capacity || h.ring_ptr < 0 || h.ring_ptr >= std::max<int64_t>(h.capacity, 1))
+    return set_err(c, SPZ_EIO, "spz_load: checkpoint does not match this learner's configuration");
+  std::vector<uint8_t> tmp;
+  try { tmp.resize(CKPT_CHUNK); } catch (...) { return set_err(c, SPZ_ENOMEM, "spz_load: host buffer"); }
+  const size_t ab = (size_t)c->n_arena * 4;
+  for (float* a : {c->P, c->T, c->M, c->V})
+    if ((rc = file_to_dev(c, fc.f, a, ab, tmp))) return rc;
+  if ((rc = file_to_dev(c, fc.f, c->rec, (size_t)c->rec_cap * SPZ_REC_WIDTH * 4, tmp))) return rc;
+  if (ring) {
+    if ((rc = file_to_dev(c, fc.f, c->buf, (size_t)(c->row_bytes * c->cap), tmp))) return rc;
+    c->ptr = h.ring_ptr;
+    c->size = h.ring_size;
+  }
+  // The bf16 operand images are a pure function of the float32 parameters.
+  if (c->bf16) {
+    CK(launch_to_bf16(c->P, c->Pb, c->n_arena, c->sc));
+    CK(launch_to_bf16(c->T, c->Tb, c->n_arena, c->sc));
+    CK(hipStreamSynchronize(c->sc));
+  }
+  c->seed = h.seed;
+  CK(hipMemcpy(c->d_step, &h.step, 8, hipMemcpyHostToDevice));
+  c->h_step = h.step;
+  return SPZ_OK;
+}
+
 int spz_set_batch(spz_ctx* c, int32_t batch) {
   if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_set_batch: NULL context");
   if (batch < 1 || batch > c->Bmax) return set_err(c, SPZ_EINVAL, "spz_set_batch: batch out of [1, created batch]");

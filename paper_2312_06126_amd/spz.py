@@ -13,7 +13,7 @@ import numpy as np
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspz.so")
 
-SPZ_OK, SPZ_EINVAL, SPZ_ENOMEM, SPZ_EEMPTY, SPZ_ESIZE, SPZ_EHIP = 0, -1, -2, -3, -4, -5
+SPZ_OK, SPZ_EINVAL, SPZ_ENOMEM, SPZ_EEMPTY, SPZ_ESIZE, SPZ_EHIP, SPZ_EIO = 0, -1, -2, -3, -4, -5, -6
 ALGOS = {"sac": 0, "td3": 1}
 PRECS = {"fp32": 0, "bf16": 1}
 ORDERINGS = {"snapshot": 0, "sequential": 1}
@@ -28,7 +28,8 @@ REC_WIDTH = 8
 EXPORTS = ["spz_hparams_default", "spz_create", "spz_destroy", "spz_buffer_push", "spz_buffer_size",
            "spz_update", "spz_synchronize", "spz_step", "spz_set_step", "spz_param_count",
            "spz_read_params", "spz_write_params", "spz_read_losses", "spz_debug_read", "spz_last_error",
-           "spz_profile_enable", "spz_profile_read", "spz_set_batch", "spz_batch", "spz_autotune_batch"]
+           "spz_profile_enable", "spz_profile_read", "spz_set_batch", "spz_batch", "spz_autotune_batch",
+           "spz_save", "spz_load"]
 
 
 class SpzError(RuntimeError):
@@ -77,6 +78,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "spz_update": (ctypes.c_int, [P, ctypes.c_int32, P]),
         "spz_synchronize": (ctypes.c_int, [P]),
         "spz_set_batch": (ctypes.c_int, [P, ctypes.c_int32]),
+        "spz_save": (ctypes.c_int, [P, ctypes.c_char_p, ctypes.c_int32]),
+        "spz_load": (ctypes.c_int, [P, ctypes.c_char_p]),
         "spz_batch": (ctypes.c_int32, [P]),
         "spz_autotune_batch": (ctypes.c_int, [P, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, P,
                                               ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
@@ -179,6 +182,13 @@ class Spz:
 
     def synchronize(self):
         self._check(self.lib.spz_synchronize(self.ctx))
+
+    def save(self, path: str, ring: bool = True):
+        """Whole learner state to a file (with the replay ring unless ring=False)."""
+        self._check(self.lib.spz_save(self.ctx, os.fsencode(path), 1 if ring else 0))
+
+    def load(self, path: str):
+        self._check(self.lib.spz_load(self.ctx, os.fsencode(path)))
 
     def set_batch(self, batch: int):
         self._check(self.lib.spz_set_batch(self.ctx, int(batch)))
