@@ -166,6 +166,20 @@ int spz_update(spz_ctx* ctx, int32_t n_steps, void* hip_stream);
 /* Wait for all work the context enqueued. */
 int spz_synchronize(spz_ctx* ctx);
 
+/* Actions for the experience-sampling processes (Section 3.1.1: the policy
+ * network acts on the observations collected from N samplers; Section 3.1.2: the
+ * test and visualisation processes use the policy without randomisation).
+ * obs: host float32 [n, obs_dim]; act: host float32 [n, act_dim] (caller-owned).
+ * SAC: stochastic = 0 gives the mean action tanh(mu); stochastic = 1 a policy
+ * sample tanh(mu + exp(clip(log_std)) eps) with eps from Philox purpose 4 at
+ * counter `counter` (step word), element index row * act_dim + j, so a call is
+ * reproducible from (seed, counter). TD3: tanh of the actor output (stochastic must
+ * be 0; samplers add their own exploration noise). Uses the current online actor
+ * with the context's GEMM precision; rows are processed in chunks of the created
+ * batch. Waits for the context's outstanding work; synchronous.
+ * Errors: SPZ_EINVAL, SPZ_EHIP. */
+int spz_act(spz_ctx* ctx, const float* obs, int64_t n, int32_t stochastic, uint32_t counter, float* act);
+
 /* Checkpoints (the paper publishes weights through files, Section 3.3.1). A file
  * holds the whole learner state: online and target parameters, Adam moments,
  * log(alpha), the step counter, the Philox seed, the loss records and, with

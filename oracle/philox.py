@@ -25,6 +25,7 @@ PURPOSE_INIT = 0
 PURPOSE_IDX = 1
 PURPOSE_NOISE_TGT = 2
 PURPOSE_NOISE_POL = 3
+PURPOSE_ACT = 4          # sampler actions: step word = the caller's counter
 
 
 def block(c0, c1, c2, c3, k0, k1, rounds: int = 10):

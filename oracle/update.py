@@ -229,6 +229,27 @@ class Oracle:
         return count(self.dims(key))
 
     # ---------------------------------------------------------------- the step
+    def act(self, obs, stochastic: bool, counter: int):
+        """Actions of the current actor for sampler observations (the policy acting
+        for the sampling processes, Section 3.1.1; deterministic for test and
+        visualisation, Section 3.1.2). SAC: tanh(mu), or tanh(mu + sigma eps) with
+        eps from purpose ACT at step word `counter`; TD3: tanh(z)."""
+        hp = self.hp
+        obs = np.asarray(obs, np.float64)
+        n = obs.shape[0]
+        z, _ = forward(self.net["actor"], obs, self.rnd)
+        A = self.A
+        if self.algo == "td3":
+            if stochastic:
+                raise ValueError("TD3 actions are deterministic")
+            return np.tanh(z)
+        mu = z[:, :A]
+        if not stochastic:
+            return np.tanh(mu)
+        eps = philox.normals(self.seed, counter, philox.PURPOSE_ACT, n * A).reshape(n, A)
+        lc = np.clip(z[:, A:2 * A], hp["log_std_min"], hp["log_std_max"])
+        return np.tanh(mu + np.exp(lc) * eps)
+
     def set_batch(self, batch: int):
         """Batch size of the following steps; a row's index and noise depend only on
         (seed, step, row), so this equals a learner created with that batch."""

@@ -921,6 +921,46 @@ int spz_update(spz_ctx* c, int32_t n_steps, void* hip_stream) {
   return SPZ_OK;
 }
 
+// ---------------------------------------------------------------------------- sampler actions
+int spz_act(spz_ctx* c, const float* obs, int64_t n, int32_t stochastic, uint32_t counter, float* act) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_act: NULL context");
+  if (n < 0 || (n > 0 && (!obs || !act))) return set_err(c, SPZ_EINVAL, "spz_act: bad arrays");
+  if (stochastic && c->td3) return set_err(c, SPZ_EINVAL, "spz_act: TD3 policies are deterministic");
+  if (n == 0) return SPZ_OK;
+  CK(hipSetDevice(c->hp.device));
+  int rc = ctx_sync(c);
+  if (rc) return rc;
+  if (!c->stage) {
+    CK(hipMalloc(&c->stage, (size_t)(65536 * (2 * (int64_t)c->O + c->A + 2) * 4)));
+    c->stage_rows = 65536;
+  }
+  // Chunks of at most the created batch (the actor workspaces' row count) and of the
+  // observation staging area.
+  const int64_t chunk = std::min<int64_t>(c->Bpmax, c->stage_rows) / 256 * 256;
+  const int saveB = c->B, saveBp = c->Bp;
+  const int pa = c->net[0].L.back().out_p;
+  hipStream_t s = c->sc;
+  for (int64_t r0 = 0; r0 < n && rc == SPZ_OK; r0 += chunk) {
+    const int m = (int)std::min(chunk, n - r0);
+    const int rows = (m + 255) / 256 * 256;
+    hipError_t e = hipMemcpy(c->stage, obs + r0 * c->O, (size_t)m * c->O * 4, hipMemcpyHostToDevice);
+    ObsArgs oa{c->stage, m, rows, c->O, c->Ka, c->xsp, c->Kc};
+    if (e == hipSuccess) e = launch_obs_operand(c->bf16, oa, s);
+    c->B = m;
+    c->Bp = rows;
+    if (e == hipSuccess) e = forward(c, 0, false, c->xsp, c->Kc, c->ha.data(), nullptr, true, nullptr, c->z, s);
+    c->B = saveB;
+    c->Bp = saveBp;
+    ActHeadArgs ha{c->z, pa, c->A, m, r0, c->td3 ? 0 : 1, stochastic ? 1 : 0, c->seed, counter,
+                   c->hp.log_std_min, c->hp.log_std_max, c->th};
+    if (e == hipSuccess) e = launch_act_head(ha, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e == hipSuccess) e = hipMemcpy(act + r0 * c->A, c->th, (size_t)m * c->A * 4, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) rc = set_err(c, SPZ_EHIP, std::string("spz_act: ") + hipGetErrorString(e));
+  }
+  return rc;
+}
+
 // ---------------------------------------------------------------------------- checkpoints
 namespace {
 

@@ -83,7 +83,7 @@ __host__ __device__ inline uint32_t philox_word(uint64_t seed, uint64_t i, uint3
   switch (i & 3) { case 0: return o.x; case 1: return o.y; case 2: return o.z; default: return o.w; }
 }
 
-enum Purpose : uint32_t { P_INIT = 0, P_IDX = 1, P_NOISE_TGT = 2, P_NOISE_POL = 3 };
+enum Purpose : uint32_t { P_INIT = 0, P_IDX = 1, P_NOISE_TGT = 2, P_NOISE_POL = 3, P_ACT = 4 };
 
 // ----------------------------------------------------------------------------- GEMM
 enum GemmMode { GEMM_FWD = 0, GEMM_DGRAD = 1, GEMM_WGRAD = 2 };

@@ -51,6 +51,19 @@ struct HeadBwdArgs {
   const uint32_t* bits; int64_t ldbits;
 };
 
+// Sampler observations -> actor operand rows: x[r, c] = obs[r, c] for r < n, c < O;
+// zero for c in [O, ldx_used) and for rows [n, rows).
+struct ObsArgs { const float* obs; int n, rows, O, cols; void* x; int64_t ldx; };
+
+// Actions for samplers from the actor head output z [rows, ldz]: SAC mean action
+// tanh(mu) or a policy sample tanh(mu + exp(clip(l)) eps), eps from Philox purpose
+// P_ACT at counter `counter`, element index (row0 + r) * A + j; TD3 tanh(z).
+struct ActHeadArgs {
+  const float* z; int ldz; int A, n; int64_t row0;
+  int sac, stochastic; uint64_t seed; uint32_t counter; float lmin, lmax;
+  float* a;
+};
+
 // q[r] = bias + sum over p < parts in order of part[p * ld + r], r < rows.
 struct RdotFinalArgs {
   const float* part; int parts; int64_t ld; int rows; const float* bias; float* q;
@@ -101,6 +114,8 @@ hipError_t launch_td3_head(bool bf16, const Td3HeadArgs& h, hipStream_t s);
 hipError_t launch_rowdot(bool bf16, const RowdotArgs& r, hipStream_t s);
 hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s);
 hipError_t launch_rdot_final(const RdotFinalArgs& a, hipStream_t s);
+hipError_t launch_obs_operand(bool bf16, const ObsArgs& a, hipStream_t s);
+hipError_t launch_act_head(const ActHeadArgs& a, hipStream_t s);
 hipError_t launch_td_target(const TdArgs& a, hipStream_t s);
 int loss_blocks(int Bp);
 hipError_t launch_critic_loss(const CriticLossArgs& a, hipStream_t s);

@@ -277,6 +277,29 @@ __global__ void __launch_bounds__(256) k_rdot_final(RdotFinalArgs a) {
   a.q[r] = s + *a.bias;
 }
 
+// ------------------------------------------------------------------------------ sampler actions
+template <typename T>
+__global__ void __launch_bounds__(256) k_obs_operand(ObsArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)a.rows * a.cols) return;
+  const int r = (int)(i / a.cols), c = (int)(i - (int64_t)r * a.cols);
+  const float v = (r < a.n && c < a.O) ? a.obs[(int64_t)r * a.O + c] : 0.0f;
+  static_cast<T*>(a.x)[(int64_t)r * a.ldx + c] = from_f<T>(v);
+}
+
+__global__ void __launch_bounds__(256) k_act_head(ActHeadArgs h) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (int64_t)h.n * h.A) return;
+  const int r = (int)(e / h.A), j = (int)(e - (int64_t)r * h.A);
+  const float* z = h.z + (int64_t)r * h.ldz;
+  float u = z[j];
+  if (h.sac && h.stochastic) {
+    const float eps = normal_at(h.seed, (uint64_t)(h.row0 * h.A + e), h.counter, P_ACT);
+    u += expf(fminf(fmaxf(z[h.A + j], h.lmin), h.lmax)) * eps;
+  }
+  h.a[e] = tanhf(u);
+}
+
 // ------------------------------------------------------------------------------ TD target, losses
 __global__ void __launch_bounds__(256) k_td_target(TdArgs a) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
@@ -617,6 +640,16 @@ hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s) {
 hipError_t launch_rdot_final(const RdotFinalArgs& a, hipStream_t s) {
   if (a.parts < 1 || a.ld < a.rows) return hipErrorInvalidValue;
   k_rdot_final<<<blocks(a.rows, 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+hipError_t launch_obs_operand(bool bf16, const ObsArgs& a, hipStream_t s) {
+  if (a.n < 0 || a.n > a.rows || a.cols < a.O || a.ldx < a.cols) return hipErrorInvalidValue;
+  SPZ_LAUNCH_T(bf16, k_obs_operand, blocks((int64_t)a.rows * a.cols, 256), 256, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_act_head(const ActHeadArgs& a, hipStream_t s) {
+  if (a.n < 1) return hipSuccess;
+  k_act_head<<<blocks((int64_t)a.n * a.A, 256), 256, 0, s>>>(a);
   return hipGetLastError();
 }
 hipError_t launch_td_target(const TdArgs& a, hipStream_t s) {

@@ -29,7 +29,7 @@ EXPORTS = ["spz_hparams_default", "spz_create", "spz_destroy", "spz_buffer_push"
            "spz_update", "spz_synchronize", "spz_step", "spz_set_step", "spz_param_count",
            "spz_read_params", "spz_write_params", "spz_read_losses", "spz_debug_read", "spz_last_error",
            "spz_profile_enable", "spz_profile_read", "spz_set_batch", "spz_batch", "spz_autotune_batch",
-           "spz_save", "spz_load"]
+           "spz_save", "spz_load", "spz_act"]
 
 
 class SpzError(RuntimeError):
@@ -79,6 +79,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "spz_synchronize": (ctypes.c_int, [P]),
         "spz_set_batch": (ctypes.c_int, [P, ctypes.c_int32]),
         "spz_save": (ctypes.c_int, [P, ctypes.c_char_p, ctypes.c_int32]),
+        "spz_act": (ctypes.c_int, [P, fp, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, fp]),
         "spz_load": (ctypes.c_int, [P, ctypes.c_char_p]),
         "spz_batch": (ctypes.c_int32, [P]),
         "spz_autotune_batch": (ctypes.c_int, [P, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, P,
@@ -182,6 +183,16 @@ class Spz:
 
     def synchronize(self):
         self._check(self.lib.spz_synchronize(self.ctx))
+
+    def act(self, obs, stochastic: bool = False, counter: int = 0) -> np.ndarray:
+        """Actions of the current policy for sampler observations [n, obs_dim]."""
+        obs = np.ascontiguousarray(obs, dtype=np.float32)
+        n = obs.shape[0]
+        assert obs.shape == (n, self.obs_dim)
+        out = np.empty((n, self.act_dim), np.float32)
+        self._check(self.lib.spz_act(self.ctx, _fptr(obs), n, 1 if stochastic else 0, int(counter) & 0xFFFFFFFF,
+                                     _fptr(out)))
+        return out
 
     def save(self, path: str, ring: bool = True):
         """Whole learner state to a file (with the replay ring unless ring=False)."""

@@ -350,6 +350,30 @@ def test_autotune_batch_probes_geometrically():
     g.close()
 
 
+@pytest.mark.parametrize("w", [RAGGED, RAGGED_BF16, FUSED_BF16, RAGGED_TD3], ids=lambda w: w.name)
+def test_sampler_actions_parity(w):
+    """spz_act against the oracle's actor after a few updates: mean and sampled
+    actions, batches below, at and above the created batch (chunked)."""
+    log("act %s" % w.name)
+    g, o = make_pair(w, 5000)
+    g.update(2)
+    o.update(2)
+    teacher_force(o, g)
+    tol = 1e-5 if w.prec == "fp32" else 2e-2
+    for n in (1, 37, w.batch, 2 * w.batch + 5):
+        obs = synth.workload_rows(w, 100, n, 7)[0]
+        for stochastic in ((False, True) if w.algo == "sac" else (False,)):
+            got = g.act(obs, stochastic=stochastic, counter=9)
+            ref = o.act(obs.astype(np.float64), stochastic, 9)
+            err = np.abs(got - ref).max()
+            assert err <= tol, (n, stochastic, err)
+    if w.algo == "td3":
+        from paper_2312_06126_amd.spz import SpzError
+        with pytest.raises(SpzError):
+            g.act(obs, stochastic=True)
+    g.close()
+
+
 def _full_state(g, w, n_steps):
     st = {k: g.read_params(k) for k in state_keys(w.algo)}
     st["rec"] = g.read_losses(1, n_steps)

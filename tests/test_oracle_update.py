@@ -155,6 +155,26 @@ def test_sac_td_target_closed_form():
     assert np.array_equal(o.sac_target(s2, r, d, eps, alpha)[0], r)
 
 
+def test_sampler_actions_closed_form():
+    """Actor with a constant head: the mean action is tanh(mu); the stochastic
+    action is tanh(mu + exp(clip(l)) eps) with eps the purpose-4 normals of the
+    counter, row-major over (row, action); TD3 gives tanh(z)."""
+    o = tiny()
+    m0, l0 = np.array([0.2, -0.4]), np.array([-0.5, 25.0])   # second log-std beyond the clamp
+    _constant_head(o.net["actor"], np.concatenate([m0, l0]))
+    obs = np.random.default_rng(3).standard_normal((7, O))
+    np.testing.assert_allclose(o.act(obs, False, 0), np.tile(np.tanh(m0), (7, 1)), rtol=1e-15)
+    eps = philox.normals(o.seed, 123, philox.PURPOSE_ACT, 7 * A).reshape(7, A)
+    want = np.tanh(m0 + np.exp(np.minimum(l0, HP["log_std_max"])) * eps)
+    np.testing.assert_allclose(o.act(obs, True, 123), want, rtol=1e-15)
+    assert not np.array_equal(o.act(obs, True, 124), want)
+    t = tiny("td3")
+    _constant_head(t.net["actor"], np.array([0.3, -1.2]))
+    np.testing.assert_allclose(t.act(obs, False, 0), np.tile(np.tanh([0.3, -1.2]), (7, 1)), rtol=1e-15)
+    with pytest.raises(ValueError):
+        t.act(obs, True, 0)
+
+
 def test_critic_loss_closed_form():
     o = tiny()
     _constant_head(o.net["critic1"], 1.5)
