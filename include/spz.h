@@ -151,6 +151,19 @@ void spz_destroy(spz_ctx* ctx);
 int spz_buffer_push(spz_ctx* ctx, const float* obs, const float* act, const float* rew,
                     const float* done, const float* next_obs, int64_t n);
 
+/* Asynchronous form of spz_buffer_push (Section 3.3.2: experience reaches the
+ * update process without taking its time). The rows are copied into library-owned
+ * pinned staging before the call returns (the caller may reuse its arrays), moved
+ * to the device on the library's own ingestion stream, and written into the ring
+ * on the stream of the last spz_update (or an internal stream before the first):
+ * they are seen by exactly the steps enqueued after this call, and the fill level
+ * and write pointer (spz_buffer_size) advance at once. The same sequence of calls
+ * therefore gives the same results as with spz_buffer_push. Blocks only when all
+ * four staging slots (65536 rows each) still wait for their rows to be committed.
+ * Errors: SPZ_EINVAL (n < 0, or NULL with n > 0), SPZ_ENOMEM, SPZ_EHIP. */
+int spz_buffer_push_async(spz_ctx* ctx, const float* obs, const float* act, const float* rew,
+                          const float* done, const float* next_obs, int64_t n);
+
 /* Rows currently held by the ring (0 .. capacity). */
 int64_t spz_buffer_size(const spz_ctx* ctx);
 

@@ -74,6 +74,15 @@ struct spz_ctx {
   int64_t row_bytes = 0, cap = 0, ptr = 0, size = 0;
   int off_a = 0, off_s2 = 0, off_r = 0, off_d = 0;
   float* stage = nullptr;
+  // asynchronous ingestion: pinned host slots copied to device slots on their own
+  // stream, committed into the ring on the update stream
+  struct IngestSlot { float* host = nullptr; float* dev = nullptr; hipEvent_t copied = nullptr, done = nullptr; bool used = false; };
+  std::vector<IngestSlot> slots;
+  int next_slot = 0;
+  hipStream_t si = nullptr;
+  hipStream_t commit_stream = nullptr;   // stream the latest ring commits were enqueued on
+  bool commits_pending = false;          // ... and the next update must be ordered after them
+  hipEvent_t ev_commit = nullptr;
   int64_t stage_rows = 0;
   // step state
   int64_t* d_step = nullptr;
@@ -109,6 +118,7 @@ struct spz_ctx {
   hipStream_t sc = nullptr, sa = nullptr;
   hipEvent_t ev_fork = nullptr, ev_c = nullptr, ev_a = nullptr;
   hipStream_t last = nullptr;
+  bool has_last = false;   // an update was enqueued on `last` (which may be the null stream)
   std::vector<void*> scratch;   // ping-pong view of cs_h, one entry per hidden layer
   std::vector<void*> allocs;
   // kernel timing
@@ -599,7 +609,8 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
 }
 
 int ctx_sync(spz_ctx* c) {
-  if (c->last) CK(hipStreamSynchronize(c->last));
+  if (c->has_last) CK(hipStreamSynchronize(c->last));
+  if (c->si) CK(hipStreamSynchronize(c->si));
   CK(hipStreamSynchronize(c->sc));
   CK(hipStreamSynchronize(c->sa));
   return SPZ_OK;
@@ -717,6 +728,7 @@ int setup(spz_ctx* c) {
   CK(hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming));
   CK(hipEventCreateWithFlags(&c->ev_c, hipEventDisableTiming));
   CK(hipEventCreateWithFlags(&c->ev_a, hipEventDisableTiming));
+  CK(hipEventCreateWithFlags(&c->ev_commit, hipEventDisableTiming));
   // parameters: host init, targets = online, bf16 images
   std::vector<float> img;
   host_init(c, img);
@@ -736,7 +748,16 @@ void release(spz_ctx* c) {
   (void)hipSetDevice(c->hp.device);
   if (c->sc) (void)hipStreamSynchronize(c->sc);
   if (c->sa) (void)hipStreamSynchronize(c->sa);
-  if (c->last) (void)hipStreamSynchronize(c->last);
+  if (c->has_last) (void)hipStreamSynchronize(c->last);
+  if (c->si) (void)hipStreamSynchronize(c->si);
+  for (auto& sl : c->slots) {
+    if (sl.host) (void)hipHostFree(sl.host);
+    if (sl.dev) (void)hipFree(sl.dev);
+    if (sl.copied) (void)hipEventDestroy(sl.copied);
+    if (sl.done) (void)hipEventDestroy(sl.done);
+  }
+  if (c->si) (void)hipStreamDestroy(c->si);
+  if (c->ev_commit) (void)hipEventDestroy(c->ev_commit);
   for (void* p : c->allocs) (void)hipFree(p);
   if (c->stage) (void)hipFree(c->stage);
   for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
@@ -907,13 +928,101 @@ int spz_buffer_push(spz_ctx* c, const float* obs, const float* act, const float*
 
 int64_t spz_buffer_size(const spz_ctx* c) { return c ? c->size : SPZ_EINVAL; }
 
+namespace {
+constexpr int64_t INGEST_ROWS = 65536;   // rows per ingestion slot
+constexpr int INGEST_SLOTS = 4;
+
+int ingest_init(spz_ctx* c) {
+  if (c->si) return SPZ_OK;
+  const int64_t rowf = 2 * (int64_t)c->O + c->A + 2;
+  const size_t bytes = (size_t)(INGEST_ROWS * rowf * 4);
+  c->slots.resize(INGEST_SLOTS);
+  for (auto& sl : c->slots) {
+    if (hipHostMalloc((void**)&sl.host, bytes, hipHostMallocDefault) != hipSuccess)
+      return set_err(c, SPZ_ENOMEM, "spz_buffer_push_async: pinned host staging");
+    if (hipMalloc((void**)&sl.dev, bytes) != hipSuccess)
+      return set_err(c, SPZ_ENOMEM, "spz_buffer_push_async: device staging");
+    CK(hipEventCreateWithFlags(&sl.copied, hipEventDisableTiming));
+    CK(hipEventCreateWithFlags(&sl.done, hipEventDisableTiming));
+  }
+  CK(hipStreamCreateWithFlags(&c->si, hipStreamNonBlocking));
+  return SPZ_OK;
+}
+}  // namespace
+
+int spz_buffer_push_async(spz_ctx* c, const float* obs, const float* act, const float* rew, const float* done,
+                          const float* next_obs, int64_t n) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_buffer_push_async: NULL context");
+  if (n < 0) return set_err(c, SPZ_EINVAL, "spz_buffer_push_async: n < 0");
+  if (n == 0) return SPZ_OK;
+  if (!obs || !act || !rew || !done || !next_obs)
+    return set_err(c, SPZ_EINVAL, "spz_buffer_push_async: NULL array");
+  CK(hipSetDevice(c->hp.device));
+  int rc = ingest_init(c);
+  if (rc) return rc;
+  // Commits go to the stream updates are enqueued on, so they take effect between
+  // the steps enqueued before this call and those enqueued after it.
+  hipStream_t su = c->has_last ? c->last : c->sc;
+  const int64_t CH = INGEST_ROWS;
+  const int64_t skip = n > c->cap ? n - c->cap : 0;
+  for (int64_t r0 = skip; r0 < n; r0 += CH) {
+    const int64_t m = std::min(CH, n - r0);
+    auto& sl = c->slots[c->next_slot];
+    c->next_slot = (c->next_slot + 1) % INGEST_SLOTS;
+    if (sl.used) CK(hipEventSynchronize(sl.done));   // the slot's previous rows are in the ring
+    float* ho = sl.host;
+    float* ha = ho + CH * c->O;
+    float* hr = ha + CH * c->A;
+    float* hd = hr + CH;
+    float* hn = hd + CH;
+    memcpy(ho, obs + r0 * c->O, (size_t)(m * c->O * 4));
+    memcpy(ha, act + r0 * c->A, (size_t)(m * c->A * 4));
+    memcpy(hr, rew + r0, (size_t)(m * 4));
+    memcpy(hd, done + r0, (size_t)(m * 4));
+    memcpy(hn, next_obs + r0 * c->O, (size_t)(m * c->O * 4));
+    float* dob = sl.dev;
+    float* dac = dob + CH * c->O;
+    float* drw = dac + CH * c->A;
+    float* ddn = drw + CH;
+    float* dnx = ddn + CH;
+    CK(hipMemcpyAsync(dob, ho, (size_t)(m * c->O * 4), hipMemcpyHostToDevice, c->si));
+    CK(hipMemcpyAsync(dac, ha, (size_t)(m * c->A * 4), hipMemcpyHostToDevice, c->si));
+    CK(hipMemcpyAsync(drw, hr, (size_t)(m * 4), hipMemcpyHostToDevice, c->si));
+    CK(hipMemcpyAsync(ddn, hd, (size_t)(m * 4), hipMemcpyHostToDevice, c->si));
+    CK(hipMemcpyAsync(dnx, hn, (size_t)(m * c->O * 4), hipMemcpyHostToDevice, c->si));
+    CK(hipEventRecord(sl.copied, c->si));
+    CK(hipStreamWaitEvent(su, sl.copied, 0));
+    PackArgs p{c->buf, c->row_bytes, c->off_a, c->off_s2, c->off_r, c->off_d, c->O, c->A, m,
+               (c->ptr + r0) % c->cap, c->cap, dob, dac, drw, ddn, dnx};
+    CK(launch_pack(c->bf16, p, su));
+    CK(hipEventRecord(sl.done, su));
+    sl.used = true;
+  }
+  c->commit_stream = su;
+  c->commits_pending = true;
+  c->ptr = (c->ptr + n) % c->cap;
+  c->size = std::min(c->size + n, c->cap);
+  return SPZ_OK;
+}
+
 int spz_update(spz_ctx* c, int32_t n_steps, void* hip_stream) {
   if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_update: NULL context");
   if (n_steps < 0) return set_err(c, SPZ_EINVAL, "spz_update: n_steps < 0");
   if (c->size == 0) return set_err(c, SPZ_EEMPTY, "spz_update: replay buffer is empty");
   CK(hipSetDevice(c->hp.device));
   hipStream_t s0 = static_cast<hipStream_t>(hip_stream);
+  // Steps enqueued earlier on another stream, and ring commits of asynchronous
+  // pushes enqueued on another stream, come first.
+  hipStream_t before[2] = {c->has_last && c->last != s0 ? c->last : s0,
+                           c->commits_pending && c->commit_stream != s0 ? c->commit_stream : s0};
+  for (int i = 0; i < 2; ++i)
+    if (before[i] != s0 && (i == 0 || before[1] != before[0])) {
+      CK(hipEventRecord(c->ev_commit, before[i]));
+      CK(hipStreamWaitEvent(s0, c->ev_commit, 0));
+    }
+  c->commits_pending = false;
   c->last = s0;
+  c->has_last = true;
   for (int i = 0; i < n_steps; ++i) {
     const int rc = enqueue_step(c, s0);
     if (rc) return rc;

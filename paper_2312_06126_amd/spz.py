@@ -29,7 +29,7 @@ EXPORTS = ["spz_hparams_default", "spz_create", "spz_destroy", "spz_buffer_push"
            "spz_update", "spz_synchronize", "spz_step", "spz_set_step", "spz_param_count",
            "spz_read_params", "spz_write_params", "spz_read_losses", "spz_debug_read", "spz_last_error",
            "spz_profile_enable", "spz_profile_read", "spz_set_batch", "spz_batch", "spz_autotune_batch",
-           "spz_save", "spz_load", "spz_act"]
+           "spz_save", "spz_load", "spz_act", "spz_buffer_push_async"]
 
 
 class SpzError(RuntimeError):
@@ -75,6 +75,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "spz_destroy": (None, [P]),
         "spz_buffer_push": (ctypes.c_int, [P, fp, fp, fp, fp, fp, ctypes.c_int64]),
         "spz_buffer_size": (ctypes.c_int64, [P]),
+        "spz_buffer_push_async": (ctypes.c_int, [P, fp, fp, fp, fp, fp, ctypes.c_int64]),
         "spz_update": (ctypes.c_int, [P, ctypes.c_int32, P]),
         "spz_synchronize": (ctypes.c_int, [P]),
         "spz_set_batch": (ctypes.c_int, [P, ctypes.c_int32]),
@@ -174,6 +175,13 @@ class Spz:
         assert arrs[0].shape == (n, self.obs_dim) and arrs[4].shape == (n, self.obs_dim)
         assert arrs[1].shape == (n, self.act_dim) and arrs[3].shape == (n,)
         self._check(self.lib.spz_buffer_push(self.ctx, *map(_fptr, arrs), n))
+
+    def buffer_push_async(self, obs, act, rew, done, next_obs):
+        arrs = [np.ascontiguousarray(x, dtype=np.float32) for x in (obs, act, rew, done, next_obs)]
+        n = arrs[2].shape[0]
+        assert arrs[0].shape == (n, self.obs_dim) and arrs[4].shape == (n, self.obs_dim)
+        assert arrs[1].shape == (n, self.act_dim) and arrs[3].shape == (n,)
+        self._check(self.lib.spz_buffer_push_async(self.ctx, *map(_fptr, arrs), n))
 
     def buffer_size(self) -> int:
         return int(self.lib.spz_buffer_size(self.ctx))

@@ -374,6 +374,43 @@ def test_sampler_actions_parity(w):
     g.close()
 
 
+@pytest.mark.parametrize("use_stream", [False, True], ids=["null_stream", "side_stream"])
+def test_async_push_equals_sync_push_bit_exact(use_stream):
+    """The same sequence of pushes and updates gives identical results with
+    asynchronous and synchronous pushes: rows are seen by exactly the steps
+    enqueued after the push. Covers several staging slots (more rows than four
+    slots hold), a wrapping ring, and a torch side stream for the updates."""
+    import torch
+    w = RAGGED.replace(capacity=300_000)
+    rows = synth.workload_rows(w, 0, 600_000, 0)
+    part = lambda a, b: [x[a:b] for x in rows]
+    plan = [("push", 0, 3000), ("update", 2), ("push", 3000, 4500), ("update", 2), ("push", 4500, 5000),
+            ("push", 5000, 5200), ("update", 3), ("push", 5200, 600_000), ("update", 2)]
+    stream = torch.cuda.Stream() if use_stream else None
+    out = []
+    for async_ in (False, True):
+        g = make_gpu(w)
+        sizes = []
+        for op in plan:
+            if op[0] == "push":
+                (g.buffer_push_async if async_ else g.buffer_push)(*part(op[1], op[2]))
+                sizes.append(g.buffer_size())
+            else:
+                g.update(op[1], stream)
+        g.synchronize()
+        if stream is not None:
+            stream.synchronize()
+        st = {k: g.read_params(k) for k in ("actor", "critic1", "tcritic2", "log_alpha", "m_critic2")}
+        st["rec"] = g.read_losses(1, 9)
+        st["idx"] = g.debug_indices()
+        st["sizes"] = np.array(sizes)
+        out.append(st)
+        g.close()
+    assert list(out[0]["sizes"]) == [3000, 4500, 5000, 5200, 300_000]
+    for k in out[0]:
+        assert np.array_equal(out[0][k], out[1][k]), k
+
+
 def _full_state(g, w, n_steps):
     st = {k: g.read_params(k) for k in state_keys(w.algo)}
     st["rec"] = g.read_losses(1, n_steps)
