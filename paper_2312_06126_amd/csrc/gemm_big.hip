@@ -103,11 +103,59 @@ __device__ inline bf16x8 frag(const bf16_t* lds, int rb, int ks, int lane) {
 //   NOSTORE (fwd): C itself is not written.
 constexpr int SCR_PITCH = 36;   // floats per scratch row
 
+// Epilogue inputs of one tile, staged in LDS (after the scratch) so that each
+// 32x32 block reads them with LDS latency: bias [BN] fp32, output-layer weights
+// [BN] bf16 (as BN/2 words), and mask bits [BN/32 word columns][BM rows] (read by
+// the input gradient, written by the forward and stored to memory at the end).
+template <int BN>
+struct EpiLds {
+  static constexpr int BIAS = 0, RDW = BN, BITS = BN + BN / 2;
+  static constexpr int WORDS = BN + BN / 2 + (BN / 32) * BM;
+};
+
+// Global loads of the staged inputs, issued before the last slice's MFMAs so their
+// latency is hidden; one 16-byte load per thread and input at most.
+template <int MODE, int BN, int F>
+struct EpiPrefetch {
+  static constexpr bool BIAS = MODE == GEMM_FWD, RDOT = (F & EPI_RDOT) != 0, BITS = (F & EPI_BITS) != 0;
+  static constexpr int NBITS = (BN / 32) * BM / 4;   // 16-byte pieces of the bits tile
+  u32x4 bits, rdw;
+  float4 bias;
+  __device__ inline void load(const GemmArgs& g, int m0, int n0, int tid) {
+    if constexpr (BIAS) {
+      if (g.bias && tid < BN / 4) bias = *reinterpret_cast<const float4*>(g.bias + n0 + 4 * tid);
+      else bias = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    }
+    if constexpr (RDOT) {
+      if (tid < BN / 8) rdw = *reinterpret_cast<const u32x4*>(static_cast<const bf16_t*>(g.rdot_w) + n0 + 8 * tid);
+    }
+    if constexpr (BITS) {
+      if (tid < NBITS) {
+        const int wc = tid / (BM / 4), r4 = (tid % (BM / 4)) * 4;
+        bits = *reinterpret_cast<const u32x4*>(g.bits + (int64_t)(n0 / 32 + wc) * g.ldbits + m0 + r4);
+      }
+    }
+  }
+  __device__ inline void store(uint32_t* lds, int tid) const {
+    using L = EpiLds<BN>;
+    if constexpr (BIAS) {
+      if (tid < BN / 4) *reinterpret_cast<float4*>(lds + L::BIAS + 4 * tid) = bias;
+    }
+    if constexpr (RDOT) {
+      if (tid < BN / 8) *reinterpret_cast<u32x4*>(lds + L::RDW + 4 * tid) = rdw;
+    }
+    if constexpr (BITS) {
+      if (tid < NBITS) *reinterpret_cast<u32x4*>(lds + L::BITS + 4 * tid) = bits;
+    }
+  }
+};
+
 // One 32x32 accumulator block (i, j) of the wave: cs accumulates the column sums of
 // the lane's 8 columns, rd[p] the row dots of the lane's rows r and r + 16.
 template <int MODE, int BN, int F>
 __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int j, int m0, int n0, int wm, int wn,
-                                 int lane, int z, float* scr, float (&cs)[8], float (&rd)[2]) {
+                                 int lane, int z, float* scr, const uint32_t* in, float (&cs)[8], float (&rd)[2]) {
+  using L = EpiLds<BN>;
   constexpr int WCOLS = BN / WN;
   constexpr bool OUTF32 = F & EPI_F32, RELU = F & EPI_RELU, MASK = F & EPI_MASK, BITS = F & EPI_BITS;
   constexpr bool BITS_OUT = F & EPI_BITS_OUT, CSUM = F & EPI_CSUM, RDOT = F & EPI_RDOT;
@@ -116,21 +164,20 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
   const int cw = wn * WCOLS + 32 * j;   // first column of the 32-column block in the tile
   const int cb = cw + 8 * cgrp;
   float bias[8];
-  uint32_t ww[4] = {0u, 0u, 0u, 0u};   // rdot_w of the lane's 8 columns, packed bf16
 #pragma unroll
   for (int e = 0; e < 8; ++e) bias[e] = 0.0f;
   if constexpr (MODE == GEMM_FWD) {
-    if (g.bias) {
-      const float4 b0 = *reinterpret_cast<const float4*>(g.bias + n0 + cb);
-      const float4 b1 = *reinterpret_cast<const float4*>(g.bias + n0 + cb + 4);
-      bias[0] = b0.x; bias[1] = b0.y; bias[2] = b0.z; bias[3] = b0.w;
-      bias[4] = b1.x; bias[5] = b1.y; bias[6] = b1.z; bias[7] = b1.w;
-    }
+    const float4 b0 = *reinterpret_cast<const float4*>(in + L::BIAS + cb);
+    const float4 b1 = *reinterpret_cast<const float4*>(in + L::BIAS + cb + 4);
+    bias[0] = b0.x; bias[1] = b0.y; bias[2] = b0.z; bias[3] = b0.w;
+    bias[4] = b1.x; bias[5] = b1.y; bias[6] = b1.z; bias[7] = b1.w;
   }
+  uint32_t ww[4] = {0u, 0u, 0u, 0u};   // output-layer weights of the lane's 8 columns, packed bf16
   if constexpr (RDOT) {
-    const uint4 w4 = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(g.rdot_w) + n0 + cb);
-    ww[0] = w4.x; ww[1] = w4.y; ww[2] = w4.z; ww[3] = w4.w;
+    const u32x4 w4 = *reinterpret_cast<const u32x4*>(in + L::RDW + cb / 2);
+    ww[0] = w4[0]; ww[1] = w4[1]; ww[2] = w4[2]; ww[3] = w4[3];
   }
+  uint32_t* bits_lds = const_cast<uint32_t*>(in) + L::BITS + (cw >> 5) * BM;
   // The wave reads back what it wrote; LDS operations of one wave complete in order.
 #pragma unroll
   for (int q = 0; q < 16; ++q)
@@ -138,7 +185,8 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     const int r = rsub + 16 * p;
-    const int64_t row = m0 + wm * (BM / WM) + 32 * i + r;
+    const int rl = wm * (BM / WM) + 32 * i + r;   // row within the tile
+    const int64_t row = m0 + rl;
     const float4 x0 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp);
     const float4 x1 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp + 4);
     float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
@@ -163,7 +211,7 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
       }
     }
     if constexpr (BITS) {
-      const uint32_t wd = g.bits[(int64_t)((n0 + cw) >> 5) * g.ldbits + row] >> (8 * cgrp);
+      const uint32_t wd = bits_lds[rl] >> (8 * cgrp);
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = (wd >> e) & 1u ? v[e] : 0.0f;
     }
@@ -187,12 +235,8 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
         }
         if constexpr (BITS_OUT) bt |= (hl > 0.0f ? 1u : 0u) << (2 * e) | (hh > 0.0f ? 1u : 0u) << (2 * e + 1);
       }
-      if constexpr (BITS_OUT) {
-        bt <<= 8 * cgrp;
-        bt |= __shfl_xor(bt, 1);
-        bt |= __shfl_xor(bt, 2);
-        if (cgrp == 0) g.bits_out[(int64_t)((n0 + cw) >> 5) * g.ldbits + row] = bt;
-      }
+      // Each of the four lanes of a row owns one byte of the row's word.
+      if constexpr (BITS_OUT) reinterpret_cast<uint8_t*>(bits_lds + rl)[cgrp] = (uint8_t)bt;
       if constexpr (STORE)
         *reinterpret_cast<uint4*>(static_cast<bf16_t*>(g.C) + row * g.ldc + n0 + cb) = make_uint4(w[0], w[1], w[2], w[3]);
     }
@@ -200,15 +244,17 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
 }
 
 // Epilogue. Accumulator blocks leave through a per-wave LDS scratch so that each
-// lane handles 8 consecutive columns of one row: 16-byte loads of mask and bias and
-// 16-byte (bf16) or 32-byte (fp32) stores. 32x32 accumulator layout: lane holds
-// column lane%32; register q holds row 8*(q/4) + 4*(lane/32) + q%4 of the block.
-// The four lanes 4r..4r+3 hold the 32 columns of one row of a 32x32 block.
+// lane handles 8 consecutive columns of one row: 16-byte loads and stores. 32x32
+// accumulator layout: lane holds column lane%32; register q holds row
+// 8*(q/4) + 4*(lane/32) + q%4 of the block. The four lanes 4r..4r+3 hold the 32
+// columns of one row of a 32x32 block. Bias, output-layer weights and mask bits
+// come from the LDS staging area (EpiLds).
 //   CSUM (dgrad): column sums of the stored (rounded) values over the tile's 256
 //     rows go to g.colsum[mt, :]: per lane over its rows, a fixed butterfly over the
 //     16 lanes of a column group, then the WM waves of the column in order via LDS.
 //   BITS_OUT (fwd): one bit per stored value (> 0), 32 columns per word, words of
-//     one 32-column block stored row-contiguously.
+//     one 32-column block stored row-contiguously; gathered in LDS and written to
+//     memory with one 16-byte store per thread at the end.
 //   BITS (dgrad): the same bits as the mask.
 //   RDOT (fwd): per row, the dot product of the stored values of the wave's
 //     BN/WN columns with rdot_w, one partial per (column tile, wave column).
@@ -218,7 +264,8 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
 // column stay live.
 template <int MODE, int BN, int F>
 __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0,
-                                int n0, int wm, int wn, int lane, int wave, int z, int mt, float* smem_f) {
+                                int n0, int wm, int wn, int lane, int wave, int z, int mt, float* smem_f,
+                                uint32_t* in) {
   constexpr int TM_ = BM / WM / 32, TN_ = BN / WN / 32, WCOLS = BN / WN;
   float* scr = smem_f + wave * (32 * SCR_PITCH);
   float* csh = smem_f + (NT / 64) * 32 * SCR_PITCH;   // [WM][BN]
@@ -231,14 +278,19 @@ __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM /
       for (int e = 0; e < 8; ++e) cs[e] = 0.0f;
 #pragma unroll
       for (int i = 0; i < TM_; ++i)
-        epi_block<MODE, BN, F>(g, acc[i][j], i, j, m0, n0, wm, wn, lane, z, scr, cs, rd);
+        epi_block<MODE, BN, F>(g, acc[i][j], i, j, m0, n0, wm, wn, lane, z, scr, in, cs, rd);
+      // Reduce-scatter over lane bits 2, 3, 4 (each exchange halves the columns a
+      // lane keeps), then across the two lane halves: 8 exchanges instead of 32.
+      const bool b2 = lane & 4, b3 = lane & 8, b4 = lane & 16;
+      float t4[4], t2[2];
 #pragma unroll
-      for (int o = 4; o < 64; o <<= 1)
+      for (int e = 0; e < 4; ++e) t4[e] = (b2 ? cs[4 + e] : cs[e]) + __shfl_xor(b2 ? cs[e] : cs[4 + e], 4);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) cs[e] += __shfl_xor(cs[e], o);
-      if (rsub == 0)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) csh[wm * BN + wn * WCOLS + 32 * j + 8 * cgrp + e] = cs[e];
+      for (int e = 0; e < 2; ++e) t2[e] = (b3 ? t4[2 + e] : t4[e]) + __shfl_xor(b3 ? t4[e] : t4[2 + e], 8);
+      float t1 = (b4 ? t2[1] : t2[0]) + __shfl_xor(b4 ? t2[0] : t2[1], 16);
+      t1 += __shfl_xor(t1, 32);
+      if (lane < 32)
+        csh[wm * BN + wn * WCOLS + 32 * j + 8 * cgrp + 4 * b2 + 2 * b3 + (b4 ? 1 : 0)] = t1;
       __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
@@ -254,12 +306,9 @@ __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM /
       float cs[8], rd[2] = {0.0f, 0.0f};
 #pragma unroll
       for (int j = 0; j < TN_; ++j) {
-        epi_block<MODE, BN, F>(g, acc[i][j], i, j, m0, n0, wm, wn, lane, z, scr, cs, rd);
+        epi_block<MODE, BN, F>(g, acc[i][j], i, j, m0, n0, wm, wn, lane, z, scr, in, cs, rd);
         __builtin_amdgcn_sched_barrier(0);
       }
-      // Compiler-only fence: the bias and weight loads of the next block row are
-      // issued again instead of being kept live in registers from this one.
-      asm volatile("" ::: "memory");
       if constexpr ((F & EPI_RDOT) != 0) {
         const int part = (n0 + wn * WCOLS) / WCOLS;
 #pragma unroll
@@ -270,6 +319,16 @@ __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM /
           if (cgrp == 0) g.rdot_part[(int64_t)part * g.ldrd + m0 + wm * (BM / WM) + 32 * i + rsub + 16 * p] = t;
         }
       }
+    }
+  }
+  if constexpr ((F & EPI_BITS_OUT) != 0) {
+    // The tile's mask words, one 16-byte piece per thread, row-contiguous per word column.
+    __syncthreads();
+    constexpr int NB = (BN / 32) * BM / 4;
+    for (int t = threadIdx.x; t < NB; t += NT) {
+      const int wc = t / (BM / 4), r4 = (t % (BM / 4)) * 4;
+      *reinterpret_cast<u32x4*>(g.bits_out + (int64_t)(n0 / 32 + wc) * g.ldbits + m0 + r4) =
+          *reinterpret_cast<const u32x4*>(in + EpiLds<BN>::BITS + 4 * t);
     }
   }
 }
@@ -344,8 +403,10 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   // interleave pattern (a transposing fragment read is two instructions).
   constexpr int NR = (AKC ? TM : 2 * TM) + (BKC ? TN : 2 * TN);
   constexpr int NW = TA::PER + TB::PER;
+  EpiPrefetch<MODE, BN, F> pre;
   int sc = 0;   // stage of slice kt
   for (int kt = 0; kt < nk; ++kt) {
+    if (kt == nk - 1) pre.load(g, m0, n0, tid);
     const int s1 = sc == STAGES - 1 ? 0 : sc + 1;   // stage of slice kt + 1
     const int s2 = s1 == STAGES - 1 ? 0 : s1 + 1;   // stage of slice kt + 2 (= that of kt - 1)
     const bf16_t* Sc = S + sc * SE;
@@ -402,8 +463,14 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
     sc = s1;
   }
   // The barrier of the last slice came after every wave's last LDS read, so the
-  // epilogue may reuse LDS as scratch.
-  epilogue<MODE, BN, F>(g, acc, m0, n0, wm, wn, lane, wave, z, mt, reinterpret_cast<float*>(smem));
+  // epilogue may reuse LDS: scratch first, then the staged inputs.
+  float* scratch = reinterpret_cast<float*>(smem);
+  uint32_t* in = reinterpret_cast<uint32_t*>(scratch + (NT / 64) * 32 * SCR_PITCH + WM * BN);
+  if constexpr (MODE != GEMM_WGRAD) {
+    pre.store(in, tid);
+    __syncthreads();
+  }
+  epilogue<MODE, BN, F>(g, acc, m0, n0, wm, wn, lane, wave, z, mt, scratch, in);
 }
 
 template <int MODE, int BN, int F>
@@ -411,7 +478,7 @@ hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
   using TA = BigTile<MODE != GEMM_WGRAD, BM>;
   using TB = BigTile<MODE == GEMM_FWD, BN>;
   const size_t tiles = STAGES * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
-  const size_t scratch = ((NT / 64) * 32 * SCR_PITCH + WM * BN) * sizeof(float);
+  const size_t scratch = ((NT / 64) * 32 * SCR_PITCH + WM * BN + EpiLds<BN>::WORDS) * sizeof(float);
   const size_t lds = tiles > scratch ? tiles : scratch;
   static bool attr = false;
   if (!attr) {
