@@ -178,17 +178,16 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
     ww[0] = w4[0]; ww[1] = w4[1]; ww[2] = w4[2]; ww[3] = w4[3];
   }
   uint32_t* bits_lds = const_cast<uint32_t*>(in) + L::BITS + (cw >> 5) * BM;
-  // The wave reads back what it wrote; LDS operations of one wave complete in order.
-#pragma unroll
-  for (int q = 0; q < 16; ++q)
-    scr[(8 * (q >> 2) + 4 * (lane >> 5) + (q & 3)) * SCR_PITCH + (lane & 31)] = a[q];
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
+#pragma unroll
+    for (int q = 8 * p; q < 8 * p + 8; ++q)
+      scr[(8 * ((q >> 2) - 2 * p) + 4 * (lane >> 5) + (q & 3)) * SCR_PITCH + (lane & 31)] = a[q];
     const int r = rsub + 16 * p;
     const int rl = wm * (BM / WM) + 32 * i + r;   // row within the tile
     const int64_t row = m0 + rl;
-    const float4 x0 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp);
-    const float4 x1 = *reinterpret_cast<const float4*>(scr + r * SCR_PITCH + 8 * cgrp + 4);
+    const float4 x0 = *reinterpret_cast<const float4*>(scr + rsub * SCR_PITCH + 8 * cgrp);
+    const float4 x1 = *reinterpret_cast<const float4*>(scr + rsub * SCR_PITCH + 8 * cgrp + 4);
     float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
     if constexpr (MODE == GEMM_WGRAD) {
       float* dst = static_cast<float*>(g.C) + ((int64_t)z * g.M + row) * g.ldc + n0 + cb;
