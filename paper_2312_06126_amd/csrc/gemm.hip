@@ -271,10 +271,10 @@ hipError_t launch_mode(const GemmArgs& g, hipStream_t s) {
 
 int wgrad_splits(bool bf16, int M, int N, int K) {
   int tiles, target;
-  if (bf16 && M % 256 == 0 && N >= 128) {
-    // large-tile kernel (256 x 256 tiles, or 256 x 128 when N is not a multiple of
-    // 256): about one workgroup per CU
-    tiles = (M / 256) * (N % 256 == 0 ? N / 256 : N / 128);
+  if (bf16 && big_gemm_fits(GEMM_WGRAD, M, N, K, 1)) {
+    // large-tile kernel: about one workgroup per CU
+    const int bn = big_bn(N, false);
+    tiles = (M / 256) * ((N + bn - 1) / bn);
     target = 256;
   } else {
     const int bm = pick_tile(M), bn = pick_tile(N);
@@ -312,19 +312,6 @@ hipError_t gemm_generic(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t
   return hipErrorInvalidValue;
 }
 
-// The same product restricted to output columns [off, off + n).
-GemmArgs column_slice(bool bf16, GemmMode mode, const GemmArgs& g, int off, int n) {
-  GemmArgs r = g;
-  const int64_t e = bf16 ? 2 : 4;
-  const int64_t ec = (mode == GEMM_WGRAD || g.out_f32) ? 4 : e;
-  r.N = n;
-  r.B = static_cast<const uint8_t*>(g.B) + (mode == GEMM_FWD ? (int64_t)off * g.ldb : off) * e;
-  r.C = static_cast<uint8_t*>(g.C) + (int64_t)off * ec;
-  if (g.bias) r.bias = g.bias + off;
-  if (g.mask) r.mask = static_cast<const uint8_t*>(g.mask) + (int64_t)off * e;
-  return r;
-}
-
 }  // namespace
 
 bool gemm_colsum_fused(bool bf16, GemmMode mode, int M, int N, int K) {
@@ -354,13 +341,9 @@ hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   const int vec = bf16 ? 8 : 4;
   if (g.lda % vec || g.ldb % vec) return hipErrorInvalidValue;
   if (mode == GEMM_WGRAD && (g.splits < 1 || g.K % g.splits)) return hipErrorInvalidValue;
-  const int n_big = g.N / 128 * 128;
-  if (bf16 && n_big > 0 && big_gemm_fits(mode, g.M, n_big, g.K, mode == GEMM_WGRAD ? g.splits : 1) &&
-      big_epilogue_supported(mode, epilogue_flags(mode, g))) {
-    hipError_t e = gemm_big(mode, column_slice(bf16, mode, g, 0, n_big), s);
-    if (e != hipSuccess || n_big == g.N) return e;
-    return gemm_generic(bf16, mode, column_slice(bf16, mode, g, n_big, g.N - n_big), s);
-  }
+  if (bf16 && big_gemm_fits(mode, g.M, g.N, g.K, mode == GEMM_WGRAD ? g.splits : 1) &&
+      big_epilogue_supported(mode, epilogue_flags(mode, g)))
+    return gemm_big(mode, g, s);
   return gemm_generic(bf16, mode, g, s);
 }
 

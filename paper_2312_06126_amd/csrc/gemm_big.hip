@@ -53,13 +53,23 @@ struct BigTile {
   static_assert(NV % NT == 0, "tile must split evenly over the workgroup");
   u32x4 r[PER];
 
-  __device__ inline void load(const bf16_t* __restrict__ base, int64_t ld, int r0, int k0, int tid) {
+  // RG (ragged last tile of N, N % 8 == 0): rows (KC) or columns (m/n-contiguous)
+  // at or beyond lim read as zero. Separate instantiation: the predicate in the
+  // main loop costs the whole-tile products several percent.
+  template <bool RG>
+  __device__ inline void load(const bf16_t* __restrict__ base, int64_t ld, int r0, int k0, int tid, int lim) {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int v = tid + p * NT;
       const int a = v / VPR, b = (v % VPR) * 8;
       const bf16_t* src = KC ? base + (int64_t)(r0 + a) * ld + (k0 + b) : base + (int64_t)(k0 + a) * ld + (r0 + b);
-      r[p] = *reinterpret_cast<const u32x4*>(src);
+      if constexpr (RG) {
+        const bool ok = KC ? r0 + a < lim : r0 + b < lim;
+        r[p] = ok ? *reinterpret_cast<const u32x4*>(src) : u32x4{0u, 0u, 0u, 0u};
+      } else {
+        (void)lim;
+        r[p] = *reinterpret_cast<const u32x4*>(src);
+      }
     }
   }
   __device__ inline void store(bf16_t* lds, int tid) const {
@@ -123,7 +133,7 @@ struct EpiPrefetch {
   float4 bias;
   __device__ inline void load(const GemmArgs& g, int m0, int n0, int tid) {
     if constexpr (BIAS) {
-      if (g.bias && tid < BN / 4) bias = *reinterpret_cast<const float4*>(g.bias + n0 + 4 * tid);
+      if (g.bias && tid < BN / 4 && n0 + 4 * tid < g.N) bias = *reinterpret_cast<const float4*>(g.bias + n0 + 4 * tid);
       else bias = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     }
     if constexpr (RDOT) {
@@ -189,6 +199,7 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
     const float4 x0 = *reinterpret_cast<const float4*>(scr + rsub * SCR_PITCH + 8 * cgrp);
     const float4 x1 = *reinterpret_cast<const float4*>(scr + rsub * SCR_PITCH + 8 * cgrp + 4);
     float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+    if (n0 + cb >= g.N) continue;   // ragged last column tile (N % 8 == 0)
     if constexpr (MODE == GEMM_WGRAD) {
       float* dst = static_cast<float*>(g.C) + ((int64_t)z * g.M + row) * g.ldc + n0 + cb;
       *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
@@ -335,7 +346,7 @@ __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM /
 // One kernel per (product, column tile, epilogue variant): a runtime switch over the
 // variants inside one kernel let common code move above the switch and raised the
 // register pressure of every variant to the point of spilling.
-template <int MODE, int BN, int F>
+template <int MODE, int BN, int F, bool RG>
 __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int tiles_n) {
   constexpr bool AKC = MODE != GEMM_WGRAD;
   constexpr bool BKC = MODE == GEMM_FWD;
@@ -378,19 +389,19 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   TB tb;
   const int nk = (kend - kbeg) / BK;
   // Prologue: slices 0 and 1 in stages 0 and 1, slice 2 in registers.
-  ta.load(A, g.lda, m0, kbeg, tid);
-  tb.load(B, g.ldb, n0, kbeg, tid);
+  ta.template load<false>(A, g.lda, m0, kbeg, tid, g.M);
+  tb.template load<RG>(B, g.ldb, n0, kbeg, tid, g.N);
   ta.store(S, tid);
   tb.store(S + TA::ELEMS, tid);
   if (nk > 1) {
-    ta.load(A, g.lda, m0, kbeg + BK, tid);
-    tb.load(B, g.ldb, n0, kbeg + BK, tid);
+    ta.template load<false>(A, g.lda, m0, kbeg + BK, tid, g.M);
+    tb.template load<RG>(B, g.ldb, n0, kbeg + BK, tid, g.N);
     ta.store(S + SE, tid);
     tb.store(S + SE + TA::ELEMS, tid);
   }
   if (nk > 2) {
-    ta.load(A, g.lda, m0, kbeg + 2 * BK, tid);
-    tb.load(B, g.ldb, n0, kbeg + 2 * BK, tid);
+    ta.template load<false>(A, g.lda, m0, kbeg + 2 * BK, tid, g.M);
+    tb.template load<RG>(B, g.ldb, n0, kbeg + 2 * BK, tid, g.N);
   }
   __syncthreads();
   bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
@@ -414,8 +425,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
       tb.store(S + s2 * SE + TA::ELEMS, tid);
     }
     if (kt + 3 < nk) {
-      ta.load(A, g.lda, m0, kbeg + (kt + 3) * BK, tid);
-      tb.load(B, g.ldb, n0, kbeg + (kt + 3) * BK, tid);
+      ta.template load<false>(A, g.lda, m0, kbeg + (kt + 3) * BK, tid, g.M);
+      tb.template load<RG>(B, g.ldb, n0, kbeg + (kt + 3) * BK, tid, g.N);
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i) fa1[i] = frag<AKC, TA::PITCH>(Sc, (wm * TM + i) * 32, 16, lane);
@@ -472,7 +483,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   epilogue<MODE, BN, F>(g, acc, m0, n0, wm, wn, lane, wave, z, mt, scratch, in);
 }
 
-template <int MODE, int BN, int F>
+template <int MODE, int BN, int F, bool RG>
 hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
   using TA = BigTile<MODE != GEMM_WGRAD, BM>;
   using TB = BigTile<MODE == GEMM_FWD, BN>;
@@ -481,46 +492,50 @@ hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
   const size_t lds = tiles > scratch ? tiles : scratch;
   static bool attr = false;
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_gemm_big<MODE, BN, F>,
+    hipError_t e = hipFuncSetAttribute((const void*)k_gemm_big<MODE, BN, F, RG>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const int tiles_m = g.M / BM, tiles_n = g.N / BN;
+  const int tiles_m = g.M / BM, tiles_n = (g.N + BN - 1) / BN;
   const int splits = MODE == GEMM_WGRAD ? g.splits : 1;
-  k_gemm_big<MODE, BN, F><<<tiles_m * tiles_n * splits, NT, lds, s>>>(g, tiles_m, tiles_n);
+  k_gemm_big<MODE, BN, F, RG><<<tiles_m * tiles_n * splits, NT, lds, s>>>(g, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
 template <int MODE, int BN>
 hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
+  const bool rg = g.N % BN != 0;
 #define SPZ_CASE(F) \
-  case (F): return launch_big_f<MODE, BN, (F)>(g, s)
+  case (F): return rg ? launch_big_f<MODE, BN, (F), true>(g, s) : launch_big_f<MODE, BN, (F), false>(g, s)
+#define SPZ_CASE_WHOLE(F) \
+  case (F): return rg ? hipErrorInvalidValue : launch_big_f<MODE, BN, (F), false>(g, s)
   if constexpr (MODE == GEMM_WGRAD) {
-    return launch_big_f<MODE, BN, EPI_F32>(g, s);
+    return rg ? launch_big_f<MODE, BN, EPI_F32, true>(g, s) : launch_big_f<MODE, BN, EPI_F32, false>(g, s);
   } else if constexpr (MODE == GEMM_FWD) {
     switch (epilogue_flags((GemmMode)MODE, g)) {
       SPZ_CASE(EPI_F32);
       SPZ_CASE(0);
       SPZ_CASE(EPI_RELU);
-      SPZ_CASE(EPI_RELU | EPI_BITS_OUT);
-      SPZ_CASE(EPI_RELU | EPI_RDOT);
-      SPZ_CASE(EPI_RELU | EPI_RDOT | EPI_NOSTORE);
-      SPZ_CASE(EPI_RELU | EPI_BITS_OUT | EPI_RDOT);
-      SPZ_CASE(EPI_RELU | EPI_BITS_OUT | EPI_RDOT | EPI_NOSTORE);
+      SPZ_CASE_WHOLE(EPI_RELU | EPI_BITS_OUT);
+      SPZ_CASE_WHOLE(EPI_RELU | EPI_RDOT);
+      SPZ_CASE_WHOLE(EPI_RELU | EPI_RDOT | EPI_NOSTORE);
+      SPZ_CASE_WHOLE(EPI_RELU | EPI_BITS_OUT | EPI_RDOT);
+      SPZ_CASE_WHOLE(EPI_RELU | EPI_BITS_OUT | EPI_RDOT | EPI_NOSTORE);
     }
   } else {
     switch (epilogue_flags((GemmMode)MODE, g)) {
       SPZ_CASE(EPI_F32);
       SPZ_CASE(0);
       SPZ_CASE(EPI_MASK);
-      SPZ_CASE(EPI_MASK | EPI_CSUM);
-      SPZ_CASE(EPI_CSUM);
-      SPZ_CASE(EPI_BITS);
-      SPZ_CASE(EPI_BITS | EPI_CSUM);
+      SPZ_CASE_WHOLE(EPI_MASK | EPI_CSUM);
+      SPZ_CASE_WHOLE(EPI_CSUM);
+      SPZ_CASE_WHOLE(EPI_BITS);
+      SPZ_CASE_WHOLE(EPI_BITS | EPI_CSUM);
     }
   }
 #undef SPZ_CASE
+#undef SPZ_CASE_WHOLE
   return hipErrorInvalidValue;
 }
 
@@ -554,15 +569,25 @@ bool big_gemm_colsum(GemmMode mode, int M, int N, int K) {
   return mode == GEMM_DGRAD && big_gemm_fits(mode, M, N, K, 1);
 }
 
+int big_bn(int N, bool fused) {
+  if (N % 256 == 0) return 256;
+  if (fused) return 128;          // fused epilogues need whole column tiles (N % 128 == 0)
+  return N > 256 ? 256 : 128;     // ragged last column tile
+}
+
 bool big_gemm_fits(GemmMode mode, int M, int N, int K, int splits) {
   (void)mode;
-  if (M % BM || N % 128) return false;
+  // Below 128 columns the generic kernel's small tiles waste less work.
+  if (M % BM || N % 8 || N < 128) return false;
   const int kk = mode == GEMM_WGRAD ? K / splits : K;
   return kk % BK == 0 && kk > 0;
 }
 
 hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s) {
-  const bool bn256 = g.N % 256 == 0;
+  const int f = epilogue_flags(mode, g);
+  const bool fused = f & (EPI_BITS | EPI_BITS_OUT | EPI_RDOT | EPI_CSUM | EPI_NOSTORE);
+  if (fused && g.N % 128) return hipErrorInvalidValue;
+  const bool bn256 = big_bn(g.N, fused) == 256;
   switch (mode) {
     case GEMM_FWD: return bn256 ? launch_big<GEMM_FWD, 256>(g, s) : launch_big<GEMM_FWD, 128>(g, s);
     case GEMM_DGRAD: return bn256 ? launch_big<GEMM_DGRAD, 256>(g, s) : launch_big<GEMM_DGRAD, 128>(g, s);

@@ -141,8 +141,12 @@ hipError_t splitk_reduce(const float* part, int splits, int M, int N, int64_t ld
                          int64_t ldo, hipStream_t s);
 // Choose a split count for a WGRAD of (M, N, K) and return it (K % (32*splits) == 0).
 int wgrad_splits(bool bf16, int M, int N, int K);
-// Large-tile bf16 kernel (gemm_big.hip): M % 256 == 0, N % 128 == 0, K slices of 32.
+// Large-tile bf16 kernel (gemm_big.hip): M % 256 == 0, N >= 128 with N % 8 == 0 (a
+// ragged last column tile reads zeros and stores nothing past N), K slices of 32.
 bool big_gemm_fits(GemmMode mode, int M, int N, int K, int splits);
+// Its column tile: 256 when N % 256 == 0; with fused epilogue features 128 (they
+// need N % 128 == 0); otherwise 256 above N = 256 and 128 below.
+int big_bn(int N, bool fused);
 // True when gemm() with these arguments can produce the fused column sums (GemmArgs::colsum).
 bool gemm_colsum_fused(bool bf16, GemmMode mode, int M, int N, int K);
 bool big_gemm_colsum(GemmMode mode, int M, int N, int K);

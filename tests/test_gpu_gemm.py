@@ -5,8 +5,8 @@ bf16) operands. Products of two bf16 values are exact in float32, so the kernel
 differs from the reference only by float32 accumulation order: float32 outputs
 agree to rel 1e-5 (norm) and bf16 outputs to one bf16 ulp per element.
 Shapes cover the large-tile kernel (256-row tiles, 256/128-wide column tiles,
-k-contiguous and transposing LDS reads), its ragged column remainder handled by
-the generic kernel, the generic kernel alone, and split-K weight gradients.
+k-contiguous and transposing LDS reads, ragged last column tiles for any
+N % 8 == 0), the generic kernel alone, and split-K weight gradients.
 """
 import ctypes
 
@@ -83,21 +83,24 @@ def run(env, bf16, mode, M, N, K, splits=1, relu=0, out_f32=0, use_bias=False, u
     return got
 
 
-@pytest.mark.parametrize("M,N,K", [(512, 512, 96), (256, 1024, 1024), (512, 384, 64), (512, 416, 416)])
+@pytest.mark.parametrize("M,N,K", [(512, 512, 96), (256, 1024, 1024), (512, 384, 64), (512, 416, 416),
+                                   (512, 64, 1024), (256, 200, 96), (512, 136, 64)])
 @pytest.mark.parametrize("variant", ["relu_bf16", "plain_f32", "bias_bf16"])
 def test_forward_bf16(env, M, N, K, variant):
     run(env, True, 0, M, N, K, relu=variant == "relu_bf16", out_f32=variant == "plain_f32",
         use_bias=variant != "plain_f32")
 
 
-@pytest.mark.parametrize("M,N,K", [(512, 512, 64), (256, 1024, 1024), (512, 416, 96), (256, 32, 1024)])
+@pytest.mark.parametrize("M,N,K", [(512, 512, 64), (256, 1024, 1024), (512, 416, 96), (256, 32, 1024),
+                                   (512, 280, 64)])
 @pytest.mark.parametrize("masked", [True, False])
 def test_dgrad_bf16(env, M, N, K, masked):
     run(env, True, 1, M, N, K, use_mask=masked, out_f32=not masked)
 
 
 @pytest.mark.parametrize("M,N,K,splits", [(256, 256, 512, 1), (512, 1024, 2048, 4), (1024, 416, 1024, 2),
-                                          (1024, 384, 512, 2), (64, 1024, 1024, 4), (256, 128, 256, 1)])
+                                          (1024, 384, 512, 2), (64, 1024, 1024, 4), (256, 128, 256, 1),
+                                          (256, 160, 512, 2), (512, 264, 256, 1)])
 def test_wgrad_bf16(env, M, N, K, splits):
     run(env, True, 2, M, N, K, splits=splits)
 
