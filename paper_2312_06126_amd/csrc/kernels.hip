@@ -495,28 +495,36 @@ __global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ 
 // range and log(alpha); then Polyak tbar <- (1 - tau) tbar + tau theta on the
 // target ranges; refreshes the bfloat16 shadows of what it wrote.
 __global__ void __launch_bounds__(256) k_adam_polyak(AdamArgs a) {
+  // Bias corrections 1 - beta^t of the step (actor: delayed-step count for TD3),
+  // computed once per block in double precision.
+  __shared__ float bc[4];   // beta1 / beta2 corrections at t, then at the actor's t
+  const int64_t t = *a.step + a.step_add;
+  const int64_t ta = a.td3 ? t / a.delay : t;
+  if (threadIdx.x < 4) {
+    const double beta = (threadIdx.x & 1) ? (double)a.b2 : (double)a.b1;
+    bc[threadIdx.x] = (float)(1.0 - pow(beta, (double)(threadIdx.x < 2 ? t : ta)));
+  }
+  __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n) return;
-  const int64_t t = *a.step + a.step_add;
   const bool in_actor = i >= a.a0 && i < a.a1;
   const bool in_critic = i >= a.c0 && i < a.c1 && a.do_critic;
   const bool is_alpha = i == a.la;
   float lr;
-  int64_t tt;
+  int sel;
   if (in_actor && a.do_actor) {
     lr = a.lr_a;
-    tt = a.td3 ? t / a.delay : t;
+    sel = 2;
   } else if (in_critic) {
     lr = a.lr_c;
-    tt = t;
+    sel = 0;
   } else if (is_alpha && a.do_alpha) {
     lr = a.lr_al;
-    tt = t;
+    sel = 0;
   } else {
     return;
   }
-  const float bc1 = (float)(1.0 - pow((double)a.b1, (double)tt));
-  const float bc2 = (float)(1.0 - pow((double)a.b2, (double)tt));
+  const float bc1 = bc[sel], bc2 = bc[sel + 1];
   const float g = a.G[i];
   const float m = a.b1 * a.M[i] + (1.0f - a.b1) * g;
   const float v = a.b2 * a.V[i] + (1.0f - a.b2) * g * g;
