@@ -8,14 +8,19 @@
 //     (128 or 64 float32 accumulators per lane). Two waves per SIMD let one
 //     wave's LDS reads and global loads overlap the other's matrix work, which
 //     measured faster than one wave per SIMD with 128 x 128 wave tiles.
-//   * Both operands are copied global -> registers -> LDS in their memory layout
-//     (16-byte vector loads and stores, no shuffles). A k-contiguous tile is read
-//     back as one 16-byte LDS read per fragment; an m/n-contiguous (k-major) tile
-//     is read with two ds_read_b64_tr_b16 transposing reads per fragment: within
-//     each 16-lane group, lane i addresses 4 consecutive values of row k0 + i/4
-//     at column m0 + 4(i%4), and lane j receives column m0 + j for the 4 rows.
-//   * Three LDS stages of one 32-deep k slice each, one barrier per slice. In
-//     slice k: the registers holding slice k+2 go to the stage freed by slice k-1,
+//   * Forward product (both operands k-contiguous): 64-deep chunks go straight
+//     from global memory into LDS (global_load_lds, 128-byte row segments, chunk-
+//     swizzled rows) in two stages, one barrier per chunk; see fwd_main_loop.
+//   * Input- and weight-gradient products: both operands are copied global ->
+//     registers -> LDS in their memory layout (16-byte vector loads and stores, no
+//     shuffles). A k-contiguous tile is read back as one 16-byte LDS read per
+//     fragment; an m/n-contiguous (k-major) tile is read with two
+//     ds_read_b64_tr_b16 transposing reads per fragment: within each 16-lane
+//     group, lane i addresses 4 consecutive values of row k0 + i/4 at column
+//     m0 + 4(i%4), and lane j receives column m0 + j for the 4 rows.
+//   * Gradient products: three LDS stages of one 32-deep k slice each, one
+//     barrier per slice. In slice k: the registers holding slice k+2 go to the
+//     stage freed by slice k-1,
 //     the global loads of slice k+3 are issued, the first 16-deep half of slice k
 //     is multiplied while the fragments of its second half are read, the barrier
 //     publishes slice k+1, and the second half is multiplied while the fragments
@@ -38,6 +43,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 #define LDS_AS __attribute__((address_space(3)))
 
 constexpr int BM = 256, BK = 32, NT = 512, WM = 4, WN = 2, STAGES = 3;
+#define GLB_AS __attribute__((address_space(1)))
 
 template <bool KC, int ROWS>
 struct BigTile {
@@ -95,6 +101,61 @@ __device__ inline bf16x8 frag(const bf16_t* lds, int rb, int ks, int lane) {
     const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(p + 4 * PITCH));
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   }
+}
+
+// Forward-product operands (both k-contiguous) are loaded 64 deep at a time straight
+// into LDS (global_load_lds, 16 bytes per lane), so that every row contributes one
+// 128-byte segment per load: half the L2 requests of 64-byte segments, which measured
+// clearly faster, and no register staging or LDS store instructions.
+constexpr int CK = 64;   // k depth of one forward chunk
+
+// Chunk swizzle of the 128-byte LDS rows of a forward chunk (eight 16-byte chunks):
+// chunk c of row r sits at position c ^ csw(r), so the 16 rows read by one 16-lane
+// phase of a fragment read fall on 16 distinct 16-byte bank groups.
+__host__ __device__ constexpr int csw(int r) { return (r >> 1) & 7; }
+
+// ROWS x 64 operand chunk: one wave instruction fills 1 KB of LDS (lane l at byte
+// 16 l) = 8 rows. Element offsets beyond the last k are clamped to a valid address
+// (those values are never read back); RG rows at or beyond lim (ragged last tile of
+// N) are loaded from row lim - 1 (their products land only in columns not stored).
+template <int ROWS>
+struct FwdChunk {
+  static constexpr int BYTES = ROWS * CK * 2;
+  static constexpr int PER = BYTES / 1024 / (NT / 64);   // instructions per wave
+  static_assert(PER * 1024 * (NT / 64) == BYTES, "chunk must split evenly over the waves");
+  template <bool RG>
+  __device__ static inline void issue(const bf16_t* __restrict__ base, int64_t ld, int r0, int k0, int kmax,
+                                      uint8_t* lds, int wave, int lane, int lim) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int idx = wave + p * (NT / 64);
+      const int rr = idx * 8 + (lane >> 3);
+      const int k = k0 + 8 * ((lane & 7) ^ csw(rr));
+      int row = r0 + rr;
+      if constexpr (RG) row = row < lim ? row : lim - 1;
+      const bf16_t* src = base + (int64_t)row * ld + (k < kmax ? k : kmax);
+      __builtin_amdgcn_global_load_lds((GLB_AS void*)src, (LDS_AS void*)(lds + idx * 1024), 16, 0, 0);
+    }
+  }
+};
+
+// Fragment (32 rows x 16 k, lane layout of frag<true, ...>) at k offset ks of a chunk.
+__device__ inline bf16x8 cfrag(const uint8_t* lds, int rb, int ks, int lane) {
+  const int row = rb + (lane & 31);
+  const int c = (ks >> 3) + (lane >> 5);
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(lds + row * 128 + (c ^ csw(row)) * 16));
+}
+
+// Workgroup barrier after this wave's loads into LDS have landed but for the N most
+// recent ones (loads complete in issue order) and its LDS reads are done. A plain
+// __syncthreads would also wait for the loads still meant to be in flight.
+template <int N>
+__device__ inline void sync_loads() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | ((N >> 4) << 14));   // vmcnt N, expcnt 7, lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // Epilogue. Accumulator blocks leave through a per-wave LDS scratch so that each
@@ -343,6 +404,90 @@ __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM /
   }
 }
 
+// Main loop of the forward product: 64-deep chunks in two LDS stages, one barrier per
+// chunk. Chunk c is multiplied in four 16-deep steps, each step's MFMAs overlapping
+// the fragment reads of the next step; the barrier sits between steps 2 and 3: it
+// publishes chunk c + 1 (whose loads, issued right after the previous barrier, have
+// had four steps to land) and retires every wave's reads of chunk c, whose stage then
+// receives the loads of chunk c + 2 while step 3 runs. An odd number of 32-deep slices
+// ends with a half chunk of two steps.
+template <int BN, bool RG>
+__device__ inline void fwd_main_loop(const GemmArgs& g, f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0, int n0,
+                                     int wm, int wn, int wave, int lane, uint8_t* smem) {
+  constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
+  using CA = FwdChunk<BM>;
+  using CB = FwdChunk<BN>;
+  constexpr int SB = CA::BYTES + CB::BYTES;   // bytes per stage: A chunk then B chunk
+  constexpr int LPC = CA::PER + CB::PER;      // load instructions per wave and chunk
+  constexpr int NR = TM + TN;                 // fragment reads per step
+  const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.A);
+  const bf16_t* __restrict__ B = static_cast<const bf16_t*>(g.B);
+  const int nk = g.K / BK;                    // 32-deep slices
+  const int nfull = nk >> 1;
+  const int kmax = g.K - 8;
+  auto stage = [&](int c) { return smem + (c & 1) * SB; };
+  auto issue = [&](int c) {
+    CA::template issue<false>(A, g.lda, m0, c * CK, kmax, stage(c), wave, lane, g.M);
+    CB::template issue<RG>(B, g.ldb, n0, c * CK, kmax, stage(c) + CA::BYTES, wave, lane, g.N);
+  };
+  bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+  auto read_step = [&](const uint8_t* st, int ks, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN]) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[i] = cfrag(st, (wm * TM + i) * 32, ks, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[j] = cfrag(st + CA::BYTES, (wn * TN + j) * 32, ks, lane);
+  };
+  auto mma = [&](const bf16x8 (&fa)[TM], const bf16x8 (&fb)[TN]) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
+  // One LDS read per MFMA (sched_group_barrier masks: 0x008 MFMA, 0x020 global load,
+  // 0x100 LDS read).
+  auto interleave_reads = [&]() {
+#pragma unroll
+    for (int t = 0; t < NR; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+  };
+  issue(0);
+  asm volatile("" ::: "memory");
+  issue(1);
+  sync_loads<LPC>();   // chunk 0 landed
+  read_step(stage(0), 0, fa0, fb0);
+  for (int c = 0; c < nfull; ++c) {
+    const uint8_t* st = stage(c);
+    read_step(st, 16, fa1, fb1);
+    mma(fa0, fb0);
+    interleave_reads();
+    read_step(st, 32, fa0, fb0);
+    mma(fa1, fb1);
+    interleave_reads();
+    read_step(st, 48, fa1, fb1);
+    mma(fa0, fb0);
+    interleave_reads();
+    sync_loads<0>();   // chunk c + 1 landed (the only loads in flight)
+    issue(c + 2);
+    read_step(stage(c + 1), 0, fa0, fb0);
+    mma(fa1, fb1);
+#pragma unroll
+    for (int t = 0; t < LPC; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+    interleave_reads();
+  }
+  if (nk & 1) {   // half chunk nfull, published by the last barrier
+    read_step(stage(nfull), 16, fa1, fb1);
+    mma(fa0, fb0);
+    interleave_reads();
+    mma(fa1, fb1);
+  }
+}
+
 // One kernel per (product, column tile, epilogue variant): a runtime switch over the
 // variants inside one kernel let common code move above the switch and raised the
 // register pressure of every variant to the point of spilling.
@@ -385,92 +530,98 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
 
-  TA ta;
-  TB tb;
-  const int nk = (kend - kbeg) / BK;
-  // Prologue: slices 0 and 1 in stages 0 and 1, slice 2 in registers.
-  ta.template load<false>(A, g.lda, m0, kbeg, tid, g.M);
-  tb.template load<RG>(B, g.ldb, n0, kbeg, tid, g.N);
-  ta.store(S, tid);
-  tb.store(S + TA::ELEMS, tid);
-  if (nk > 1) {
-    ta.template load<false>(A, g.lda, m0, kbeg + BK, tid, g.M);
-    tb.template load<RG>(B, g.ldb, n0, kbeg + BK, tid, g.N);
-    ta.store(S + SE, tid);
-    tb.store(S + SE + TA::ELEMS, tid);
-  }
-  if (nk > 2) {
-    ta.template load<false>(A, g.lda, m0, kbeg + 2 * BK, tid, g.M);
-    tb.template load<RG>(B, g.ldb, n0, kbeg + 2 * BK, tid, g.N);
-  }
-  __syncthreads();
-  bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i) fa0[i] = frag<AKC, TA::PITCH>(S, (wm * TM + i) * 32, 0, lane);
-#pragma unroll
-  for (int j = 0; j < TN; ++j) fb0[j] = frag<BKC, TB::PITCH>(S + TA::ELEMS, (wn * TN + j) * 32, 0, lane);
-  // LDS read / write and global load instruction counts of one slice, for the
-  // interleave pattern (a transposing fragment read is two instructions).
-  constexpr int NR = (AKC ? TM : 2 * TM) + (BKC ? TN : 2 * TN);
-  constexpr int NW = TA::PER + TB::PER;
   EpiPrefetch<MODE, BN, F> pre;
-  int sc = 0;   // stage of slice kt
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt == nk - 1) pre.load(g, m0, n0, tid);
-    const int s1 = sc == STAGES - 1 ? 0 : sc + 1;   // stage of slice kt + 1
-    const int s2 = s1 == STAGES - 1 ? 0 : s1 + 1;   // stage of slice kt + 2 (= that of kt - 1)
-    const bf16_t* Sc = S + sc * SE;
-    if (kt + 2 < nk) {
-      ta.store(S + s2 * SE, tid);
-      tb.store(S + s2 * SE + TA::ELEMS, tid);
+  if constexpr (MODE == GEMM_FWD) {
+    fwd_main_loop<BN, RG>(g, acc, m0, n0, wm, wn, wave, lane, smem);
+    pre.load(g, m0, n0, tid);
+    sync_loads<0>();   // the trailing (unused) chunk loads must land before LDS is reused
+  } else {
+    TA ta;
+    TB tb;
+    const int nk = (kend - kbeg) / BK;
+    // Prologue: slices 0 and 1 in stages 0 and 1, slice 2 in registers.
+    ta.template load<false>(A, g.lda, m0, kbeg, tid, g.M);
+    tb.template load<RG>(B, g.ldb, n0, kbeg, tid, g.N);
+    ta.store(S, tid);
+    tb.store(S + TA::ELEMS, tid);
+    if (nk > 1) {
+      ta.template load<false>(A, g.lda, m0, kbeg + BK, tid, g.M);
+      tb.template load<RG>(B, g.ldb, n0, kbeg + BK, tid, g.N);
+      ta.store(S + SE, tid);
+      tb.store(S + SE + TA::ELEMS, tid);
     }
-    if (kt + 3 < nk) {
-      ta.template load<false>(A, g.lda, m0, kbeg + (kt + 3) * BK, tid, g.M);
-      tb.template load<RG>(B, g.ldb, n0, kbeg + (kt + 3) * BK, tid, g.N);
+    if (nk > 2) {
+      ta.template load<false>(A, g.lda, m0, kbeg + 2 * BK, tid, g.M);
+      tb.template load<RG>(B, g.ldb, n0, kbeg + 2 * BK, tid, g.N);
     }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) fa1[i] = frag<AKC, TA::PITCH>(Sc, (wm * TM + i) * 32, 16, lane);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) fb1[j] = frag<BKC, TB::PITCH>(Sc + TA::ELEMS, (wn * TN + j) * 32, 16, lane);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa0[i], fb0[j], acc[i][j], 0, 0, 0);
-    // sched_group_barrier masks: 0x008 MFMA, 0x020 global load, 0x100 LDS read, 0x200 LDS write.
-#pragma unroll
-    for (int t = 0; t < NW; ++t) {
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-#pragma unroll
-    for (int t = 0; t < NW; ++t) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-#pragma unroll
-    for (int t = 0; t < NR; ++t) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-    // Publishes slice kt + 1 (stored one slice earlier) and retires every wave's
-    // reads of slice kt - 1, whose stage the next slice overwrites.
     __syncthreads();
-    if (kt + 1 < nk) {
-      const bf16_t* Sn = S + s1 * SE;
-#pragma unroll
-      for (int i = 0; i < TM; ++i) fa0[i] = frag<AKC, TA::PITCH>(Sn, (wm * TM + i) * 32, 0, lane);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) fb0[j] = frag<BKC, TB::PITCH>(Sn + TA::ELEMS, (wn * TN + j) * 32, 0, lane);
+    bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+  #pragma unroll
+    for (int i = 0; i < TM; ++i) fa0[i] = frag<AKC, TA::PITCH>(S, (wm * TM + i) * 32, 0, lane);
+  #pragma unroll
+    for (int j = 0; j < TN; ++j) fb0[j] = frag<BKC, TB::PITCH>(S + TA::ELEMS, (wn * TN + j) * 32, 0, lane);
+    // LDS read / write and global load instruction counts of one slice, for the
+    // interleave pattern (a transposing fragment read is two instructions).
+    constexpr int NR = (AKC ? TM : 2 * TM) + (BKC ? TN : 2 * TN);
+    constexpr int NW = TA::PER + TB::PER;
+    int sc = 0;   // stage of slice kt
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt == nk - 1) pre.load(g, m0, n0, tid);
+      const int s1 = sc == STAGES - 1 ? 0 : sc + 1;   // stage of slice kt + 1
+      const int s2 = s1 == STAGES - 1 ? 0 : s1 + 1;   // stage of slice kt + 2 (= that of kt - 1)
+      const bf16_t* Sc = S + sc * SE;
+      if (kt + 2 < nk) {
+        ta.store(S + s2 * SE, tid);
+        tb.store(S + s2 * SE + TA::ELEMS, tid);
+      }
+      if (kt + 3 < nk) {
+        ta.template load<false>(A, g.lda, m0, kbeg + (kt + 3) * BK, tid, g.M);
+        tb.template load<RG>(B, g.ldb, n0, kbeg + (kt + 3) * BK, tid, g.N);
+      }
+  #pragma unroll
+      for (int i = 0; i < TM; ++i) fa1[i] = frag<AKC, TA::PITCH>(Sc, (wm * TM + i) * 32, 16, lane);
+  #pragma unroll
+      for (int j = 0; j < TN; ++j) fb1[j] = frag<BKC, TB::PITCH>(Sc + TA::ELEMS, (wn * TN + j) * 32, 16, lane);
+  #pragma unroll
+      for (int i = 0; i < TM; ++i)
+  #pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa0[i], fb0[j], acc[i][j], 0, 0, 0);
+      // sched_group_barrier masks: 0x008 MFMA, 0x020 global load, 0x100 LDS read, 0x200 LDS write.
+  #pragma unroll
+      for (int t = 0; t < NW; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+  #pragma unroll
+      for (int t = 0; t < NW; ++t) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+  #pragma unroll
+      for (int t = 0; t < NR; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+      // Publishes slice kt + 1 (stored one slice earlier) and retires every wave's
+      // reads of slice kt - 1, whose stage the next slice overwrites.
+      __syncthreads();
+      if (kt + 1 < nk) {
+        const bf16_t* Sn = S + s1 * SE;
+  #pragma unroll
+        for (int i = 0; i < TM; ++i) fa0[i] = frag<AKC, TA::PITCH>(Sn, (wm * TM + i) * 32, 0, lane);
+  #pragma unroll
+        for (int j = 0; j < TN; ++j) fb0[j] = frag<BKC, TB::PITCH>(Sn + TA::ELEMS, (wn * TN + j) * 32, 0, lane);
+      }
+  #pragma unroll
+      for (int i = 0; i < TM; ++i)
+  #pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa1[i], fb1[j], acc[i][j], 0, 0, 0);
+  #pragma unroll
+      for (int t = 0; t < NR; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+      sc = s1;
     }
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa1[i], fb1[j], acc[i][j], 0, 0, 0);
-#pragma unroll
-    for (int t = 0; t < NR; ++t) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-    sc = s1;
   }
   // The barrier of the last slice came after every wave's last LDS read, so the
   // epilogue may reuse LDS: scratch first, then the staged inputs.
@@ -487,7 +638,8 @@ template <int MODE, int BN, int F, bool RG>
 hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
   using TA = BigTile<MODE != GEMM_WGRAD, BM>;
   using TB = BigTile<MODE == GEMM_FWD, BN>;
-  const size_t tiles = STAGES * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
+  const size_t tiles = MODE == GEMM_FWD ? 2 * (FwdChunk<BM>::BYTES + FwdChunk<BN>::BYTES)
+                                        : STAGES * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
   const size_t scratch = ((NT / 64) * 32 * SCR_PITCH + WM * BN + EpiLds<BN>::WORDS) * sizeof(float);
   const size_t lds = tiles > scratch ? tiles : scratch;
   static bool attr = false;
