@@ -9,6 +9,8 @@
  *   mode 2 (wgrad):     C[M, N] = A[K, M]^T . B[K, N]   (split over K in `splits` slices,
  *                                                        reduced in slice order)
  * bf16 != 0: A, B, mask (and C unless out_f32 or mode 2) are bfloat16; else float32.
+ * bf16 mode 1: the hook also builds the transposed image of B (a temporary device
+ * buffer), which the large-tile kernel reads.
  * Leading dimensions are in elements. Shapes must satisfy the kernels' tiling
  * contract (M and N multiples of 32 with M % 128 == 0 for modes 0 and 1, K a
  * multiple of 32 * splits); otherwise SPZ_EINVAL. Synchronous.
@@ -35,7 +37,8 @@ int spzt_gemm(int32_t bf16, int32_t mode, int32_t M, int32_t N, int32_t K, int32
  *           rdot_w [N] bf16 (or null): rdot_part[p * ldrd + r] = sum over columns c of
  *             group p (spzt_rdot_cols(N) columns each) of C[r, c] * rdot_w[c];
  *           no_store: C is not written (requires rdot_w).
- *   mode 1: C = (A . B) * bit(r, c) in bf16 (bits required);
+ *   mode 1: C = (A . B) * bit(r, c) in bf16 (bits required; the hook builds the
+ *           transposed image of B that the kernel reads);
  *           colsum (or null): colsum[t * ldcs + c] = sum of stored C[r, c] over the
  *             256 rows r of row tile t.
  * Synchronous.

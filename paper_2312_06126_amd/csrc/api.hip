@@ -69,6 +69,14 @@ struct spz_ctx {
   // parameters
   float *P = nullptr, *G = nullptr, *M = nullptr, *V = nullptr, *T = nullptr;
   bf16_t *Pb = nullptr, *Tb = nullptr;
+  // bf16 contexts: transposed images of the online weights the input-gradient
+  // products read (layer l >= 1 of each net, the critics' output layers aside), at
+  // the same arena offsets as Pb: PbT + L.w holds W^T [in_p, out_p]. Refreshed
+  // whenever Pb changes.
+  bf16_t* PbT = nullptr;
+  TransposeJob* tjobs = nullptr;
+  int n_tjobs = 0, t_tiles = 0;
+  double t_elems = 0.0;
   // replay ring
   uint8_t* buf = nullptr;
   int64_t row_bytes = 0, cap = 0, ptr = 0, size = 0;
@@ -290,6 +298,15 @@ const void* elem(const spz_ctx* c, const void* base, int64_t off) {
   return static_cast<const uint8_t*>(base) + off * (int64_t)es(c);
 }
 
+// Transposed weight images (bf16 contexts) from Pb.
+hipError_t refresh_wt(spz_ctx* c, hipStream_t s) {
+  if (!c->bf16 || !c->n_tjobs) return hipSuccess;
+  return timed(c, "transpose", c->n_tjobs, 0, 0, 0.0, 4.0 * c->t_elems, s,
+               [&] { return launch_transpose_bf16(c->Pb, c->PbT, c->tjobs, c->n_tjobs, c->t_tiles, s); });
+}
+// Transposed image of the online layer L (the B operand of its input-gradient product).
+const void* wt(const spz_ctx* c, const Lay& L) { return c->bf16 ? c->PbT + L.w : nullptr; }
+
 // Forward of net ni. X: [Bp, ldx] operand tensor (the first in_p(0) columns are read).
 // hid[l] receives hidden layer l and, where bits[l] is set, its ReLU mask as bits;
 // critic heads write q [Bp], the actor head z [Bp, out_p]. Where the large-tile
@@ -369,15 +386,17 @@ hipError_t wgrad(spz_ctx* c, const void* dz, int64_t lddz, const void* X, int64_
 }
 
 // Input gradient through layer L: out[Bp, N] = (dz . W) masked by mask > 0 (or by
-// the mask bits when given). With
+// the mask bits when given). Wt (or null): the transposed image of W, which the
+// large-tile kernel reads. With
 // bias_out, also the column sums of the stored out (the bias gradient of the layer
 // below): fused into the product's epilogue where the large-tile kernel covers it.
-hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_t ldw, int N,
+hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_t ldw, const void* Wt, int N,
                  const void* mask, const uint32_t* bits, void* out, int64_t ldo, bool out_f32, float* bias_out,
                  float* cpart, hipStream_t s) {
   GemmArgs g{};
   g.A = dz; g.lda = L.out_p;
   g.B = W; g.ldb = ldw;
+  g.Bt = Wt; g.ldbt = L.out_p;
   g.C = out; g.ldc = ldo; g.out_f32 = out_f32 ? 1 : 0;
   if (bits) {
     g.bits = bits;
@@ -426,7 +445,7 @@ hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, v
     const int64_t ldx = l == 0 ? c->Kc : L.in_p;
     HK(wgrad(c, c->c_dz[cur], L.out_p, Xl, ldx, L, c->c_wpart, c->c_cpart, l == nl - 2, s));
     if (l > 0) {
-      HK(dgrad(c, c->c_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], bits[l - 1],
+      HK(dgrad(c, c->c_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, hid[l - 1], bits[l - 1],
                c->c_dz[cur ^ 1], L.in_p, false, c->G + n.L[l - 1].b, c->c_cpart, s));
       cur ^= 1;
     }
@@ -446,12 +465,12 @@ hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* 
   int cur = 0;
   for (int l = nl - 2; l >= 1; --l) {
     const Lay& L = n.L[l];
-    HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, L.in_p, hid[l - 1], bits[l - 1],
+    HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, hid[l - 1], bits[l - 1],
              c->a_dz[cur ^ 1], L.in_p, false, nullptr, nullptr, s));
     cur ^= 1;
   }
   const Lay& L0 = n.L[0];
-  return dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, c->Ap, nullptr, nullptr, da,
+  return dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, nullptr, c->Ap, nullptr, nullptr, da,
                c->Ap, true, nullptr, nullptr, s);
 }
 
@@ -466,7 +485,7 @@ hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
     const int64_t ldx = l == 0 ? c->Kc : L.in_p;
     HK(wgrad(c, cur, L.out_p, Xl, ldx, L, c->a_wpart, c->a_cpart, l == nl - 1, s));
     if (l > 0) {
-      HK(dgrad(c, cur, L, wop(c, false, L.w), L.in_p, L.in_p, c->ha[l - 1], c->bha[l - 1], c->a_dz[nxt],
+      HK(dgrad(c, cur, L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, c->ha[l - 1], c->bha[l - 1], c->a_dz[nxt],
                L.in_p, false, c->G + n.L[l - 1].b, c->a_cpart, s));
       cur = c->a_dz[nxt];
       nxt ^= 1;
@@ -562,8 +581,9 @@ hipError_t adam(spz_ctx* c, bool critics, bool actor_step, bool actor, int step_
   const double n_adam = (critics ? n_crit : 0.0) + (a.do_actor ? n_act : 0.0) + (a.do_alpha ? 1.0 : 0.0);
   const double n_pol = (a.polyak_critic ? n_crit : 0.0) + (a.polyak_actor ? n_act : 0.0);
   const double bytes = 28.0 * n_adam + 8.0 * n_pol + (c->bf16 ? 2.0 * (n_adam + n_pol) : 0.0);
-  return timed(c, "adam_polyak", (int)c->n_arena, 0, (critics ? 2 : 0) + (actor ? 1 : 0), 0.0, bytes, s,
-               [&] { return launch_adam(a, s); });
+  HK(timed(c, "adam_polyak", (int)c->n_arena, 0, (critics ? 2 : 0) + (actor ? 1 : 0), 0.0, bytes, s,
+           [&] { return launch_adam(a, s); }));
+  return refresh_wt(c, s);
 }
 
 int enqueue_step(spz_ctx* c, hipStream_t s0) {
@@ -639,6 +659,25 @@ int setup(spz_ctx* c) {
   if (c->bf16) {
     CK(dalloc_t(c, &c->Pb, (size_t)c->n_arena * 2));
     CK(dalloc_t(c, &c->Tb, (size_t)c->n_arena * 2));
+    CK(dalloc_t(c, &c->PbT, (size_t)c->n_arena * 2));
+    std::vector<TransposeJob> jobs;
+    int tiles = 0;
+    for (int ni = 0; ni < 3; ++ni) {
+      const Net& n = c->net[ni];
+      const int last = (int)n.L.size() - (ni == 0 ? 1 : 2);   // critic output layers: head kernels
+      for (int l = 1; l <= last; ++l) {
+        const Lay& L = n.L[l];
+        jobs.push_back(TransposeJob{L.w, L.w, L.in_p, L.out_p, L.out_p, L.in_p, tiles});
+        tiles += transpose_tiles(L.out_p, L.in_p);
+        c->t_elems += (double)L.out_p * L.in_p;
+      }
+    }
+    c->n_tjobs = (int)jobs.size();
+    c->t_tiles = tiles;
+    if (c->n_tjobs) {
+      CK(dalloc_t(c, &c->tjobs, jobs.size() * sizeof(TransposeJob)));
+      CK(hipMemcpy(c->tjobs, jobs.data(), jobs.size() * sizeof(TransposeJob), hipMemcpyHostToDevice));
+    }
   }
   CK(dalloc_t(c, &c->d_step, 8));
   CK(dalloc_t(c, &c->rec, (size_t)c->rec_cap * SPZ_REC_WIDTH * 4));
@@ -737,6 +776,7 @@ int setup(spz_ctx* c) {
   if (c->bf16) {
     CK(launch_to_bf16(c->P, c->Pb, c->n_arena, c->sc));
     CK(launch_to_bf16(c->T, c->Tb, c->n_arena, c->sc));
+    CK(refresh_wt(c, c->sc));
   }
   CK(hipStreamSynchronize(c->sc));
   CK(hipDeviceSynchronize());
@@ -1186,6 +1226,7 @@ int spz_load(spz_ctx* c, const char* path) {
   if (c->bf16) {
     CK(launch_to_bf16(c->P, c->Pb, c->n_arena, c->sc));
     CK(launch_to_bf16(c->T, c->Tb, c->n_arena, c->sc));
+    CK(refresh_wt(c, c->sc));
     CK(hipStreamSynchronize(c->sc));
   }
   c->seed = h.seed;
@@ -1362,6 +1403,7 @@ int spz_write_params(spz_ctx* c, int32_t which, const float* in, int64_t n_float
   if (c->bf16 && (arena == c->P || arena == c->T)) {
     bf16_t* sh = arena == c->P ? c->Pb : c->Tb;
     CK(launch_to_bf16(arena + n.off, sh + n.off, n.end - n.off, c->sc));
+    if (arena == c->P) CK(refresh_wt(c, c->sc));
     CK(hipStreamSynchronize(c->sc));
   }
   return SPZ_OK;

@@ -8,20 +8,21 @@
 //     (128 or 64 float32 accumulators per lane). Two waves per SIMD let one
 //     wave's LDS reads and global loads overlap the other's matrix work, which
 //     measured faster than one wave per SIMD with 128 x 128 wave tiles.
-//   * Forward product (both operands k-contiguous): 64-deep chunks go straight
-//     from global memory into LDS (global_load_lds, 128-byte row segments, chunk-
-//     swizzled rows) in two stages, one barrier per chunk; see fwd_main_loop.
-//   * Input- and weight-gradient products: both operands are copied global ->
-//     registers -> LDS in their memory layout (16-byte vector loads and stores, no
-//     shuffles). A k-contiguous tile is read back as one 16-byte LDS read per
-//     fragment; an m/n-contiguous (k-major) tile is read with two
-//     ds_read_b64_tr_b16 transposing reads per fragment: within each 16-lane
-//     group, lane i addresses 4 consecutive values of row k0 + i/4 at column
-//     m0 + 4(i%4), and lane j receives column m0 + j for the 4 rows.
-//   * Gradient products: three LDS stages of one 32-deep k slice each, one
-//     barrier per slice. In slice k: the registers holding slice k+2 go to the
-//     stage freed by slice k-1,
-//     the global loads of slice k+3 are issued, the first 16-deep half of slice k
+//   * Forward and input-gradient products (both operands k-contiguous; the input
+//     gradient reads the transposed weight image GemmArgs::Bt): 64-deep chunks go
+//     straight from global memory into LDS (global_load_lds, 128-byte row
+//     segments, chunk-swizzled rows) in two stages, one barrier per chunk; see
+//     chunk_main_loop.
+//   * Register-staged operands are copied global -> registers -> LDS in their
+//     memory layout (16-byte vector loads and stores, no shuffles). An
+//     m/n-contiguous (k-major) tile is read with two ds_read_b64_tr_b16
+//     transposing reads per fragment: within each 16-lane group, lane i addresses
+//     4 consecutive values of row k0 + i/4 at column m0 + 4(i%4), and lane j
+//     receives column m0 + j for the 4 rows.
+//   * Weight-gradient product (both operands register-staged): three LDS stages
+//     of one 32-deep k slice each, one barrier per slice. In slice k: the
+//     registers holding slice k+2 go to the stage freed by slice k-1, the global
+//     loads of slice k+3 are issued, the first 16-deep half of slice k
 //     is multiplied while the fragments of its second half are read, the barrier
 //     publishes slice k+1, and the second half is multiplied while the fragments
 //     of slice k+1's first half are read. The matrix cores never wait for an LDS
@@ -404,20 +405,29 @@ __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM /
   }
 }
 
-// Main loop of the forward product: 64-deep chunks in two LDS stages, one barrier per
-// chunk. Chunk c is multiplied in four 16-deep steps, each step's MFMAs overlapping
-// the fragment reads of the next step; the barrier sits between steps 2 and 3: it
-// publishes chunk c + 1 (whose loads, issued right after the previous barrier, have
-// had four steps to land) and retires every wave's reads of chunk c, whose stage then
-// receives the loads of chunk c + 2 while step 3 runs. An odd number of 32-deep slices
-// ends with a half chunk of two steps.
+// Chunked main loop of the forward and input-gradient products, C = A . B^T with A
+// [M, K] and B [N, K] both k-contiguous (the input gradient takes the transposed
+// weight image): 64-deep chunks in two LDS stages, one barrier per chunk. Chunk c
+// is multiplied in four 16-deep steps, each step's MFMAs overlapping the fragment
+// reads of the next step; the barrier sits between steps 2 and 3: it publishes
+// chunk c + 1 (whose loads, issued right after the previous barrier, have had four
+// steps to land) and retires every wave's reads of chunk c, whose stage then
+// receives chunk c + 2 while step 3 runs. An odd number of 32-deep slices ends with
+// a half chunk of two steps.
+template <int BN>
+struct ChunkLds {
+  static constexpr int ABYTES = FwdChunk<BM>::BYTES;
+  static constexpr int BYTES = ABYTES + FwdChunk<BN>::BYTES;
+};
+
 template <int BN, bool RG>
-__device__ inline void fwd_main_loop(const GemmArgs& g, f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0, int n0,
-                                     int wm, int wn, int wave, int lane, uint8_t* smem) {
+__device__ inline void chunk_main_loop(const GemmArgs& g, f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0,
+                                       int n0, int wm, int wn, int wave, int lane, uint8_t* smem) {
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
   using CA = FwdChunk<BM>;
   using CB = FwdChunk<BN>;
-  constexpr int SB = CA::BYTES + CB::BYTES;   // bytes per stage: A chunk then B chunk
+  constexpr int ABYTES = ChunkLds<BN>::ABYTES;
+  constexpr int SB = ChunkLds<BN>::BYTES;     // bytes per stage: A chunk then B chunk
   constexpr int LPC = CA::PER + CB::PER;      // load instructions per wave and chunk
   constexpr int NR = TM + TN;                 // fragment reads per step
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.A);
@@ -428,14 +438,14 @@ __device__ inline void fwd_main_loop(const GemmArgs& g, f32x16 (&acc)[BM / WM / 
   auto stage = [&](int c) { return smem + (c & 1) * SB; };
   auto issue = [&](int c) {
     CA::template issue<false>(A, g.lda, m0, c * CK, kmax, stage(c), wave, lane, g.M);
-    CB::template issue<RG>(B, g.ldb, n0, c * CK, kmax, stage(c) + CA::BYTES, wave, lane, g.N);
+    CB::template issue<RG>(B, g.ldb, n0, c * CK, kmax, stage(c) + ABYTES, wave, lane, g.N);
   };
   bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
   auto read_step = [&](const uint8_t* st, int ks, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN]) {
 #pragma unroll
     for (int i = 0; i < TM; ++i) fa[i] = cfrag(st, (wm * TM + i) * 32, ks, lane);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) fb[j] = cfrag(st + CA::BYTES, (wn * TN + j) * 32, ks, lane);
+    for (int j = 0; j < TN; ++j) fb[j] = cfrag(st + ABYTES, (wn * TN + j) * 32, ks, lane);
   };
   auto mma = [&](const bf16x8 (&fa)[TM], const bf16x8 (&fb)[TN]) {
 #pragma unroll
@@ -531,8 +541,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
 
   EpiPrefetch<MODE, BN, F> pre;
-  if constexpr (MODE == GEMM_FWD) {
-    fwd_main_loop<BN, RG>(g, acc, m0, n0, wm, wn, wave, lane, smem);
+  if constexpr (MODE != GEMM_WGRAD) {
+    chunk_main_loop<BN, RG>(g, acc, m0, n0, wm, wn, wave, lane, smem);
     pre.load(g, m0, n0, tid);
     sync_loads<0>();   // the trailing (unused) chunk loads must land before LDS is reused
   } else {
@@ -638,8 +648,8 @@ template <int MODE, int BN, int F, bool RG>
 hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
   using TA = BigTile<MODE != GEMM_WGRAD, BM>;
   using TB = BigTile<MODE == GEMM_FWD, BN>;
-  const size_t tiles = MODE == GEMM_FWD ? 2 * (FwdChunk<BM>::BYTES + FwdChunk<BN>::BYTES)
-                                        : STAGES * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
+  const size_t tiles = MODE != GEMM_WGRAD ? 2 * ChunkLds<BN>::BYTES
+                                          : STAGES * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
   const size_t scratch = ((NT / 64) * 32 * SCR_PITCH + WM * BN + EpiLds<BN>::WORDS) * sizeof(float);
   const size_t lds = tiles > scratch ? tiles : scratch;
   static bool attr = false;
@@ -742,7 +752,14 @@ hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s) {
   const bool bn256 = big_bn(g.N, fused) == 256;
   switch (mode) {
     case GEMM_FWD: return bn256 ? launch_big<GEMM_FWD, 256>(g, s) : launch_big<GEMM_FWD, 128>(g, s);
-    case GEMM_DGRAD: return bn256 ? launch_big<GEMM_DGRAD, 256>(g, s) : launch_big<GEMM_DGRAD, 128>(g, s);
+    case GEMM_DGRAD: {
+      // The input-gradient product reads the weight as Bt [N, K] (k-contiguous).
+      if (!g.Bt || g.ldbt % 8 || g.ldbt < g.K) return hipErrorInvalidValue;
+      GemmArgs t = g;
+      t.B = g.Bt;
+      t.ldb = g.ldbt;
+      return bn256 ? launch_big<GEMM_DGRAD, 256>(t, s) : launch_big<GEMM_DGRAD, 128>(t, s);
+    }
     case GEMM_WGRAD: return bn256 ? launch_big<GEMM_WGRAD, 256>(g, s) : launch_big<GEMM_WGRAD, 128>(g, s);
   }
   return hipErrorInvalidValue;

@@ -597,6 +597,31 @@ __global__ void __launch_bounds__(256) k_to_bf16(const float* __restrict__ src, 
   if (i < n) dst[i] = f2bf(src[i]);
 }
 
+// One 64 x 64 tile of one transpose job per workgroup, through an LDS tile: reads of
+// 64 consecutive columns per row and writes of 64 consecutive rows per column.
+__global__ void __launch_bounds__(256) k_transpose_bf16(const bf16_t* __restrict__ src, bf16_t* __restrict__ dst,
+                                                        const TransposeJob* __restrict__ jobs, int njobs) {
+  __shared__ bf16_t tile[64][66];
+  const int t = blockIdx.x;
+  int j = 0;
+  while (j + 1 < njobs && jobs[j + 1].tile0 <= t) ++j;
+  const TransposeJob J = jobs[j];
+  const int tc = (J.cols + 63) / 64, tl = t - J.tile0;
+  const int r0 = (tl / tc) * 64, c0 = (tl % tc) * 64;
+  const int x = threadIdx.x & 63, y = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int r = r0 + y + 4 * i, c = c0 + x;
+    if (r < J.rows && c < J.cols) tile[y + 4 * i][x] = src[J.src_off + (int64_t)r * J.lds + c];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int c = c0 + y + 4 * i, r = r0 + x;
+    if (r < J.rows && c < J.cols) dst[J.dst_off + (int64_t)c * J.ldd + r] = tile[x][y + 4 * i];
+  }
+}
+
 inline unsigned blocks(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 }  // namespace
@@ -703,6 +728,13 @@ hipError_t launch_finish(const FinishArgs& f, hipStream_t s) {
 }
 hipError_t launch_to_bf16(const float* src, bf16_t* dst, int64_t n, hipStream_t s) {
   k_to_bf16<<<blocks(n, 256), 256, 0, s>>>(src, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_bf16(const bf16_t* src, bf16_t* dst, const TransposeJob* jobs, int njobs, int tiles,
+                                 hipStream_t s) {
+  if (njobs < 1 || tiles < 1) return hipErrorInvalidValue;
+  k_transpose_bf16<<<tiles, 256, 0, s>>>(src, dst, jobs, njobs);
   return hipGetLastError();
 }
 

@@ -1,8 +1,31 @@
 // Test hooks (include/spz_testing.h): the GEMM kernels on caller-owned device memory.
 #include "../../include/spz_testing.h"
-#include "internal.h"
+#include "kernels.h"
 
 using namespace spz;
+
+namespace {
+// The transposed image Bt [N, K] of a bf16 input-gradient operand B [K, N] (ldb),
+// which the large-tile kernel reads; *bt must be freed by the caller.
+hipError_t make_bt(const void* B, int64_t ldb, int K, int N, bf16_t** bt) {
+  *bt = nullptr;
+  if (K <= 0 || N <= 0) return hipErrorInvalidValue;
+  TransposeJob job{0, 0, ldb, K, K, N, 0};
+  TransposeJob* dj = nullptr;
+  hipError_t e = hipMalloc(reinterpret_cast<void**>(bt), (size_t)K * N * 2);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&dj), sizeof(job));
+  if (e == hipSuccess) e = hipMemcpy(dj, &job, sizeof(job), hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = launch_transpose_bf16(static_cast<const bf16_t*>(B), *bt, dj, 1, transpose_tiles(K, N), nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (dj) (void)hipFree(dj);
+  if (e != hipSuccess && *bt) {
+    (void)hipFree(*bt);
+    *bt = nullptr;
+  }
+  return e;
+}
+}  // namespace
 
 extern "C" int spzt_gemm(int32_t bf16, int32_t mode, int32_t M, int32_t N, int32_t K, int32_t splits,
                          const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
@@ -13,15 +36,22 @@ extern "C" int spzt_gemm(int32_t bf16, int32_t mode, int32_t M, int32_t N, int32
   g.bias = bias; g.mask = mask; g.ldm = ldm; g.M = M; g.N = N; g.K = K;
   g.relu = relu; g.out_f32 = out_f32; g.splits = splits;
   float* part = nullptr;
+  bf16_t* bt = nullptr;
   if (mode == GEMM_WGRAD) {
     if (hipMalloc(&part, (size_t)splits * M * N * 4) != hipSuccess) return SPZ_ENOMEM;
     g.C = part;
     g.ldc = N;
   }
-  hipError_t e = gemm(bf16 != 0, (GemmMode)mode, g, nullptr);
+  hipError_t e = hipSuccess;
+  if (bf16 && mode == GEMM_DGRAD && (e = make_bt(B, ldb, K, N, &bt)) == hipSuccess) {
+    g.Bt = bt;
+    g.ldbt = K;
+  }
+  if (e == hipSuccess) e = gemm(bf16 != 0, (GemmMode)mode, g, nullptr);
   if (e == hipSuccess && mode == GEMM_WGRAD) e = splitk_reduce(part, splits, M, N, N, (float*)C, ldc, nullptr);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (part) (void)hipFree(part);
+  if (bt) (void)hipFree(bt);
   if (e == hipErrorInvalidValue) return SPZ_EINVAL;
   return e == hipSuccess ? SPZ_OK : SPZ_EHIP;
 }
@@ -46,8 +76,15 @@ extern "C" int spzt_gemm_fused(int32_t mode, int32_t M, int32_t N, int32_t K, co
   }
   g.ldbits = ldbits;
   if (!gemm_fused_ok(true, (GemmMode)mode, M, N, K)) return SPZ_EINVAL;
-  hipError_t e = gemm(true, (GemmMode)mode, g, nullptr);
+  bf16_t* bt = nullptr;
+  hipError_t e = hipSuccess;
+  if (mode == GEMM_DGRAD && (e = make_bt(B, ldb, K, N, &bt)) == hipSuccess) {
+    g.Bt = bt;
+    g.ldbt = K;
+  }
+  if (e == hipSuccess) e = gemm(true, (GemmMode)mode, g, nullptr);
   if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (bt) (void)hipFree(bt);
   if (e == hipErrorInvalidValue) return SPZ_EINVAL;
   return e == hipSuccess ? SPZ_OK : SPZ_EHIP;
 }
