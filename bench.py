@@ -13,9 +13,10 @@ master weights / Adam). The ring is filled with synthetic rows before timing and
 stays resident in HBM; nothing is transferred from the host in the timed region.
 
 Prints one JSON line (rank 0). Also reports the dominant kernel against its
-roofline (per-launch event timings taken by the library on the stream each
-kernel runs on, during the timed region) and the CPU oracle's rate on a bounded
-sample of the same workload.
+roofline (per-launch event timings taken by the library on the stream the kernel
+runs on, during the timed region, where only that kernel's launches carry events;
+the kernel is picked, and the per-kernel table taken, in an untimed survey pass
+before) and the CPU oracle's rate on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -34,6 +35,7 @@ METRIC = "actor-critic update frames/sec (batch rows/s) at 1 MI355X; MFMA util %
 PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense matrix peaks
 PEAK_HBM_GBS = 8000.0
 GEMMS = ("gemm_fwd", "gemm_dgrad", "gemm_wgrad")
+SURVEY_STEPS = 10   # untimed steps with every kernel launch timed (per-kernel table)
 # Measured HBM traffic of the dominant kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
 # scaled by a plain copy of known size), valid while the kernel sources hash the same.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_fwd_1024_sac_large_bf16_traffic.txt")
@@ -208,8 +210,20 @@ def main():
     torch.cuda.synchronize()
     progress("warmup %d steps done" % args.warmup)
 
+    survey, top = [], None
     if not args.no_profile:
-        g.profile_enable(True, reserve_launches=120 * steps)
+        # Untimed survey pass: every kernel launch of a few steps bracketed by events,
+        # for the per-kernel table and to find the dominant kernel. In the timed
+        # region only that kernel's launches carry events (events on every launch
+        # cost the step several percent).
+        g.profile_enable(True, reserve_launches=150 * SURVEY_STEPS)
+        g.update(SURVEY_STEPS, stream)
+        survey = g.profile_read()
+        top = survey[0]
+        g.profile_enable(True, reserve_launches=40 * steps)
+        g.profile_only(top["name"], top["M"], top["N"], top["K"])
+        progress("survey %d steps; timing %s M=%d N=%d K=%d in the timed region" %
+                 (SURVEY_STEPS, top["name"], top["M"], top["N"], top["K"]))
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -221,7 +235,7 @@ def main():
     elapsed_ms = t_start.elapsed_time(t_end)
     progress("timed %d steps: %.3f ms/step" % (steps, elapsed_ms / steps))
 
-    stats = g.profile_read() if not args.no_profile else []
+    stats = g.profile_read() if top else []
     rec = g.read_losses(g.step() - steps + 1, steps)
     finite = bool((rec[:, 6] == 0).all())
     g.close()
@@ -239,18 +253,20 @@ def main():
                                                          if args.streams == 2 else "one stream")),
                losses_finite=finite)
     if stats:
-        gemm_ms = sum(s["total_ms"] for s in stats if s["name"] in GEMMS)
-        gemm_flops = sum(s["flops"] * s["launches"] for s in stats if s["name"] in GEMMS)
+        gemm_ms = sum(s["total_ms"] for s in survey if s["name"] in GEMMS)
+        gemm_flops = sum(s["flops"] * s["launches"] for s in survey if s["name"] in GEMMS)
         peak = PEAK_TFLOPS[prec] * 1e12
         out["mfma_util"] = dict(
             gemm_kernels=round(gemm_flops / (gemm_ms / 1e3) / peak, 4) if gemm_ms else None,
-            whole_step=round(gemm_flops / (elapsed_ms / 1e3) / peak, 4),
-            gemm_flops_per_step=gemm_flops / steps, peak_tflops=PEAK_TFLOPS[prec],
-            note="gemm_kernels: GEMM flops / summed GEMM kernel time (events; concurrent streams overlap)")
+            whole_step=round(gemm_flops / SURVEY_STEPS / (elapsed_ms / steps / 1e3) / peak, 4),
+            gemm_flops_per_step=gemm_flops / SURVEY_STEPS, peak_tflops=PEAK_TFLOPS[prec],
+            note="gemm_kernels: GEMM flops / summed GEMM kernel time of the survey pass (events on every "
+                 "launch; concurrent streams overlap); whole_step: GEMM flops per step / timed ms per step")
         out["roofline"] = roofline(stats, prec)
         out["kernels"] = [dict(name=s["name"], M=s["M"], N=s["N"], K=s["K"], launches=s["launches"],
                                avg_ms=round(s["avg_ms"], 5), total_ms=round(s["total_ms"], 3))
-                          for s in stats[:40]]
+                          for s in survey[:40]]
+        out["kernels_note"] = "survey pass of %d untimed steps before the timed region" % SURVEY_STEPS
     if args.sweep:
         out["sweep"] = sweep(w, args, stream)
     if args.autotune:

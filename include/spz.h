@@ -266,6 +266,13 @@ int spz_debug_read(spz_ctx* ctx, int32_t what, void* out, int64_t bytes);
  * demand); disabling drops the records. Waits for the context's work first. */
 int spz_profile_enable(spz_ctx* ctx, int32_t on, int64_t reserve_launches);
 
+/* Restrict kernel timing to the launches of one kernel family and shape (as
+ * reported by spz_profile_read: name, M, N, K), e.g. so that a timed run carries
+ * the events of only the kernel it measures; name NULL times every launch again
+ * (the default). Applies to launches enqueued after the call; existing records are
+ * kept. `name` is copied. Errors: SPZ_EINVAL (NULL ctx). */
+int spz_profile_only(spz_ctx* ctx, const char* name, int32_t M, int32_t N, int32_t K);
+
 /* One aggregated kernel shape. flops / bytes are the algorithmic work of one
  * launch (2*M*N*K for matrix products; bytes the kernel must move for the
  * memory-bound kernels, 0 when not meaningful). */

@@ -134,6 +134,9 @@ struct spz_ctx {
   struct ProfEv { int key; hipEvent_t a, b; };
   bool prof = false;
   std::vector<ProfKey> pkeys;
+  bool pf_on = false;           // time only launches of this family and shape
+  std::string pf_name;
+  int pf_M = 0, pf_N = 0, pf_K = 0;
   std::vector<ProfEv> pevs;
   std::vector<hipEvent_t> pool;
   std::string err;
@@ -200,7 +203,7 @@ hipError_t prof_take(spz_ctx* c, hipEvent_t* e) {
 template <class F>
 hipError_t timed(spz_ctx* c, const char* name, int M, int N, int K, double flops, double bytes, hipStream_t s,
                  F&& f) {
-  if (!c->prof) return f();
+  if (!c->prof || (c->pf_on && (M != c->pf_M || N != c->pf_N || K != c->pf_K || c->pf_name != name))) return f();
   hipEvent_t a, b;
   HK(prof_take(c, &a));
   HK(prof_take(c, &b));
@@ -1459,6 +1462,16 @@ int spz_profile_enable(spz_ctx* c, int32_t on, int64_t reserve_launches) {
     }
     c->pevs.reserve((size_t)reserve_launches);
   }
+  return SPZ_OK;
+}
+
+int spz_profile_only(spz_ctx* c, const char* name, int32_t M, int32_t N, int32_t K) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_profile_only: NULL context");
+  c->pf_on = name != nullptr;
+  c->pf_name = name ? name : "";
+  c->pf_M = M;
+  c->pf_N = N;
+  c->pf_K = K;
   return SPZ_OK;
 }
 

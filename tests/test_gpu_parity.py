@@ -266,6 +266,35 @@ def test_stream_and_chunk_invariance_bit_exact():
             assert np.array_equal(r[k], runs[0][k]), k
 
 
+def test_profile_only_times_one_kernel_and_keeps_results():
+    """Kernel timing restricted to one family and shape records only those launches,
+    and timing (all launches or one kernel) leaves the update bit-identical."""
+    w = FUSED_BF16
+    log("profile filter")
+    runs = []
+    for mode in ("off", "all", "one"):
+        g = make_gpu(w)
+        g.buffer_push(*synth.workload_rows(w, 0, 5000, 0))
+        if mode != "off":
+            g.profile_enable(True, 100)
+        if mode == "one":
+            g.profile_only("gemm_fwd", 512, 128, 256)
+        g.update(3)
+        stats = g.profile_read() if mode != "off" else []
+        if mode == "all":
+            assert {s["name"] for s in stats} >= {"gemm_fwd", "gemm_dgrad", "gemm_wgrad", "gather", "adam_polyak"}
+            n_fwd = [s["launches"] for s in stats if (s["name"], s["M"], s["N"], s["K"]) == ("gemm_fwd", 512, 128, 256)]
+            assert n_fwd and n_fwd[0] > 0
+        if mode == "one":
+            assert [(s["name"], s["M"], s["N"], s["K"]) for s in stats] == [("gemm_fwd", 512, 128, 256)]
+            assert stats[0]["launches"] == n_fwd[0] and stats[0]["total_ms"] > 0
+        runs.append({k: g.read_params(k) for k in ("actor", "critic1", "critic2")})
+        g.close()
+    for r in runs[1:]:
+        for k in r:
+            assert np.array_equal(r[k], runs[0][k]), k
+
+
 def test_sequential_runs_on_one_stream_and_differs_from_snapshot():
     """The sequential ordering ignores the second stream (bit-identical runs) and
     moves the actor differently from the snapshot ordering."""
