@@ -435,18 +435,27 @@ hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, v
   ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, c->c_cpart, c->c_cextra};
   HK(timed(c, "colsum", c->Bp, H.in_p, 1, 0.0, (double)c->Bp * H.in_p * es(c), s,
            [&] { return launch_colsum(c->bf16, cs, c->G + H.w, c->G + H.b, s); }));
-  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp};
+  // dz of the last hidden layer comes from the head backward, which (with the mask
+  // as bits) also takes its column sums, the bias gradient; otherwise that is a
+  // separate column sum in the weight gradient. Every later dz comes from a dgrad
+  // that also produces its bias gradient.
+  const bool hb_sums = bits[nl - 2] != nullptr;
+  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp,
+                 hb_sums ? c->c_cpart : nullptr};
   HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, head_bwd_bytes(c, H.in_p, bits[nl - 2]), s,
            [&] { return launch_head_bwd(c->bf16, hb, s); }));
-  // dz of the last hidden layer comes from the head backward; its bias gradient is a
-  // separate column sum. Every later dz comes from a dgrad that also produces its
-  // bias gradient.
+  if (hb_sums) {
+    const int blocks = head_bwd_blocks(c->Bp);
+    const Lay& Ll = n.L[nl - 2];
+    HK(timed(c, "colsum_final", blocks, Ll.out_p, 0, 0.0, 4.0 * blocks * Ll.out_p, s,
+             [&] { return launch_colsum_final(c->c_cpart, blocks, Ll.out_p, c->G + Ll.b, s); }));
+  }
   int cur = 0;
   for (int l = nl - 2; l >= 0; --l) {
     const Lay& L = n.L[l];
     const void* Xl = l == 0 ? X : hid[l - 1];
     const int64_t ldx = l == 0 ? c->Kc : L.in_p;
-    HK(wgrad(c, c->c_dz[cur], L.out_p, Xl, ldx, L, c->c_wpart, c->c_cpart, l == nl - 2, s));
+    HK(wgrad(c, c->c_dz[cur], L.out_p, Xl, ldx, L, c->c_wpart, c->c_cpart, l == nl - 2 && !hb_sums, s));
     if (l > 0) {
       HK(dgrad(c, c->c_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, hid[l - 1], bits[l - 1],
                c->c_dz[cur ^ 1], L.in_p, false, c->G + n.L[l - 1].b, c->c_cpart, s));
@@ -462,7 +471,8 @@ hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* 
   const Net& n = c->net[ni];
   const int nl = (int)n.L.size();
   const Lay& H = n.L[nl - 1];
-  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->a_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp};
+  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->a_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp,
+                 nullptr};
   HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, head_bwd_bytes(c, H.in_p, bits[nl - 2]), s,
            [&] { return launch_head_bwd(c->bf16, hb, s); }));
   int cur = 0;
@@ -755,7 +765,7 @@ int setup(spz_ctx* c) {
     }
   // column-sum partials: first-pass chunks of the standalone kernel, or one row per
   // 256-row tile of a fused dgrad epilogue
-  const int chunks = std::max(colsum_chunks((int)Bp), (int)(Bp / 256));
+  const int chunks = std::max({colsum_chunks((int)Bp), (int)(Bp / 256), head_bwd_blocks((int)Bp)});
   c->wpart_cap = wmax;
   CK(dalloc_t(c, &c->c_wpart, (size_t)wmax * 4));
   CK(dalloc_t(c, &c->a_wpart, (size_t)wmax * 4));

@@ -49,6 +49,9 @@ struct HeadBwdArgs {
   // When set (bf16, K % 32 == 0), the ReLU mask comes from these bits instead of H:
   // bit k % 32 of bits[(k / 32) * ldbits + b].
   const uint32_t* bits; int64_t ldbits;
+  // With bits: when set, the column sums of the stored dH over each block of rows go
+  // to colpart[block, K] (head_bwd_blocks(rows) blocks; reduce with launch_colsum_final).
+  float* colpart;
 };
 
 // Sampler observations -> actor operand rows: x[r, c] = obs[r, c] for r < n, c < O;
@@ -122,6 +125,7 @@ hipError_t launch_critic_loss(const CriticLossArgs& a, hipStream_t s);
 hipError_t launch_actor_loss(const ActorLossArgs& a, hipStream_t s);
 hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream_t s);
 int colsum_chunks(int rows);
+int head_bwd_blocks(int rows);
 hipError_t launch_colsum(bool bf16, const ColsumArgs& a, float* out, float* out_extra, hipStream_t s);
 // out[n] = sum over c in order of part[c, n] (c < chunks), n < N.
 hipError_t launch_colsum_final(const float* part, int chunks, int N, float* out, hipStream_t s);

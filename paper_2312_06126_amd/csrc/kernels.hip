@@ -237,11 +237,15 @@ __global__ void __launch_bounds__(256) k_head_bwd(HeadBwdArgs a) {
 
 // The same with the mask read from bits. A block covers HB_ROWS rows: their words
 // (K / 32 per row, stored row-contiguously per 32-column block) are staged in LDS
-// with coalesced loads, then each thread writes 16-byte pieces of the rows in order.
+// with coalesced loads; thread t writes the 16-byte pieces of column group t % kv
+// (kv = K / 8) in rows t / kv, t / kv + rpi, ... (rpi = 256 / kv). With colpart,
+// the column sums of the stored (rounded) values over the block's rows go to
+// colpart[block, :]: per thread over its rows, then over the rpi threads of a
+// column group in order.
 constexpr int HB_ROWS = 64;
 __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
-  extern __shared__ uint32_t wsh[];   // [K / 32][HB_ROWS]
-  const int nw = a.K / 32, kv = a.K / 8;
+  extern __shared__ uint32_t wsh[];   // [K / 32][HB_ROWS], then [rpi][K] floats for the sums
+  const int nw = a.K / 32, kv = a.K / 8, rpi = 256 / kv;
   const int r0 = blockIdx.x * HB_ROWS;
   for (int t = threadIdx.x; t < nw * HB_ROWS; t += blockDim.x) {
     const int wc = t / HB_ROWS, r = t % HB_ROWS;
@@ -249,23 +253,40 @@ __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
   }
   __syncthreads();
   const bf16_t* w = static_cast<const bf16_t*>(a.w);
-  for (int t = threadIdx.x; t < HB_ROWS * kv; t += blockDim.x) {
-    const int r = t / kv, k = (t % kv) * 8;
-    const int b = r0 + r;
-    if (b >= a.rows) break;
-    const float dq = bf2f(f2bf(a.dq[b]));
-    const uint32_t wd = wsh[(k >> 5) * HB_ROWS + r] >> (k & 31);
+  const int cg = threadIdx.x % kv, rs = threadIdx.x / kv, k = cg * 8;
+  float cs[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+  if (rs < rpi) {
     const uint4 w4 = *reinterpret_cast<const uint4*>(w + k);
     const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
-    uint32_t o[4];
+    for (int r = rs; r < HB_ROWS; r += rpi) {
+      const int b = r0 + r;
+      if (b >= a.rows) break;
+      const float dq = bf2f(f2bf(a.dq[b]));
+      const uint32_t wd = wsh[(k >> 5) * HB_ROWS + r] >> (k & 31);
+      uint32_t o[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float w0 = bf2f((bf16_t)(ww[e] & 0xFFFFu)), w1 = bf2f((bf16_t)(ww[e] >> 16));
-      const float v0 = (wd >> (2 * e)) & 1u ? dq * w0 : 0.0f;
-      const float v1 = (wd >> (2 * e + 1)) & 1u ? dq * w1 : 0.0f;
-      o[e] = (uint32_t)f2bf(v0) | ((uint32_t)f2bf(v1) << 16);
+      for (int e = 0; e < 4; ++e) {
+        const float w0 = bf2f((bf16_t)(ww[e] & 0xFFFFu)), w1 = bf2f((bf16_t)(ww[e] >> 16));
+        const bf16_t h0 = f2bf((wd >> (2 * e)) & 1u ? dq * w0 : 0.0f);
+        const bf16_t h1 = f2bf((wd >> (2 * e + 1)) & 1u ? dq * w1 : 0.0f);
+        cs[2 * e] += bf2f(h0);
+        cs[2 * e + 1] += bf2f(h1);
+        o[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+      }
+      *reinterpret_cast<uint4*>(static_cast<bf16_t*>(a.dH) + (int64_t)b * a.ld + k) = make_uint4(o[0], o[1], o[2], o[3]);
     }
-    *reinterpret_cast<uint4*>(static_cast<bf16_t*>(a.dH) + (int64_t)b * a.ld + k) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+  if (!a.colpart) return;
+  float* ssh = reinterpret_cast<float*>(wsh + nw * HB_ROWS);
+  if (rs < rpi) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ssh[rs * a.K + k + e] = cs[e];
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < a.K; c += blockDim.x) {
+    float t = 0.0f;
+    for (int q = 0; q < rpi; ++q) t += ssh[q * a.K + c];
+    a.colpart[(int64_t)blockIdx.x * a.K + c] = t;
   }
 }
 
@@ -661,15 +682,17 @@ hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s) {
   const int vec = bf16 ? 8 : 4;
   if (a.K % vec || a.ld % vec) return hipErrorInvalidValue;
   if (a.bits) {
-    if (!bf16 || a.K % 32 || a.ldbits < a.rows) return hipErrorInvalidValue;
-    const size_t lds = (size_t)(a.K / 32) * HB_ROWS * 4;
+    if (!bf16 || a.K % 32 || a.K / 8 > 256 || a.ldbits < a.rows) return hipErrorInvalidValue;
+    const size_t lds = (size_t)(a.K / 32) * HB_ROWS * 4 + (a.colpart ? (size_t)(256 / (a.K / 8)) * a.K * 4 : 0);
     if (lds > 64 * 1024) return hipErrorInvalidValue;
     k_head_bwd_bits<<<blocks(a.rows, HB_ROWS), 256, lds, s>>>(a);
     return hipGetLastError();
   }
+  if (a.colpart) return hipErrorInvalidValue;
   SPZ_LAUNCH_T(bf16, k_head_bwd, blocks((int64_t)a.rows * (a.K / vec), 256), 256, s, a);
   return hipGetLastError();
 }
+int head_bwd_blocks(int rows) { return (int)blocks(rows, HB_ROWS); }
 hipError_t launch_rdot_final(const RdotFinalArgs& a, hipStream_t s) {
   if (a.parts < 1 || a.ld < a.rows) return hipErrorInvalidValue;
   k_rdot_final<<<blocks(a.rows, 256), 256, 0, s>>>(a);
