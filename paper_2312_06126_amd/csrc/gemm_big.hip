@@ -159,21 +159,27 @@ __device__ inline void sync_loads() {
   asm volatile("" ::: "memory");
 }
 
-// Epilogue. Accumulator blocks leave through a per-wave LDS scratch so that each
-// lane handles 8 consecutive columns of one row: 16-byte loads of mask and bias and
-// 16-byte (bf16) or 32-byte (fp32) stores. 32x32 accumulator layout: lane holds
+// Epilogue. Accumulator blocks leave in pairs of horizontally adjacent 32x32 blocks
+// (64 columns) through a per-wave LDS scratch, so that each lane handles 8
+// consecutive columns of one row and the 8 lanes of a row cover 128 bytes of bf16
+// output: 16-byte loads of mask and bias, 16-byte (bf16) or 32-byte (fp32) stores,
+// whole 128-byte lines per row and store. 32x32 accumulator layout: lane holds
 // column lane%32; register q holds row 8*(q/4) + 4*(lane/32) + q%4 of the block.
-// The four lanes 4r..4r+3 hold the 32 columns of one row of a 32x32 block.
 //   CSUM (dgrad): column sums of the stored (rounded) values over the tile's 256
 //     rows go to g.colsum[mt, :]: per lane over its rows, a fixed butterfly over the
-//     16 lanes of a column group, then the WM waves of the column in order via LDS.
+//     8 lanes of a column group, then the WM waves of the column in order via LDS.
 //   BITS_OUT (fwd): one bit per stored value (> 0), 32 columns per word, words of
 //     one 32-column block stored row-contiguously.
 //   BITS (dgrad): the same bits as the mask.
 //   RDOT (fwd): per row, the dot product of the stored values of the wave's
 //     BN/WN columns with rdot_w, one partial per (column tile, wave column).
 //   NOSTORE (fwd): C itself is not written.
-constexpr int SCR_PITCH = 36;   // floats per scratch row
+constexpr int SCR_ROWS = 8;     // scratch rows per wave (one pass of a block pair)
+constexpr int SCR_PITCH = 68;   // floats per scratch row
+// Floats of the per-wave scratches and the column-sum area [WM][BN]; the staged
+// epilogue inputs follow.
+template <int BN>
+constexpr int scr_floats() { return (NT / 64) * SCR_ROWS * SCR_PITCH + WM * BN; }
 
 // Epilogue inputs of one tile, staged in LDS (after the scratch) so that each
 // 32x32 block reads them with LDS latency: bias [BN] fp32, output-layer weights
@@ -222,19 +228,20 @@ struct EpiPrefetch {
   }
 };
 
-// One 32x32 accumulator block (i, j) of the wave: cs accumulates the column sums of
-// the lane's 8 columns, rd[p] the row dots of the lane's rows r and r + 16.
+// Blocks (i, 2 jp) and (i, 2 jp + 1) of the wave, in four passes of 8 rows: cs
+// accumulates the column sums of the lane's 8 columns, rd[p] the row dots of its
+// row in pass p.
 template <int MODE, int BN, int F>
-__device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int j, int m0, int n0, int wm, int wn,
-                                 int lane, int z, float* scr, const uint32_t* in, float (&cs)[8], float (&rd)[2]) {
+__device__ inline void epi_pair(const GemmArgs& g, const f32x16& a0, const f32x16& a1, int i, int jp, int m0,
+                                int n0, int wm, int wn, int lane, int z, float* scr, const uint32_t* in,
+                                float (&cs)[8], float (&rd)[4]) {
   using L = EpiLds<BN>;
   constexpr int WCOLS = BN / WN;
   constexpr bool OUTF32 = F & EPI_F32, RELU = F & EPI_RELU, MASK = F & EPI_MASK, BITS = F & EPI_BITS;
   constexpr bool BITS_OUT = F & EPI_BITS_OUT, CSUM = F & EPI_CSUM, RDOT = F & EPI_RDOT;
   constexpr bool STORE = !(F & EPI_NOSTORE);
-  const int cgrp = lane & 3, rsub = lane >> 2;
-  const int cw = wn * WCOLS + 32 * j;   // first column of the 32-column block in the tile
-  const int cb = cw + 8 * cgrp;
+  const int cgrp = lane & 7, rsub = lane >> 3;
+  const int cb = wn * WCOLS + 64 * jp + 8 * cgrp;   // lane's first column in the tile
   float bias[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) bias[e] = 0.0f;
@@ -249,14 +256,16 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
     const u32x4 w4 = *reinterpret_cast<const u32x4*>(in + L::RDW + cb / 2);
     ww[0] = w4[0]; ww[1] = w4[1]; ww[2] = w4[2]; ww[3] = w4[3];
   }
-  uint32_t* bits_lds = const_cast<uint32_t*>(in) + L::BITS + (cw >> 5) * BM;
+  // Mask words of the lane's 32-column block; its 8 columns are bits 8 (cgrp % 4) on.
+  uint32_t* bits_lds = const_cast<uint32_t*>(in) + L::BITS + (cb >> 5) * BM;
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
+  for (int p = 0; p < 4; ++p) {
 #pragma unroll
-    for (int q = 8 * p; q < 8 * p + 8; ++q)
-      scr[(8 * ((q >> 2) - 2 * p) + 4 * (lane >> 5) + (q & 3)) * SCR_PITCH + (lane & 31)] = a[q];
-    const int r = rsub + 16 * p;
-    const int rl = wm * (BM / WM) + 32 * i + r;   // row within the tile
+    for (int q = 4 * p; q < 4 * p + 4; ++q) {
+      scr[(4 * (lane >> 5) + (q & 3)) * SCR_PITCH + (lane & 31)] = a0[q];
+      scr[(4 * (lane >> 5) + (q & 3)) * SCR_PITCH + 32 + (lane & 31)] = a1[q];
+    }
+    const int rl = wm * (BM / WM) + 32 * i + 8 * p + rsub;   // row within the tile
     const int64_t row = m0 + rl;
     const float4 x0 = *reinterpret_cast<const float4*>(scr + rsub * SCR_PITCH + 8 * cgrp);
     const float4 x1 = *reinterpret_cast<const float4*>(scr + rsub * SCR_PITCH + 8 * cgrp + 4);
@@ -283,7 +292,7 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
       }
     }
     if constexpr (BITS) {
-      const uint32_t wd = bits_lds[rl] >> (8 * cgrp);
+      const uint32_t wd = bits_lds[rl] >> (8 * (cgrp & 3));
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = (wd >> e) & 1u ? v[e] : 0.0f;
     }
@@ -307,10 +316,10 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
         }
         if constexpr (BITS_OUT) bt |= (hl > 0.0f ? 1u : 0u) << (2 * e) | (hh > 0.0f ? 1u : 0u) << (2 * e + 1);
       }
-      // Each of the four lanes of a row owns one byte of the row's word.
-      if constexpr (BITS_OUT) reinterpret_cast<uint8_t*>(bits_lds + rl)[cgrp] = (uint8_t)bt;
+      // Each of the four lanes of a row and 32-column block owns one byte of its word.
+      if constexpr (BITS_OUT) reinterpret_cast<uint8_t*>(bits_lds + rl)[cgrp & 3] = (uint8_t)bt;
       // Non-temporal: the stored activations are re-read by later kernels, not by
-      // this one (measured 1.2% faster per update step than plain stores).
+      // this one (measured faster per update step than plain stores).
       if constexpr (STORE)
         __builtin_nontemporal_store(u32x4{w[0], w[1], w[2], w[3]},
                                     reinterpret_cast<u32x4*>(static_cast<bf16_t*>(g.C) + row * g.ldc + n0 + cb));
@@ -318,54 +327,40 @@ __device__ inline void epi_block(const GemmArgs& g, const f32x16& a, int i, int 
   }
 }
 
-// Epilogue. Accumulator blocks leave through a per-wave LDS scratch so that each
-// lane handles 8 consecutive columns of one row: 16-byte loads and stores. 32x32
-// accumulator layout: lane holds column lane%32; register q holds row
-// 8*(q/4) + 4*(lane/32) + q%4 of the block. The four lanes 4r..4r+3 hold the 32
-// columns of one row of a 32x32 block. Bias, output-layer weights and mask bits
-// come from the LDS staging area (EpiLds).
-//   CSUM (dgrad): column sums of the stored (rounded) values over the tile's 256
-//     rows go to g.colsum[mt, :]: per lane over its rows, a fixed butterfly over the
-//     16 lanes of a column group, then the WM waves of the column in order via LDS.
-//   BITS_OUT (fwd): one bit per stored value (> 0), 32 columns per word, words of
-//     one 32-column block stored row-contiguously; gathered in LDS and written to
-//     memory with one 16-byte store per thread at the end.
-//   BITS (dgrad): the same bits as the mask.
-//   RDOT (fwd): per row, the dot product of the stored values of the wave's
-//     BN/WN columns with rdot_w, one partial per (column tile, wave column).
-//   NOSTORE (fwd): C itself is not written.
-// Blocks go column-block-major when column sums accumulate over row blocks and
-// row-block-major otherwise, so that only the running sums of one block row or
-// column stay live.
+// Epilogue over the wave's blocks, in pairs (epi_pair). Bias, output-layer weights
+// and mask bits come from the LDS staging area (EpiLds). Pairs go column-major when
+// column sums accumulate over row blocks and row-major otherwise, so that only the
+// running sums of one block row or column stay live. BITS_OUT words are gathered in
+// LDS and written to memory with one 16-byte store per thread at the end.
 template <int MODE, int BN, int F>
 __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0,
                                 int n0, int wm, int wn, int lane, int wave, int z, int mt, float* smem_f,
                                 uint32_t* in) {
   constexpr int TM_ = BM / WM / 32, TN_ = BN / WN / 32, WCOLS = BN / WN;
-  float* scr = smem_f + wave * (32 * SCR_PITCH);
-  float* csh = smem_f + (NT / 64) * 32 * SCR_PITCH;   // [WM][BN]
-  const int cgrp = lane & 3, rsub = lane >> 2;
+  static_assert(TN_ % 2 == 0, "blocks leave in horizontal pairs");
+  float* scr = smem_f + wave * (SCR_ROWS * SCR_PITCH);
+  float* csh = smem_f + (NT / 64) * SCR_ROWS * SCR_PITCH;   // [WM][BN]
+  const int cgrp = lane & 7, rsub = lane >> 3;
   if constexpr ((F & EPI_CSUM) != 0) {
 #pragma unroll
-    for (int j = 0; j < TN_; ++j) {
-      float cs[8], rd[2];
+    for (int jp = 0; jp < TN_ / 2; ++jp) {
+      float cs[8], rd[4];
 #pragma unroll
       for (int e = 0; e < 8; ++e) cs[e] = 0.0f;
 #pragma unroll
       for (int i = 0; i < TM_; ++i)
-        epi_block<MODE, BN, F>(g, acc[i][j], i, j, m0, n0, wm, wn, lane, z, scr, in, cs, rd);
-      // Reduce-scatter over lane bits 2, 3, 4 (each exchange halves the columns a
-      // lane keeps), then across the two lane halves: 8 exchanges instead of 32.
-      const bool b2 = lane & 4, b3 = lane & 8, b4 = lane & 16;
+        epi_pair<MODE, BN, F>(g, acc[i][2 * jp], acc[i][2 * jp + 1], i, jp, m0, n0, wm, wn, lane, z, scr, in, cs,
+                              rd);
+      // Reduce-scatter over lane bits 3, 4, 5 (the 8 rows of a column group; each
+      // exchange halves the columns a lane keeps).
+      const bool b3 = lane & 8, b4 = lane & 16, b5 = lane & 32;
       float t4[4], t2[2];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) t4[e] = (b2 ? cs[4 + e] : cs[e]) + __shfl_xor(b2 ? cs[e] : cs[4 + e], 4);
+      for (int e = 0; e < 4; ++e) t4[e] = (b3 ? cs[4 + e] : cs[e]) + __shfl_xor(b3 ? cs[e] : cs[4 + e], 8);
 #pragma unroll
-      for (int e = 0; e < 2; ++e) t2[e] = (b3 ? t4[2 + e] : t4[e]) + __shfl_xor(b3 ? t4[e] : t4[2 + e], 8);
-      float t1 = (b4 ? t2[1] : t2[0]) + __shfl_xor(b4 ? t2[0] : t2[1], 16);
-      t1 += __shfl_xor(t1, 32);
-      if (lane < 32)
-        csh[wm * BN + wn * WCOLS + 32 * j + 8 * cgrp + 4 * b2 + 2 * b3 + (b4 ? 1 : 0)] = t1;
+      for (int e = 0; e < 2; ++e) t2[e] = (b4 ? t4[2 + e] : t4[e]) + __shfl_xor(b4 ? t4[e] : t4[2 + e], 16);
+      const float t1 = (b5 ? t2[1] : t2[0]) + __shfl_xor(b5 ? t2[0] : t2[1], 32);
+      csh[wm * BN + wn * WCOLS + 64 * jp + 8 * cgrp + 4 * b3 + 2 * b4 + (b5 ? 1 : 0)] = t1;
       __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
@@ -378,20 +373,22 @@ __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM /
   } else {
 #pragma unroll
     for (int i = 0; i < TM_; ++i) {
-      float cs[8], rd[2] = {0.0f, 0.0f};
+      float cs[8], rd[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int j = 0; j < TN_; ++j) {
-        epi_block<MODE, BN, F>(g, acc[i][j], i, j, m0, n0, wm, wn, lane, z, scr, in, cs, rd);
+      for (int jp = 0; jp < TN_ / 2; ++jp) {
+        epi_pair<MODE, BN, F>(g, acc[i][2 * jp], acc[i][2 * jp + 1], i, jp, m0, n0, wm, wn, lane, z, scr, in, cs,
+                              rd);
         __builtin_amdgcn_sched_barrier(0);
       }
       if constexpr ((F & EPI_RDOT) != 0) {
         const int part = (n0 + wn * WCOLS) / WCOLS;
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
+        for (int p = 0; p < 4; ++p) {
           float t = rd[p];
           t += __shfl_xor(t, 1);
           t += __shfl_xor(t, 2);
-          if (cgrp == 0) g.rdot_part[(int64_t)part * g.ldrd + m0 + wm * (BM / WM) + 32 * i + rsub + 16 * p] = t;
+          t += __shfl_xor(t, 4);
+          if (cgrp == 0) g.rdot_part[(int64_t)part * g.ldrd + m0 + wm * (BM / WM) + 32 * i + 8 * p + rsub] = t;
         }
       }
     }
@@ -639,7 +636,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   // The barrier of the last slice came after every wave's last LDS read, so the
   // epilogue may reuse LDS: scratch first, then the staged inputs.
   float* scratch = reinterpret_cast<float*>(smem);
-  uint32_t* in = reinterpret_cast<uint32_t*>(scratch + (NT / 64) * 32 * SCR_PITCH + WM * BN);
+  uint32_t* in = reinterpret_cast<uint32_t*>(scratch + scr_floats<BN>());
   if constexpr (MODE != GEMM_WGRAD) {
     pre.store(in, tid);
     __syncthreads();
@@ -653,7 +650,7 @@ hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
   using TB = BigTile<MODE == GEMM_FWD, BN>;
   const size_t tiles = MODE != GEMM_WGRAD ? 2 * ChunkLds<BN>::BYTES
                                           : STAGES * (TA::ELEMS + TB::ELEMS) * sizeof(bf16_t);
-  const size_t scratch = ((NT / 64) * 32 * SCR_PITCH + WM * BN + EpiLds<BN>::WORDS) * sizeof(float);
+  const size_t scratch = (scr_floats<BN>() + EpiLds<BN>::WORDS) * sizeof(float);
   const size_t lds = tiles > scratch ? tiles : scratch;
   static bool attr = false;
   if (!attr) {
