@@ -175,7 +175,7 @@ def main():
                          "from batch 16384 on a context created with the workload's batch")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--data-seed", type=int, default=0)
-    ap.add_argument("--cpu-sample-batch", type=int, default=16384)
+    ap.add_argument("--cpu-sample-batch", type=int, default=32768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
     args = ap.parse_args()
