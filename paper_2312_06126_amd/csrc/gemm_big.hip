@@ -192,12 +192,13 @@ struct EpiLds {
 };
 
 // Global loads of the staged inputs, issued before the last slice's MFMAs so their
-// latency is hidden; one 16-byte load per thread and input at most.
+// latency is hidden; 16-byte loads.
 template <int MODE, int BN, int F>
 struct EpiPrefetch {
   static constexpr bool BIAS = MODE == GEMM_FWD, RDOT = (F & EPI_RDOT) != 0, BITS = (F & EPI_BITS) != 0;
   static constexpr int NBITS = (BN / 32) * BM / 4;   // 16-byte pieces of the bits tile
-  u32x4 bits, rdw;
+  static constexpr int NBP = (NBITS + NT - 1) / NT;   // ... per thread
+  u32x4 bits[NBP], rdw;
   float4 bias;
   __device__ inline void load(const GemmArgs& g, int m0, int n0, int tid) {
     if constexpr (BIAS) {
@@ -208,9 +209,13 @@ struct EpiPrefetch {
       if (tid < BN / 8) rdw = *reinterpret_cast<const u32x4*>(static_cast<const bf16_t*>(g.rdot_w) + n0 + 8 * tid);
     }
     if constexpr (BITS) {
-      if (tid < NBITS) {
-        const int wc = tid / (BM / 4), r4 = (tid % (BM / 4)) * 4;
-        bits = *reinterpret_cast<const u32x4*>(g.bits + (int64_t)(n0 / 32 + wc) * g.ldbits + m0 + r4);
+#pragma unroll
+      for (int p = 0; p < NBP; ++p) {
+        const int t = tid + p * NT;
+        if (t < NBITS) {
+          const int wc = t / (BM / 4), r4 = (t % (BM / 4)) * 4;
+          bits[p] = *reinterpret_cast<const u32x4*>(g.bits + (int64_t)(n0 / 32 + wc) * g.ldbits + m0 + r4);
+        }
       }
     }
   }
@@ -223,7 +228,9 @@ struct EpiPrefetch {
       if (tid < BN / 8) *reinterpret_cast<u32x4*>(lds + L::RDW + 4 * tid) = rdw;
     }
     if constexpr (BITS) {
-      if (tid < NBITS) *reinterpret_cast<u32x4*>(lds + L::BITS + 4 * tid) = bits;
+#pragma unroll
+      for (int p = 0; p < NBP; ++p)
+        if (tid + p * NT < NBITS) *reinterpret_cast<u32x4*>(lds + L::BITS + 4 * (tid + p * NT)) = bits[p];
     }
   }
 };
