@@ -326,7 +326,7 @@ hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   if (g.colsum && !gemm_colsum_fused(bf16, mode, g.M, g.N, g.K)) return hipErrorInvalidValue;
   // Epilogue features of the large-tile kernel only: the whole product must run there.
   const bool fused = g.bits_out || g.bits || g.rdot_w || g.no_store;
-  if ((fused || g.colsum) && mode == GEMM_DGRAD && !g.Bt) return hipErrorInvalidValue;
+  if ((fused || g.colsum) && ((mode == GEMM_DGRAD && !g.Bt) || !big_gemm_ld_ok(mode, g))) return hipErrorInvalidValue;
   if (fused) {
     if (mode == GEMM_WGRAD || !gemm_fused_ok(bf16, mode, g.M, g.N, g.K)) return hipErrorInvalidValue;
     if ((g.bits_out || g.bits) && (g.ldbits < g.M || ((uintptr_t)(g.bits_out ? (const void*)g.bits_out : g.bits) & 3)))
@@ -343,7 +343,8 @@ hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   if (g.lda % vec || g.ldb % vec) return hipErrorInvalidValue;
   if (mode == GEMM_WGRAD && (g.splits < 1 || g.K % g.splits)) return hipErrorInvalidValue;
   if (bf16 && big_gemm_fits(mode, g.M, g.N, g.K, mode == GEMM_WGRAD ? g.splits : 1) &&
-      big_epilogue_supported(mode, epilogue_flags(mode, g)) && (mode != GEMM_DGRAD || g.Bt))
+      big_epilogue_supported(mode, epilogue_flags(mode, g)) && (mode != GEMM_DGRAD || g.Bt) &&
+      big_gemm_ld_ok(mode, g))
     return gemm_big(mode, g, s);
   return gemm_generic(bf16, mode, g, s);
 }

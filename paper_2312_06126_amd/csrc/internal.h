@@ -154,6 +154,9 @@ int big_bn(int N, bool fused);
 // True when gemm() with these arguments can produce the fused column sums (GemmArgs::colsum).
 bool gemm_colsum_fused(bool bf16, GemmMode mode, int M, int N, int K);
 bool big_gemm_colsum(GemmMode mode, int M, int N, int K);
+// Leading dimensions the large-tile kernel addresses (forward and input gradient:
+// below 2^22 elements).
+bool big_gemm_ld_ok(GemmMode mode, const GemmArgs& g);
 hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s);
 // True when a product of this shape runs entirely on the large-tile kernel, so that
 // bits_out / bits / rdot_w / no_store / colsum may be used.
