@@ -123,30 +123,33 @@ constexpr int BUF_DW3 = 0x00020000;
 __host__ __device__ constexpr int csw(int r) { return (r >> 1) & 7; }
 
 // ROWS x 64 operand chunk: one wave instruction fills 1 KB of LDS (lane l at byte
-// 16 l) = 8 rows. Element offsets beyond the last k are clamped to a valid address
-// (those values are never read back); RG rows at or beyond lim (ragged last tile of
-// N) are loaded from row lim - 1 (their products land only in columns not stored).
-// The buffer resource starts at row r0 and covers the rows up to lim (at most 2 GiB,
-// the 32-bit offset range; a tile's offsets stay far below that).
+// 16 l) = 8 rows. Each chunk gets its own buffer resource, starting at element
+// (r0, k0) and ending with row lim - 1, so the per-lane offsets do not change from
+// chunk to chunk (they stay in registers) and the hardware range check turns reads
+// past the end of the operand into zeros: the k beyond the last column of a row read
+// the next row's values (never read back), and chunks past the end of the product
+// read nothing. RG rows at or beyond lim (ragged last tile of N) are loaded from row
+// lim - 1 (their products land only in columns not stored). Offsets are 32-bit: 256
+// rows of the operand stay below 2 GiB (big_gemm_ld_ok).
 template <int ROWS>
 struct FwdChunk {
   static constexpr int BYTES = ROWS * CK * 2;
   static constexpr int PER = BYTES / 1024 / (NT / 64);   // instructions per wave
   static_assert(PER * 1024 * (NT / 64) == BYTES, "chunk must split evenly over the waves");
   template <bool RG>
-  __device__ static inline void issue(const bf16_t* __restrict__ base, int64_t ld, int r0, int k0, int kmax,
-                                      uint8_t* lds, int wave, int lane, int lim) {
-    const int64_t nrec = ((int64_t)lim - r0) * ld * 2;
-    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(base + (int64_t)r0 * ld), (short)0, (int)(nrec < 0x7fffffff ? nrec : 0x7fffffff), BUF_DW3);
+  __device__ static inline void issue(const bf16_t* __restrict__ base, int64_t ld, int r0, int k0, uint8_t* lds,
+                                      int wave, int lane, int lim) {
+    int64_t nrec = ((int64_t)lim - r0) * ld * 2 - (int64_t)k0 * 2;
+    nrec = nrec < 0 ? 0 : (nrec < 0x7fffffff ? nrec : 0x7fffffff);
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(base + (int64_t)r0 * ld + k0), (short)0, (int)nrec, BUF_DW3);
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int idx = wave + p * (NT / 64);
       const int rr = idx * 8 + (lane >> 3);
-      const int k = k0 + 8 * ((lane & 7) ^ csw(rr));
       int row = rr;
       if constexpr (RG) row = r0 + row < lim ? row : lim - 1 - r0;
-      const int voff = (row * (int)ld + (k < kmax ? k : kmax)) * 2;
+      const int voff = (row * (int)ld + 8 * ((lane & 7) ^ csw(rr))) * 2;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (LDS_AS void*)(lds + idx * 1024), 16, voff, 0, 0, 0);
     }
   }
@@ -453,11 +456,11 @@ __device__ inline void chunk_main_loop(const GemmArgs& g, f32x16 (&acc)[BM / WM 
   const bf16_t* __restrict__ B = static_cast<const bf16_t*>(g.B);
   const int nk = g.K / BK;                    // 32-deep slices
   const int nfull = nk >> 1;
-  const int kmax = g.K - 8;
+  wave = __builtin_amdgcn_readfirstlane(wave);   // LDS destinations (M0) from scalar registers
   auto stage = [&](int c) { return smem + (c & 1) * SB; };
   auto issue = [&](int c) {
-    CA::template issue<false>(A, g.lda, m0, c * CK, kmax, stage(c), wave, lane, g.M);
-    CB::template issue<RG>(B, g.ldb, n0, c * CK, kmax, stage(c) + ABYTES, wave, lane, g.N);
+    CA::template issue<false>(A, g.lda, m0, c * CK, stage(c), wave, lane, g.M);
+    CB::template issue<RG>(B, g.ldb, n0, c * CK, stage(c) + ABYTES, wave, lane, g.N);
   };
   bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
   auto read_step = [&](const uint8_t* st, int ks, bf16x8 (&fa)[TM], bf16x8 (&fb)[TN]) {
