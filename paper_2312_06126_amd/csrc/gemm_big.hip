@@ -41,6 +41,8 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef int16_t i16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 #define LDS_AS __attribute__((address_space(3)))
 
 constexpr int BM = 256, BK = 32, NT = 512, WM = 4, WN = 2, STAGES = 3;
@@ -210,7 +212,7 @@ struct EpiLds {
 // latency is hidden; 16-byte loads.
 template <int MODE, int BN, int F>
 struct EpiPrefetch {
-  static constexpr bool BIAS = MODE == GEMM_FWD, RDOT = (F & EPI_RDOT) != 0, BITS = (F & EPI_BITS) != 0;
+  static constexpr bool BIAS = false, RDOT = (F & EPI_RDOT) != 0, BITS = (F & EPI_BITS) != 0;   // bias: in the accumulators
   static constexpr int NBITS = (BN / 32) * BM / 4;   // 16-byte pieces of the bits tile
   static constexpr int NBP = (NBITS + NT - 1) / NT;   // ... per thread
   u32x4 bits[NBP], rdw;
@@ -264,15 +266,6 @@ __device__ inline void epi_pair(const GemmArgs& g, const f32x16& a0, const f32x1
   constexpr bool STORE = !(F & EPI_NOSTORE);
   const int cgrp = lane & 7, rsub = lane >> 3;
   const int cb = wn * WCOLS + 64 * jp + 8 * cgrp;   // lane's first column in the tile
-  float bias[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) bias[e] = 0.0f;
-  if constexpr (MODE == GEMM_FWD) {
-    const float4 b0 = *reinterpret_cast<const float4*>(in + L::BIAS + cb);
-    const float4 b1 = *reinterpret_cast<const float4*>(in + L::BIAS + cb + 4);
-    bias[0] = b0.x; bias[1] = b0.y; bias[2] = b0.z; bias[3] = b0.w;
-    bias[4] = b1.x; bias[5] = b1.y; bias[6] = b1.z; bias[7] = b1.w;
-  }
   uint32_t ww[4] = {0u, 0u, 0u, 0u};   // output-layer weights of the lane's 8 columns, packed bf16
   if constexpr (RDOT) {
     const u32x4 w4 = *reinterpret_cast<const u32x4*>(in + L::RDW + cb / 2);
@@ -299,10 +292,11 @@ __device__ inline void epi_pair(const GemmArgs& g, const f32x16& a0, const f32x1
       *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
       continue;
     }
+    // The forward's bias is already in the accumulators (k_gemm_big). ReLU of a bf16
+    // output is taken on the rounded values (below).
+    if constexpr (RELU && OUTF32) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      if constexpr (MODE == GEMM_FWD) v[e] += bias[e];
-      if constexpr (RELU) v[e] = v[e] < 0.0f ? 0.0f : v[e];
+      for (int e = 0; e < 8; ++e) v[e] = v[e] < 0.0f ? 0.0f : v[e];
     }
     if constexpr (MASK) {
       const uint4 mk = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(g.mask) + row * g.ldm + n0 + cb);
@@ -327,15 +321,18 @@ __device__ inline void epi_pair(const GemmArgs& g, const f32x16& a0, const f32x1
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         w[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
+        // ReLU on the two rounded values at once: a bf16 is negative exactly when its
+        // bits are as int16 (a rounded -0.0 becomes +0.0).
+        if constexpr (RELU) w[e] = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(i16x2, w[e]), i16x2{0, 0}));
         const float hl = __uint_as_float(w[e] << 16), hh = __uint_as_float(w[e] & 0xFFFF0000u);
         if constexpr (CSUM) {
           cs[2 * e] += hl;
           cs[2 * e + 1] += hh;
         }
-        if constexpr (RDOT) {
-          rd[p] = fmaf(hl, __uint_as_float(ww[e] << 16), rd[p]);
-          rd[p] = fmaf(hh, __uint_as_float(ww[e] & 0xFFFF0000u), rd[p]);
-        }
+        // Two products of bf16 values and the running sum in one instruction.
+        if constexpr (RDOT)
+          rd[p] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), __builtin_bit_cast(bf16x2, ww[e]), rd[p],
+                                                  false);
         if constexpr (BITS_OUT) bt |= (hl > 0.0f ? 1u : 0u) << (2 * e) | (hh > 0.0f ? 1u : 0u) << (2 * e + 1);
       }
       // Each of the four lanes of a row and 32-column block owns one byte of its word.
@@ -554,13 +551,20 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.A);
   const bf16_t* __restrict__ B = static_cast<const bf16_t*>(g.B);
 
+  // The forward's bias starts the accumulators (accumulator column = lane % 32).
   f32x16 acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int j = 0; j < TN; ++j) {
+    float b = 0.0f;
+    if constexpr (MODE == GEMM_FWD) {
+      const int n = n0 + wn * (BN / WN) + 32 * j + (lane & 31);
+      if (g.bias && n < g.N) b = g.bias[n];
+    }
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = b;
+  }
 
   EpiPrefetch<MODE, BN, F> pre;
   if constexpr (MODE != GEMM_WGRAD) {
