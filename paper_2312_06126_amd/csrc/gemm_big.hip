@@ -298,8 +298,11 @@ __device__ inline void epi_pair(const GemmArgs& g, const f32x16& a0, const f32x1
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = v[e] < 0.0f ? 0.0f : v[e];
     }
+    // Row offsets within the tile in 32-bit arithmetic (leading dimensions below 2^22,
+    // big_gemm_ld_ok), added to the tile's base address.
     if constexpr (MASK) {
-      const uint4 mk = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(g.mask) + row * g.ldm + n0 + cb);
+      const uint4 mk = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(g.mask) + (int64_t)m0 * g.ldm + n0 +
+                                                        (rl * (int)g.ldm + cb));
       const uint32_t mw[4] = {mk.x, mk.y, mk.z, mk.w};
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -307,41 +310,75 @@ __device__ inline void epi_pair(const GemmArgs& g, const f32x16& a0, const f32x1
         v[e] = h > 0.0f ? v[e] : 0.0f;
       }
     }
-    if constexpr (BITS) {
+    if constexpr (BITS && OUTF32) {
       const uint32_t wd = bits_lds[rl] >> (8 * (cgrp & 3));
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = (wd >> e) & 1u ? v[e] : 0.0f;
     }
     if constexpr (OUTF32) {
-      float* dst = static_cast<float*>(g.C) + row * g.ldc + n0 + cb;
+      float* dst = static_cast<float*>(g.C) + (int64_t)m0 * g.ldc + n0 + (rl * (int)g.ldc + cb);
       *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
       *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
     } else {
-      uint32_t w[4], bt = 0;
+      // bf16 output. The epilogue is VALU-bound, so the per-value work is done on the
+      // rounded pairs where that is exact: ReLU (a bf16 is negative exactly when its
+      // bits are as int16; a rounded -0.0 becomes +0.0), the mask bits (masking before
+      // or after rounding gives the same bits), the mask bits out (after ReLU a value
+      // is > 0 exactly when its bits are nonzero); column sums and the row dot take
+      // both values of a pair with one v_dot2_f32_bf16 (products by 1, 0 are exact).
+      static_assert(!BITS_OUT || RELU, "mask bits out are taken of ReLU outputs");
+      uint32_t w[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         w[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
-        // ReLU on the two rounded values at once: a bf16 is negative exactly when its
-        // bits are as int16 (a rounded -0.0 becomes +0.0).
-        if constexpr (RELU) w[e] = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(i16x2, w[e]), i16x2{0, 0}));
-        const float hl = __uint_as_float(w[e] << 16), hh = __uint_as_float(w[e] & 0xFFFF0000u);
-        if constexpr (CSUM) {
-          cs[2 * e] += hl;
-          cs[2 * e + 1] += hh;
+        if constexpr (RELU)
+          w[e] = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(i16x2, w[e]), i16x2{0, 0}));
+      }
+      if constexpr (BITS) {
+        const int wd = (int)(bits_lds[rl] >> (8 * (cgrp & 3)));
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          w[e] &= (0x0000FFFFu & (uint32_t)__builtin_amdgcn_sbfe(wd, 2 * e, 1)) |
+                  (0xFFFF0000u & (uint32_t)__builtin_amdgcn_sbfe(wd, 2 * e + 1, 1));
+      }
+      if constexpr (CSUM) {
+        // (1, 0) and (0, 1) from registers: folded into an inline constant, (1, 0) was
+        // encoded as the 32-bit 1.0f, which the packed operand reads as (0, 1).
+        uint32_t k_lo = 0x00003F80u, k_hi = 0x3F800000u;
+        asm volatile("" : "+v"(k_lo), "+v"(k_hi));
+        const bf16x2 lo1 = __builtin_bit_cast(bf16x2, k_lo), hi1 = __builtin_bit_cast(bf16x2, k_hi);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          cs[2 * e] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), lo1, cs[2 * e], false);
+          cs[2 * e + 1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), hi1, cs[2 * e + 1], false);
         }
-        // Two products of bf16 values and the running sum in one instruction.
-        if constexpr (RDOT)
+      }
+      if constexpr (RDOT) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
           rd[p] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), __builtin_bit_cast(bf16x2, ww[e]), rd[p],
                                                   false);
-        if constexpr (BITS_OUT) bt |= (hl > 0.0f ? 1u : 0u) << (2 * e) | (hh > 0.0f ? 1u : 0u) << (2 * e + 1);
       }
-      // Each of the four lanes of a row and 32-column block owns one byte of its word.
-      if constexpr (BITS_OUT) reinterpret_cast<uint8_t*>(bits_lds + rl)[cgrp & 3] = (uint8_t)bt;
+      if constexpr (BITS_OUT) {
+        // halves clamped to 0 / 1, pair e at bits 2e (low) and 16 + 2e (high)
+        uint32_t t = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint32_t m;
+          // one packed min (the compiler splits the vector form into compares and selects)
+          // (1, 1) from a register: an inline constant would give the high half 0
+          asm("v_pk_min_u16 %0, %1, %2" : "=v"(m) : "v"(w[e]), "s"(0x00010001u));
+          t |= m << (2 * e);
+        }
+        // Each of the four lanes of a row and 32-column block owns one byte of its word.
+        reinterpret_cast<uint8_t*>(bits_lds + rl)[cgrp & 3] = (uint8_t)((t | (t >> 15)) & 0xFFu);
+      }
       // Non-temporal: the stored activations are re-read by later kernels, not by
       // this one (measured faster per update step than plain stores).
       if constexpr (STORE)
         __builtin_nontemporal_store(u32x4{w[0], w[1], w[2], w[3]},
-                                    reinterpret_cast<u32x4*>(static_cast<bf16_t*>(g.C) + row * g.ldc + n0 + cb));
+                                    reinterpret_cast<u32x4*>(static_cast<bf16_t*>(g.C) + (int64_t)m0 * g.ldc + n0 +
+                                                             (rl * (int)g.ldc + cb)));
     }
   }
 }
@@ -776,7 +813,8 @@ bool big_gemm_ld_ok(GemmMode mode, const GemmArgs& g) {
   // byte offsets: 256 rows of the widest operand must stay below 2 GiB.
   constexpr int64_t LIM = (int64_t)1 << 22;
   if (mode == GEMM_WGRAD) return true;
-  return g.lda < LIM && (mode == GEMM_FWD ? g.ldb : g.ldbt) < LIM;
+  // The epilogue addresses rows of C (and of a stored mask) within a tile the same way.
+  return g.lda < LIM && (mode == GEMM_FWD ? g.ldb : g.ldbt) < LIM && g.ldc < LIM && (!g.mask || g.ldm < LIM);
 }
 
 hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s) {
