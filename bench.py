@@ -17,6 +17,10 @@ roofline (per-launch event timings taken by the library on the stream the kernel
 runs on, during the timed region, where only that kernel's launches carry events;
 the kernel is picked, and the per-kernel table taken, in an untimed survey pass
 before) and the CPU oracle's rate on a bounded sample of the same workload.
+roofline.traffic (HBM bytes per launch) and roofline.mfma_busy (share of cycles the
+matrix cores are busy, rocprofv3's MfmaUtil) come from the committed counter
+summaries under profiles/, and are null once the kernel sources differ from the
+ones the counters were taken on.
 """
 from __future__ import annotations
 
@@ -39,6 +43,8 @@ SURVEY_STEPS = 10   # untimed steps with every kernel launch timed (per-kernel t
 # Measured HBM traffic of the dominant kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
 # scaled by a plain copy of known size), valid while the kernel sources hash the same.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_fwd_1024_sac_large_bf16_traffic.txt")
+# Matrix-core busy share of the dominant kernel (rocprofv3 MfmaUtil), same validity rule.
+MFMA_FILE = os.path.join(ROOT, "profiles", "gemm_mfma_util_sac_large_bf16.md")
 KERNEL_SOURCES = ("gemm_big.hip", "gemm.hip", "internal.h")
 
 
@@ -71,21 +77,26 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str):
-    """Bytes per launch from the committed counter summary, or None when there is
-    none for this kernel or the kernel sources changed since it was taken."""
+def profile_value(path: str, kernel: str, key: str):
+    """A `key: value` entry of a committed counter summary, or None when there is none
+    for this kernel or the kernel sources changed since the counters were taken."""
     try:
         kv = {}
-        with open(TRAFFIC_FILE) as fh:
+        with open(path) as fh:
             for line in fh:
-                if ":" in line and not line.startswith("#"):
+                if ":" in line and not line.startswith(("#", "|")):
                     k, v = line.split(":", 1)
                     kv[k.strip()] = v.strip()
         if kv.get("kernel") != kernel or kv.get("source_sha256") != kernel_source_hash():
             return None
-        return float(kv["traffic_bytes_per_launch"])
+        return float(kv[key])
     except (OSError, KeyError, ValueError):
         return None
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)."""
+    return profile_value(TRAFFIC_FILE, kernel, "traffic_bytes_per_launch")
 
 
 def roofline(stats, prec: str):
@@ -103,6 +114,7 @@ def roofline(stats, prec: str):
     r["frac"] = round(achieved / peak, 4)
     r["kernel"] = "%s M=%d N=%d K=%d" % (top["name"], top["M"], top["N"], top["K"])
     r["traffic"] = measured_traffic(r["kernel"])
+    r["mfma_busy"] = profile_value(MFMA_FILE, r["kernel"], "mfma_busy") if top["name"] in GEMMS else None
     r["avg_launch_ms"] = round(top["avg_ms"], 5)
     r["launches"] = top["launches"]
     r["per_launch"] = top["flops"] if top["name"] in GEMMS else top["bytes"]
