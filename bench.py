@@ -69,11 +69,17 @@ def fill_ring(g, w, data_seed: int, rows: int):
 
 
 def kernel_source_hash() -> str:
+    """Hash of the GEMM sources with comments and blank space removed (an edit to a
+    comment leaves the counters valid; any change to the code does not)."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2312_06126_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2312_06126_amd", "csrc", f)) as fh:
+            src = fh.read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", "", src)
+        h.update("\n".join(ln.strip() for ln in src.splitlines() if ln.strip()).encode())
     return h.hexdigest()[:16]
 
 

@@ -31,6 +31,10 @@
 //   * XCD-aware tile order: workgroup b runs on XCD b % 8, so logical tiles are
 //     handed out in contiguous ranges per XCD; the column tiles of one row panel
 //     (and the split-K slices of one weight-gradient tile) share an L2.
+//   * Epilogue: the forward's bias starts the accumulators; blocks leave in pairs
+//     through a per-wave LDS scratch as 16-byte row pieces (whole 128-byte lines per
+//     store); ReLU, mask bits, column sums and row dots work on rounded bf16 pairs
+//     (the epilogue is VALU-heavy); see epi_pair.
 #include "internal.h"
 
 namespace spz {
