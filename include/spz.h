@@ -108,6 +108,13 @@ typedef struct spz_hparams {
   int32_t device;                 /* HIP device ordinal                            */
   int32_t n_streams;              /* 2: actor and critic on concurrent streams; 1: one stream */
   int32_t ordering;               /* SPZ_ORDER_SNAPSHOT | SPZ_ORDER_SEQUENTIAL (below)     */
+  int32_t actor_row_split;        /* SAC: 1 takes the actor loss's gradient through each
+                                     critic only on the rows where that critic attains
+                                     min(Q1, Q2) (the other rows carry zero gradient
+                                     there, Section 3.2.2's twin-critic minimum), with
+                                     the same results as 0, which takes both critics
+                                     over every row. Used where the ReLU masks are kept
+                                     as bits (bf16 with 128-multiple hidden widths).  */
 } spz_hparams;
 
 /* Update ordering within a step.
@@ -125,7 +132,7 @@ typedef struct spz_hparams {
 /* Defaults: SAC, fp32, capacity 1e6, gamma 0.99, tau 0.005, lr 3e-4, Adam
  * (0.9, 0.999, 1e-8), alpha_init 1, learned alpha, target_entropy 0, log-std
  * clamp [-20, 2], TD3 noise 0.2 clipped to 0.5, delay 2, device 0, 2 streams,
- * snapshot ordering. */
+ * snapshot ordering, actor row split on. */
 void spz_hparams_default(spz_hparams* hp);
 
 /* Create a learner. obs_dim, act_dim >= 1; hidden[0..n_hidden) >= 1 with

@@ -118,6 +118,12 @@ struct spz_ctx {
   std::vector<void*> hpc[2];
   std::vector<uint32_t*> bha, bhpc[2];
   float* a_rdot = nullptr;
+  // SAC row split of the actor's gradient through the critics: two row maps [Bp]
+  // and their padded lengths (device side), the actor loss's per-block critic-1
+  // counts, and one layer's mask bits gathered by a map.
+  bool row_split = false;
+  int32_t *rmap = nullptr, *rrows = nullptr, *rcnt = nullptr;
+  uint32_t* rbits = nullptr;
   void* a_dz[2] = {nullptr, nullptr};
   void* dzh = nullptr;
   float *a_wpart = nullptr, *a_cpart = nullptr;
@@ -393,10 +399,12 @@ hipError_t wgrad(spz_ctx* c, const void* dz, int64_t lddz, const void* X, int64_
 // large-tile kernel reads. With
 // bias_out, also the column sums of the stored out (the bias gradient of the layer
 // below): fused into the product's epilogue where the large-tile kernel covers it.
+// With m_dyn (a device-side count of leading rows), only those rows are computed.
 hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_t ldw, const void* Wt, int N,
                  const void* mask, const uint32_t* bits, void* out, int64_t ldo, bool out_f32, float* bias_out,
-                 float* cpart, hipStream_t s) {
+                 float* cpart, hipStream_t s, const int32_t* m_dyn = nullptr) {
   GemmArgs g{};
+  g.m_dyn = m_dyn;
   g.A = dz; g.lda = L.out_p;
   g.B = W; g.ldb = ldw;
   g.Bt = Wt; g.ldbt = L.out_p;
@@ -414,7 +422,9 @@ hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_
     g.colsum = cpart;
     g.ldcs = N;
   }
-  HK(timed(c, "gemm_dgrad", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
+  // Row-restricted products do a data-dependent amount of work: their records carry
+  // the launch shape and no flop count.
+  HK(timed(c, m_dyn ? "gemm_dgrad_rows" : "gemm_dgrad", g.M, g.N, g.K, m_dyn ? 0.0 : 2.0 * g.M * g.N * g.K, 0.0, s,
            [&] { return gemm(c->bf16, GEMM_DGRAD, g, s); }));
   if (!bias_out) return hipSuccess;
   if (fused)
@@ -487,6 +497,36 @@ hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* 
                c->Ap, true, nullptr, nullptr, s);
 }
 
+// The same restricted to the rows listed in map (padded with -1 to the device-side
+// length *rows): the head backward gathers those rows, every later product runs on
+// the first *rows rows only, and the action gradient is scattered back to da's rows
+// (rows of da outside the map are left as they are). Each row's arithmetic is that
+// of the unrestricted chain.
+hipError_t critic_action_grad_rows(spz_ctx* c, int ni, const float* dq, void* const* hid, uint32_t* const* bits,
+                                   const int32_t* map, const int32_t* rows, float* da, hipStream_t s) {
+  const Net& n = c->net[ni];
+  const int nl = (int)n.L.size();
+  const Lay& H = n.L[nl - 1];
+  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->a_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp,
+                 nullptr, map, rows};
+  HK(timed(c, "head_bwd_rows", c->Bp, H.in_p, 0, 0.0, 0.0, s, [&] { return launch_head_bwd(c->bf16, hb, s); }));
+  int cur = 0;
+  for (int l = nl - 2; l >= 1; --l) {
+    const Lay& L = n.L[l];
+    RowBitsGatherArgs gb{bits[l - 1], c->rbits, c->Bp, L.in_p / 32, map, rows, c->Bp};
+    HK(timed(c, "row_bits_gather", c->Bp, L.in_p, 0, 0.0, 0.0, s, [&] { return launch_row_bits_gather(gb, s); }));
+    HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, nullptr, c->rbits, c->a_dz[cur ^ 1],
+             L.in_p, false, nullptr, nullptr, s, rows));
+    cur ^= 1;
+  }
+  // The action gradient of the listed rows lands in da2 (free here) and then in da.
+  const Lay& L0 = n.L[0];
+  HK(dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, nullptr, c->Ap, nullptr, nullptr,
+           c->da2, c->Ap, true, nullptr, nullptr, s, rows));
+  RowScatterArgs sa{c->da2, da, c->Ap, c->Ap, map, rows, c->Bp};
+  return timed(c, "row_scatter", c->Bp, c->Ap, 0, 0.0, 0.0, s, [&] { return launch_row_scatter(sa, s); });
+}
+
 hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
   const Net& n = c->net[0];
   const int nl = (int)n.L.size();
@@ -557,12 +597,22 @@ hipError_t actor_part(spz_ctx* c, hipStream_t s) {
   if (!c->td3)
     HK(forward(c, 2, false, c->xsp, c->Kc, c->hpc[1].data(), c->bhpc[1].data(), false, c->a_rdot, c->qp2, s));
   ActorLossArgs al{c->qp1, c->td3 ? nullptr : c->qp2, c->logp, log_alpha_ptr(c), c->dqp1,
-                   c->td3 ? nullptr : c->dqp2, c->a_lpart, c->B, c->Bp};
+                   c->td3 ? nullptr : c->dqp2, c->a_lpart, c->B, c->Bp, c->row_split ? c->rcnt : nullptr};
   HK(timed(c, "actor_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_actor_loss(al, s); }));
-  HK(critic_action_grad(c, 1, c->dqp1, c->hpc[0].data(), c->bhpc[0].data(), c->da1, s));
-  if (!c->td3) HK(critic_action_grad(c, 2, c->dqp2, c->hpc[1].data(), c->bhpc[1].data(), c->da2, s));
-  ActorHeadBwdArgs hb{c->da1, c->td3 ? nullptr : c->da2, c->Ap, c->th, c->se, c->lm, log_alpha_ptr(c),
-                      c->dzh, pa, c->A, c->B, c->td3 ? 0 : 1};
+  if (c->row_split) {
+    // The loss takes min(Q1, Q2) per row, so each row's gradient reaches one critic
+    // only: each critic's chain runs on its own rows and both land in da1.
+    MinqSplitArgs ms{c->qp1, c->qp2, c->rcnt, c->B, c->Bp, c->rmap, c->rmap + c->Bp, c->rrows};
+    HK(timed(c, "minq_split", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_minq_split(ms, s); }));
+    HK(critic_action_grad_rows(c, 1, c->dqp1, c->hpc[0].data(), c->bhpc[0].data(), c->rmap, c->rrows, c->da1, s));
+    HK(critic_action_grad_rows(c, 2, c->dqp2, c->hpc[1].data(), c->bhpc[1].data(), c->rmap + c->Bp, c->rrows + 1,
+                               c->da1, s));
+  } else {
+    HK(critic_action_grad(c, 1, c->dqp1, c->hpc[0].data(), c->bhpc[0].data(), c->da1, s));
+    if (!c->td3) HK(critic_action_grad(c, 2, c->dqp2, c->hpc[1].data(), c->bhpc[1].data(), c->da2, s));
+  }
+  ActorHeadBwdArgs hb{c->da1, c->td3 || c->row_split ? nullptr : c->da2, c->Ap, c->th, c->se, c->lm,
+                      log_alpha_ptr(c), c->dzh, pa, c->A, c->B, c->td3 ? 0 : 1};
   HK(timed(c, "actor_head_bwd", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_actor_head_bwd(c->bf16, hb, s); }));
   return actor_backward(c, s);
 }
@@ -756,6 +806,15 @@ int setup(spz_ctx* c) {
     CK(dalloc_t(c, &c->c_rdot, (size_t)rd_parts * Bp * 4));
     CK(dalloc_t(c, &c->a_rdot, (size_t)rd_parts * Bp * 4));
   }
+  // The row split needs every hidden mask of both critics as bits.
+  c->row_split = !c->td3 && c->hp.actor_row_split;
+  for (int l = 0; l < nh; ++l) c->row_split = c->row_split && c->bhpc[0][l] && c->bhpc[1][l];
+  if (c->row_split) {
+    CK(dalloc_t(c, &c->rmap, (size_t)2 * Bp * 4));
+    CK(dalloc_t(c, &c->rrows, 64));
+    CK(dalloc_t(c, &c->rcnt, (size_t)(Bp / 256) * 4));
+    CK(dalloc_t(c, &c->rbits, (size_t)Bp * (c->hmax / 32) * 4));
+  }
   // reduction workspaces
   int64_t wmax = 0, cmax = 0;
   for (int ni = 0; ni < 3; ++ni)
@@ -880,6 +939,7 @@ void spz_hparams_default(spz_hparams* hp) {
   hp->device = 0;
   hp->n_streams = 2;
   hp->ordering = SPZ_ORDER_SNAPSHOT;
+  hp->actor_row_split = 1;
 }
 
 spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int32_t n_hidden, int32_t batch,
@@ -900,7 +960,8 @@ spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int
       hp->capacity > 0xFFFFFFFFll || !(hp->tau >= 0.0f && hp->tau <= 1.0f) ||
       (hp->algo == SPZ_ALGO_SAC && !(hp->alpha_init > 0.0f)) || hp->policy_delay < 1 ||
       (hp->n_streams != 1 && hp->n_streams != 2) || !(hp->log_std_min <= hp->log_std_max) ||
-      (hp->ordering != SPZ_ORDER_SNAPSHOT && hp->ordering != SPZ_ORDER_SEQUENTIAL)) {
+      (hp->ordering != SPZ_ORDER_SNAPSHOT && hp->ordering != SPZ_ORDER_SEQUENTIAL) ||
+      (hp->actor_row_split != 0 && hp->actor_row_split != 1)) {
     set_err(nullptr, SPZ_EINVAL, "spz_create: invalid hyper-parameters");
     return nullptr;
   }

@@ -120,6 +120,9 @@ __global__ void __launch_bounds__(gemm_threads(BM, BN)) k_gemm(GemmArgs g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / S::WN, wn = wave % S::WN;
   const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+  if constexpr (MODE == GEMM_DGRAD) {
+    if (g.m_dyn && m0 >= *g.m_dyn) return;
+  }
   int kbeg = 0, kend = g.K;
   if constexpr (MODE == GEMM_WGRAD) {
     const int ks = g.K / g.splits;
@@ -324,6 +327,9 @@ bool gemm_fused_ok(bool bf16, GemmMode mode, int M, int N, int K) {
 
 hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   if (g.colsum && !gemm_colsum_fused(bf16, mode, g.M, g.N, g.K)) return hipErrorInvalidValue;
+  // A device-side row count: input-gradient products only, whole 256-row tiles, and
+  // no per-tile column sums (the skipped tiles would leave theirs unwritten).
+  if (g.m_dyn && (mode != GEMM_DGRAD || g.colsum || g.M % 256)) return hipErrorInvalidValue;
   // Epilogue features of the large-tile kernel only: the whole product must run there.
   const bool fused = g.bits_out || g.bits || g.rdot_w || g.no_store;
   if ((fused || g.colsum) && ((mode == GEMM_DGRAD && !g.Bt) || !big_gemm_ld_ok(mode, g))) return hipErrorInvalidValue;

@@ -573,7 +573,14 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   bf16_t* S = reinterpret_cast<bf16_t*>(smem);
 
   // XCD-aware logical tile: contiguous logical ranges per XCD, column tiles fastest.
-  const int total = gridDim.x;
+  int total = gridDim.x;
+  if constexpr (MODE == GEMM_DGRAD) {
+    // A device-side row count: only its tiles run, spread over the XCDs as usual.
+    if (g.m_dyn) {
+      total = (*g.m_dyn / BM) * tiles_n;
+      if ((int)blockIdx.x >= total) return;
+    }
+  }
   int L = blockIdx.x;
   if ((total & 7) == 0) L = (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3);
   const int nt = L % tiles_n;

@@ -114,6 +114,10 @@ struct GemmArgs {
   float* rdot_part;            // gemm_rdot_cols(N) columns c of stored C[r, c] * rdot_w[c]
   int64_t ldrd;
   int no_store;                // FWD with rdot_w: C is not written
+  // DGRAD: when set, only rows [0, *m_dyn) of C are computed (a device-side count,
+  // a multiple of 256 and at most M); the launch is still sized by M and the
+  // blocks past the count exit at once. Rows from *m_dyn on are left untouched.
+  const int32_t* m_dyn;
 };
 
 enum EpilogueFlag : int {

@@ -52,6 +52,10 @@ struct HeadBwdArgs {
   // With bits: when set, the column sums of the stored dH over each block of rows go
   // to colpart[block, K] (head_bwd_blocks(rows) blocks; reduce with launch_colsum_final).
   float* colpart;
+  // With bits and without colpart: when map is set, row r < *m_dyn of dH is row
+  // map[r] of the product (dq, bits read there), a zero row where map[r] < 0; rows
+  // from *m_dyn on are not written. Row maps come from launch_minq_split.
+  const int32_t* map; const int32_t* m_dyn;
 };
 
 // Sampler observations -> actor operand rows: x[r, c] = obs[r, c] for r < n, c < O;
@@ -82,6 +86,29 @@ struct CriticLossArgs {
 
 struct ActorLossArgs {
   const float *qp1, *qp2, *logp, *log_alpha; float *dqp1, *dqp2; double* part; int B, Bp;
+  // With qp2, when set: cnt1[k] = the rows b < B of the k-th 256-row block whose
+  // minimum critic is critic 1 (qp1[b] <= qp2[b], the loss's own choice).
+  int32_t* cnt1;
+};
+
+// Rows of the SAC actor loss split by the critic that attains min(qp1, qp2) (critic 1
+// on ties, as in the loss): map1 lists in ascending order the rows b < B of critic 1,
+// map2 those of critic 2; list i is padded with -1 up to rows[i] = min(n_i rounded up
+// to 512, Bp) entries (n_i: its row count). cnt1 as written by the actor loss.
+struct MinqSplitArgs {
+  const float *qp1, *qp2; const int32_t* cnt1; int B, Bp;
+  int32_t *map1, *map2, *rows;
+};
+
+// dst[w * ld + r] = src[w * ld + map[r]] (0 where map[r] < 0), w < words, r < *m_dyn:
+// the rows of a bit-packed ReLU mask (layout of HeadBwdArgs::bits) gathered by a map.
+struct RowBitsGatherArgs {
+  const uint32_t* src; uint32_t* dst; int64_t ld; int words; const int32_t* map; const int32_t* m_dyn; int rows;
+};
+
+// dst[map[r] * ld + j] = src[r * ld + j] for r < *m_dyn with map[r] >= 0, j < cols.
+struct RowScatterArgs {
+  const float* src; float* dst; int64_t ld; int cols; const int32_t* map; const int32_t* m_dyn; int rows;
 };
 
 struct ActorHeadBwdArgs {
@@ -123,6 +150,9 @@ hipError_t launch_td_target(const TdArgs& a, hipStream_t s);
 int loss_blocks(int Bp);
 hipError_t launch_critic_loss(const CriticLossArgs& a, hipStream_t s);
 hipError_t launch_actor_loss(const ActorLossArgs& a, hipStream_t s);
+hipError_t launch_minq_split(const MinqSplitArgs& a, hipStream_t s);
+hipError_t launch_row_bits_gather(const RowBitsGatherArgs& a, hipStream_t s);
+hipError_t launch_row_scatter(const RowScatterArgs& a, hipStream_t s);
 hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream_t s);
 int colsum_chunks(int rows);
 int head_bwd_blocks(int rows);

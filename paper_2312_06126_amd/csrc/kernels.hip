@@ -45,6 +45,17 @@ __device__ inline double block_sum(double v, double* sh) {
   return r;
 }
 
+// Sum of an int over a 256-thread block (4 waves of 64 lanes).
+__device__ inline int block_sum_i32(int v, int* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+  __syncthreads();
+  const int r = sh[0] + sh[1] + sh[2] + sh[3];
+  __syncthreads();
+  return r;
+}
+
 // ------------------------------------------------------------------------------ replay
 // Copy `bytes` (a multiple of the element size) between 16-byte aligned segments,
 // 16 bytes per lane, the tail element by element.
@@ -245,11 +256,19 @@ __global__ void __launch_bounds__(256) k_head_bwd(HeadBwdArgs a) {
 constexpr int HB_ROWS = 64;
 __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
   extern __shared__ uint32_t wsh[];   // [K / 32][HB_ROWS], then [rpi][K] floats for the sums
+  __shared__ int src_row[HB_ROWS];    // product row of each dH row of the block, -1: zero row
   const int nw = a.K / 32, kv = a.K / 8, rpi = 256 / kv;
   const int r0 = blockIdx.x * HB_ROWS;
+  const int rows = a.m_dyn ? min(a.rows, *a.m_dyn) : a.rows;
+  if (r0 >= rows) return;
+  if (threadIdx.x < HB_ROWS) {
+    const int b = r0 + threadIdx.x;
+    src_row[threadIdx.x] = b < rows ? (a.map ? a.map[b] : b) : -1;
+  }
+  __syncthreads();
   for (int t = threadIdx.x; t < nw * HB_ROWS; t += blockDim.x) {
-    const int wc = t / HB_ROWS, r = t % HB_ROWS;
-    wsh[t] = r0 + r < a.rows ? a.bits[(int64_t)wc * a.ldbits + r0 + r] : 0u;
+    const int wc = t / HB_ROWS, src = src_row[t % HB_ROWS];
+    wsh[t] = src >= 0 ? a.bits[(int64_t)wc * a.ldbits + src] : 0u;
   }
   __syncthreads();
   const bf16_t* w = static_cast<const bf16_t*>(a.w);
@@ -260,8 +279,9 @@ __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
     const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
     for (int r = rs; r < HB_ROWS; r += rpi) {
       const int b = r0 + r;
-      if (b >= a.rows) break;
-      const float dq = bf2f(f2bf(a.dq[b]));
+      if (b >= rows) break;
+      const int src = src_row[r];
+      const float dq = src >= 0 ? bf2f(f2bf(a.dq[src])) : 0.0f;
       const uint32_t wd = wsh[(k >> 5) * HB_ROWS + r] >> (k & 31);
       uint32_t o[4];
 #pragma unroll
@@ -391,6 +411,78 @@ __global__ void __launch_bounds__(256) k_actor_loss(ActorLossArgs a) {
     a.part[blockIdx.x * 2 + 0] = l0;
     a.part[blockIdx.x * 2 + 1] = l1;
   }
+  if (a.cnt1) {
+    __shared__ int shi[4];
+    const int n1 = block_sum_i32(b < a.B && a.qp1[b] <= a.qp2[b] ? 1 : 0, shi);
+    if (threadIdx.x == 0) a.cnt1[blockIdx.x] = n1;
+  }
+}
+
+// Row split by the minimum critic, one row per thread over the actor loss's 256-row
+// blocks. A block's first list position is the count of critic-1 rows in the blocks
+// before it; within the block positions follow from a ballot prefix per wave and the
+// wave totals; a critic-2 row's position is its row index less the critic-1 rows
+// before it. Block 0 pads both lists and writes their padded lengths.
+__global__ void __launch_bounds__(256) k_minq_split(MinqSplitArgs a) {
+  __shared__ int sh[4];
+  __shared__ int wtot[4];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  int p = 0;
+  for (int i = t; i < (int)blockIdx.x; i += 256) p += a.cnt1[i];
+  p = block_sum_i32(p, sh);
+  const int b = blockIdx.x * 256 + t;
+  const bool valid = b < a.B;
+  const bool take1 = valid && a.qp1[b] <= a.qp2[b];
+  const unsigned long long m = __ballot(take1);
+  if (lane == 0) wtot[wave] = __popcll(m);
+  __syncthreads();
+  int pos1 = p + __popcll(m & ((1ull << lane) - 1ull));
+  for (int w = 0; w < wave; ++w) pos1 += wtot[w];
+  if (take1) a.map1[pos1] = b;
+  else if (valid) a.map2[b - pos1] = b;
+  if (blockIdx.x != 0) return;
+  int n1 = 0;
+  for (int i = t; i < (int)gridDim.x; i += 256) n1 += a.cnt1[i];
+  n1 = block_sum_i32(n1, sh);
+  const int n2 = a.B - n1;
+  const int m1 = min((n1 + 511) / 512 * 512, a.Bp), m2 = min((n2 + 511) / 512 * 512, a.Bp);
+  for (int i = n1 + t; i < m1; i += 256) a.map1[i] = -1;
+  for (int i = n2 + t; i < m2; i += 256) a.map2[i] = -1;
+  if (t == 0) {
+    a.rows[0] = m1;
+    a.rows[1] = m2;
+  }
+}
+
+// Thread: one row, RBG_WORDS consecutive words (blockIdx.y picks the word group), so
+// that each thread's loads are independent and the grid has enough blocks to keep
+// the loads in flight.
+constexpr int RBG_WORDS = 4;
+__global__ void __launch_bounds__(256) k_row_bits_gather(RowBitsGatherArgs a) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= a.rows || r >= *a.m_dyn) return;
+  const int src = a.map[r];
+  const uint32_t* __restrict__ in = a.src;
+  uint32_t* __restrict__ out = a.dst;
+  const int w0 = blockIdx.y * RBG_WORDS;
+  uint32_t v[RBG_WORDS];
+#pragma unroll
+  for (int i = 0; i < RBG_WORDS; ++i)
+    v[i] = src >= 0 && w0 + i < a.words ? in[(int64_t)(w0 + i) * a.ld + src] : 0u;
+#pragma unroll
+  for (int i = 0; i < RBG_WORDS; ++i)
+    if (w0 + i < a.words) out[(int64_t)(w0 + i) * a.ld + r] = v[i];
+}
+
+__global__ void __launch_bounds__(256) k_row_scatter(RowScatterArgs a) {
+  const int cv = a.cols / 4;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)a.rows * cv) return;
+  const int r = (int)(i / cv), j = (int)(i - (int64_t)r * cv) * 4;
+  if (r >= *a.m_dyn) return;
+  const int b = a.map[r];
+  if (b < 0) return;
+  *reinterpret_cast<float4*>(a.dst + (int64_t)b * a.ld + j) = *reinterpret_cast<const float4*>(a.src + (int64_t)r * a.ld + j);
 }
 
 // Actor head backward. SAC: g_u = da (1 - a^2) + (alpha/B) 2 a, d mu = g_u,
@@ -681,6 +773,7 @@ hipError_t launch_rowdot(bool bf16, const RowdotArgs& r, hipStream_t s) {
 hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s) {
   const int vec = bf16 ? 8 : 4;
   if (a.K % vec || a.ld % vec) return hipErrorInvalidValue;
+  if ((a.map || a.m_dyn) && (!a.bits || a.colpart)) return hipErrorInvalidValue;
   if (a.bits) {
     if (!bf16 || a.K % 32 || a.K / 8 > 256 || a.ldbits < a.rows) return hipErrorInvalidValue;
     const size_t lds = (size_t)(a.K / 32) * HB_ROWS * 4 + (a.colpart ? (size_t)(256 / (a.K / 8)) * a.K * 4 : 0);
@@ -718,7 +811,29 @@ hipError_t launch_critic_loss(const CriticLossArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 hipError_t launch_actor_loss(const ActorLossArgs& a, hipStream_t s) {
+  if (a.cnt1 && !a.qp2) return hipErrorInvalidValue;
   k_actor_loss<<<blocks(a.Bp, 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+hipError_t launch_minq_split(const MinqSplitArgs& a, hipStream_t s) {
+  if (a.Bp % 256 || a.B < 0 || a.B > a.Bp || !a.cnt1 || !a.qp1 || !a.qp2 || !a.map1 || !a.map2 || !a.rows)
+    return hipErrorInvalidValue;
+  if (!a.Bp) return hipSuccess;
+  k_minq_split<<<a.Bp / 256, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+hipError_t launch_row_bits_gather(const RowBitsGatherArgs& a, hipStream_t s) {
+  if (a.words < 0 || a.rows < 0 || a.ld < a.rows || !a.map || !a.m_dyn) return hipErrorInvalidValue;
+  if (!a.rows || !a.words) return hipSuccess;
+  k_row_bits_gather<<<dim3(blocks(a.rows, 256), blocks(a.words, RBG_WORDS)), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+hipError_t launch_row_scatter(const RowScatterArgs& a, hipStream_t s) {
+  if (a.cols % 4 || a.ld % 4 || a.cols > a.ld || a.rows < 0 || !a.map || !a.m_dyn ||
+      ((uintptr_t)a.src & 15) || ((uintptr_t)a.dst & 15))
+    return hipErrorInvalidValue;
+  if (!a.rows || !a.cols) return hipSuccess;
+  k_row_scatter<<<blocks((int64_t)a.rows * (a.cols / 4), 256), 256, 0, s>>>(a);
   return hipGetLastError();
 }
 hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream_t s) {

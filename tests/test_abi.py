@@ -44,7 +44,7 @@ def test_hparams_defaults_roundtrip_layout(lib):
     assert abs(hp.lr_actor - 3e-4) < 1e-10 and abs(hp.beta2 - 0.999) < 1e-7
     assert hp.learn_alpha == 1 and hp.log_std_min == -20.0 and hp.log_std_max == 2.0
     assert abs(hp.policy_noise - 0.2) < 1e-7 and hp.policy_delay == 2
-    assert hp.device == 0 and hp.n_streams == 2
+    assert hp.device == 0 and hp.n_streams == 2 and hp.ordering == 0 and hp.actor_row_split == 1
 
 
 def test_selector_table_matches_header(lib):

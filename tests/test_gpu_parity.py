@@ -310,6 +310,39 @@ def test_sequential_runs_on_one_stream_and_differs_from_snapshot():
     assert not np.array_equal(runs[0]["actor"], runs[2]["actor"])
 
 
+def _split_runs(w, rows, steps, tie=False):
+    from paper_2312_06126_amd import Spz
+    out = []
+    for split in (0, 1):
+        g = Spz(w.obs_dim, w.act_dim, w.hidden, w.batch, dict(w.hparams(), actor_row_split=split), 1)
+        g.buffer_push(*synth.workload_rows(w, 0, rows, 0))
+        if tie:
+            # Equal critics: min(Q1, Q2) is a tie on every row and all rows go to critic 1.
+            g.write_params("critic2", g.read_params("critic1"))
+        g.profile_enable(True, 4096)
+        g.update(steps)
+        names = {s["name"] for s in g.profile_read()}
+        assert ("minq_split" in names) == bool(split), names
+        out.append({k: g.read_params(k) for k in ("actor", "critic1", "critic2", "log_alpha")})
+        out[-1]["rec"] = g.read_losses(1, steps)
+        g.close()
+    return out
+
+
+@pytest.mark.parametrize("w,rows,steps,tie", [
+    (FUSED_BF16, 5000, 4, False), (FUSED_BF16_DEEP, 5000, 3, False), (SEQ_BF16, 5000, 3, False),
+    (FUSED_BF16, 5000, 1, True), (W["sac_large_bf16"].replace(batch=2560, capacity=20_000), 20_000, 2, False)],
+    ids=["fused", "deep", "sequential", "all_ties", "large_b2560"])
+def test_actor_row_split_bit_exact(w, rows, steps, tie):
+    """Each critic's gradient to the action taken only on the rows where it attains
+    min(Q1, Q2) (padded row lists, device-side row counts) gives exactly what taking
+    both critics over every row gives, including the all-ties case (one list empty)."""
+    log("row split %s" % w.name)
+    a, b = _split_runs(w, rows, steps, tie)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
 @pytest.mark.parametrize("w,created", [(RAGGED.replace(batch=600), 1000), (FUSED_BF16, 1000)],
                          ids=["fp32", "bf16_fused"])
 def test_set_batch_equals_created_batch_bit_exact(w, created):
