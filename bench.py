@@ -279,7 +279,9 @@ def main():
             whole_step=round(gemm_flops / SURVEY_STEPS / (elapsed_ms / steps / 1e3) / peak, 4),
             gemm_flops_per_step=gemm_flops / SURVEY_STEPS, peak_tflops=PEAK_TFLOPS[prec],
             note="gemm_kernels: GEMM flops / summed GEMM kernel time of the survey pass (events on every "
-                 "launch; concurrent streams overlap); whole_step: GEMM flops per step / timed ms per step")
+                 "launch; concurrent streams overlap); whole_step: GEMM flops per step / timed ms per step. "
+                 "Both leave out the row-restricted input-gradient products of the SAC actor path "
+                 "(gemm_dgrad_rows: a data-dependent number of rows, about half the batch per critic)")
         out["roofline"] = roofline(stats, prec)
         out["kernels"] = [dict(name=s["name"], M=s["M"], N=s["N"], K=s["K"], launches=s["launches"],
                                avg_ms=round(s["avg_ms"], 5), total_ms=round(s["total_ms"], 3))
