@@ -14,7 +14,8 @@ stays resident in HBM; nothing is transferred from the host in the timed region.
 
 Prints one JSON line (rank 0). Also reports the dominant kernel against its
 roofline (per-launch event timings taken by the library on the stream the kernel
-runs on, during the timed region, where only that kernel's launches carry events;
+runs on, during the timed region, where only that kernel's launches carry events,
+in every TIMED_STRIDE-th step;
 the kernel is picked, and the per-kernel table taken, in an untimed survey pass
 before) and the CPU oracle's rate on a bounded sample of the same workload.
 roofline.traffic (HBM bytes per launch) and roofline.mfma_busy (share of cycles the
@@ -40,6 +41,9 @@ PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense matrix peaks
 PEAK_HBM_GBS = 8000.0
 GEMMS = ("gemm_fwd", "gemm_dgrad", "gemm_wgrad")
 SURVEY_STEPS = 10   # untimed steps with every kernel launch timed (per-kernel table)
+# In the timed region the dominant kernel's launches carry events in every
+# TIMED_STRIDE-th step only (each event pair costs the GPU a few microseconds).
+TIMED_STRIDE = 8
 # Measured HBM traffic of the dominant kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
 # scaled by a plain copy of known size), valid while the kernel sources hash the same.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_fwd_1024_sac_large_bf16_traffic.txt")
@@ -123,6 +127,7 @@ def roofline(stats, prec: str):
     r["mfma_busy"] = profile_value(MFMA_FILE, r["kernel"], "mfma_busy") if top["name"] in GEMMS else None
     r["avg_launch_ms"] = round(top["avg_ms"], 5)
     r["launches"] = top["launches"]
+    r["timed_every_steps"] = TIMED_STRIDE
     r["per_launch"] = top["flops"] if top["name"] in GEMMS else top["bytes"]
     return r
 
@@ -240,8 +245,9 @@ def main():
         top = survey[0]
         g.profile_enable(True, reserve_launches=40 * steps)
         g.profile_only(top["name"], top["M"], top["N"], top["K"])
-        progress("survey %d steps; timing %s M=%d N=%d K=%d in the timed region" %
-                 (SURVEY_STEPS, top["name"], top["M"], top["N"], top["K"]))
+        g.profile_stride(TIMED_STRIDE)
+        progress("survey %d steps; timing %s M=%d N=%d K=%d in every %dth step of the timed region" %
+                 (SURVEY_STEPS, top["name"], top["M"], top["N"], top["K"], TIMED_STRIDE))
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()

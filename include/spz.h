@@ -280,6 +280,12 @@ int spz_profile_enable(spz_ctx* ctx, int32_t on, int64_t reserve_launches);
  * kept. `name` is copied. Errors: SPZ_EINVAL (NULL ctx). */
 int spz_profile_only(spz_ctx* ctx, const char* name, int32_t M, int32_t N, int32_t K);
 
+/* Time launches only in the update steps whose step number t (1-based, global) is a
+ * multiple of `stride` (1, the default: every step), so that a long timed run carries
+ * few events; launches outside update steps are timed as before. Applies to steps
+ * enqueued after the call. Errors: SPZ_EINVAL (NULL ctx, stride < 1). */
+int spz_profile_stride(spz_ctx* ctx, int32_t stride);
+
 /* One aggregated kernel shape. flops / bytes are the algorithmic work of one
  * launch (2*M*N*K for matrix products; bytes the kernel must move for the
  * memory-bound kernels, 0 when not meaningful). */

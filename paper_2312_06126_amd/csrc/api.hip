@@ -141,6 +141,8 @@ struct spz_ctx {
   bool prof = false;
   std::vector<ProfKey> pkeys;
   bool pf_on = false;           // time only launches of this family and shape
+  int pf_stride = 1;            // ... in update steps t with t % pf_stride == 0
+  bool pf_step = true;          // the step being enqueued is one of them
   std::string pf_name;
   int pf_M = 0, pf_N = 0, pf_K = 0;
   std::vector<ProfEv> pevs;
@@ -209,7 +211,9 @@ hipError_t prof_take(spz_ctx* c, hipEvent_t* e) {
 template <class F>
 hipError_t timed(spz_ctx* c, const char* name, int M, int N, int K, double flops, double bytes, hipStream_t s,
                  F&& f) {
-  if (!c->prof || (c->pf_on && (M != c->pf_M || N != c->pf_N || K != c->pf_K || c->pf_name != name))) return f();
+  if (!c->prof || !c->pf_step ||
+      (c->pf_on && (M != c->pf_M || N != c->pf_N || K != c->pf_K || c->pf_name != name)))
+    return f();
   hipEvent_t a, b;
   HK(prof_take(c, &a));
   HK(prof_take(c, &b));
@@ -653,6 +657,12 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
   const int64_t t = c->h_step + 1;
   const bool actor_step = !c->td3 || (t % c->hp.policy_delay == 0);
   const bool sequential = c->hp.ordering == SPZ_ORDER_SEQUENTIAL;
+  // Kernel timing of this step (profile stride); launches outside steps are timed as before.
+  struct StepTiming {
+    spz_ctx* c;
+    ~StepTiming() { c->pf_step = true; }
+  } step_timing{c};
+  c->pf_step = t % c->pf_stride == 0;
   GatherArgs g{c->buf, c->row_bytes, c->off_a, c->off_s2, c->off_r, c->off_d, c->O, c->A, c->Ka, c->Kc,
                c->B, c->seed, (uint32_t)c->size, c->d_step, c->xsa, c->xs2, c->xsp, c->r, c->d, c->idx};
   {
@@ -1533,6 +1543,13 @@ int spz_profile_enable(spz_ctx* c, int32_t on, int64_t reserve_launches) {
     }
     c->pevs.reserve((size_t)reserve_launches);
   }
+  return SPZ_OK;
+}
+
+int spz_profile_stride(spz_ctx* c, int32_t stride) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_profile_stride: NULL context");
+  if (stride < 1) return set_err(c, SPZ_EINVAL, "spz_profile_stride: stride < 1");
+  c->pf_stride = stride;
   return SPZ_OK;
 }
 

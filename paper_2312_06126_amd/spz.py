@@ -28,7 +28,7 @@ REC_WIDTH = 8
 EXPORTS = ["spz_hparams_default", "spz_create", "spz_destroy", "spz_buffer_push", "spz_buffer_size",
            "spz_update", "spz_synchronize", "spz_step", "spz_set_step", "spz_param_count",
            "spz_read_params", "spz_write_params", "spz_read_losses", "spz_debug_read", "spz_last_error",
-           "spz_profile_enable", "spz_profile_only", "spz_profile_read", "spz_set_batch", "spz_batch", "spz_autotune_batch",
+           "spz_profile_enable", "spz_profile_only", "spz_profile_stride", "spz_profile_read", "spz_set_batch", "spz_batch", "spz_autotune_batch",
            "spz_save", "spz_load", "spz_act", "spz_buffer_push_async"]
 
 
@@ -97,6 +97,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "spz_last_error": (ctypes.c_char_p, [P]),
         "spz_profile_enable": (ctypes.c_int, [P, ctypes.c_int32, ctypes.c_int64]),
         "spz_profile_only": (ctypes.c_int, [P, ctypes.c_char_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
+        "spz_profile_stride": (ctypes.c_int, [P, ctypes.c_int32]),
         "spz_profile_read": (ctypes.c_int, [P, ctypes.POINTER(KernelStat), ctypes.c_int32,
                                             ctypes.POINTER(ctypes.c_int32)]),
     }
@@ -263,6 +264,10 @@ class Spz:
     def profile_only(self, name=None, M: int = 0, N: int = 0, K: int = 0):
         """Time only launches of kernel family `name` with shape (M, N, K); None: all."""
         self._check(self.lib.spz_profile_only(self.ctx, name.encode() if name else None, int(M), int(N), int(K)))
+
+    def profile_stride(self, stride: int):
+        """Time launches only in update steps whose number is a multiple of stride."""
+        self._check(self.lib.spz_profile_stride(self.ctx, int(stride)))
 
     def profile_read(self, max_entries: int = 256):
         """Aggregated kernel timings: list of dicts sorted by total time (largest first)."""

@@ -65,5 +65,6 @@ def test_null_arguments_fail_cleanly(lib):
     assert not lib.spz_create(0, 2, h, 1, 8, ctypes.byref(hp), 1)
     assert b"dimensions" in lib.spz_last_error(None)
     assert lib.spz_update(None, 1, None) == spz.SPZ_EINVAL
+    assert lib.spz_profile_stride(None, 1) == spz.SPZ_EINVAL
     assert lib.spz_buffer_push(None, None, None, None, None, None, 0) == spz.SPZ_EINVAL
     assert lib.spz_param_count(None, 0) == spz.SPZ_EINVAL

@@ -295,6 +295,24 @@ def test_profile_only_times_one_kernel_and_keeps_results():
             assert np.array_equal(r[k], runs[0][k]), k
 
 
+def test_profile_stride_times_every_kth_step():
+    """With a profile stride of 3, only steps 3 and 6 of 7 carry timed launches."""
+    w = FUSED_BF16
+    g = make_gpu(w)
+    g.buffer_push(*synth.workload_rows(w, 0, 5000, 0))
+    g.profile_enable(True, 1000)
+    g.profile_stride(3)
+    g.update(7)
+    st = {s["name"]: s["launches"] for s in g.profile_read()}
+    g.profile_enable(True, 1000)
+    g.profile_stride(1)
+    g.update(1)
+    one = {s["name"]: s["launches"] for s in g.profile_read()}
+    g.close()
+    assert st["gather"] == 2 and st["finish"] == 2, st
+    assert st == {k: 2 * v for k, v in one.items()}, (st, one)
+
+
 def test_sequential_runs_on_one_stream_and_differs_from_snapshot():
     """The sequential ordering ignores the second stream (bit-identical runs) and
     moves the actor differently from the snapshot ordering."""
