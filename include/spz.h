@@ -76,8 +76,16 @@ typedef struct spz_ctx spz_ctx;
 #define SPZ_G_LOG_ALPHA 18
 #define SPZ_N_SELECTORS 19
 
-/* Selectors for spz_debug_read. */
-#define SPZ_DBG_INDICES 0 /* int32 [batch]: replay rows sampled by the last step */
+/* Selectors for spz_debug_read (per-row values of the last step, float32 unless
+ * noted; the actor-side values are those of the last step that updated the actor). */
+#define SPZ_DBG_INDICES 0   /* int32 [batch]: replay rows sampled by the last step     */
+#define SPZ_DBG_TD_TARGET 1 /* [batch]: TD target y                                   */
+#define SPZ_DBG_Q 2         /* [2, batch]: online critics q1, q2 on (s, a)            */
+#define SPZ_DBG_QPI 3       /* [2, batch]: critics 1, 2 on (s, a~) (TD3: critic 1 twice) */
+#define SPZ_DBG_LOGPI 4     /* [batch]: log pi of the actor sample (SAC only)         */
+#define SPZ_DBG_DACTION 5   /* [batch, act_dim]: gradient of the actor loss with respect
+                               to the actor's action a~ (Section 3.2.2's twin minimum
+                               for SAC, critic 1 for TD3)                              */
 
 /* Loss record of one step: 8 floats. */
 #define SPZ_REC_LQ 0        /* mean (q1-y)^2 + mean (q2-y)^2                      */

@@ -1512,13 +1512,49 @@ int spz_read_losses(spz_ctx* c, float* out, int64_t first_step, int32_t n) {
 
 int spz_debug_read(spz_ctx* c, int32_t what, void* out, int64_t bytes) {
   if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_debug_read: NULL context");
-  if (what != SPZ_DBG_INDICES) return set_err(c, SPZ_EINVAL, "spz_debug_read: bad selector");
-  if (bytes != (int64_t)c->B * 4) return set_err(c, SPZ_ESIZE, "spz_debug_read: size mismatch");
+  const int64_t B = c->B;
+  int64_t need = 0;
+  switch (what) {
+    case SPZ_DBG_INDICES: case SPZ_DBG_TD_TARGET: need = B * 4; break;
+    case SPZ_DBG_Q: case SPZ_DBG_QPI: need = 2 * B * 4; break;
+    case SPZ_DBG_LOGPI:
+      if (c->td3) return set_err(c, SPZ_EINVAL, "spz_debug_read: no log pi in TD3");
+      need = B * 4;
+      break;
+    case SPZ_DBG_DACTION: need = B * c->A * 4; break;
+    default: return set_err(c, SPZ_EINVAL, "spz_debug_read: bad selector");
+  }
+  if (bytes != need) return set_err(c, SPZ_ESIZE, "spz_debug_read: size mismatch");
   if (!out) return set_err(c, SPZ_EINVAL, "spz_debug_read: NULL out");
   CK(hipSetDevice(c->hp.device));
   int rc = ctx_sync(c);
   if (rc) return rc;
-  CK(hipMemcpy(out, c->idx, (size_t)bytes, hipMemcpyDeviceToHost));
+  float* f = static_cast<float*>(out);
+  switch (what) {
+    case SPZ_DBG_INDICES: CK(hipMemcpy(out, c->idx, (size_t)bytes, hipMemcpyDeviceToHost)); break;
+    case SPZ_DBG_TD_TARGET: CK(hipMemcpy(f, c->y, B * 4, hipMemcpyDeviceToHost)); break;
+    case SPZ_DBG_Q:
+      CK(hipMemcpy(f, c->q1, B * 4, hipMemcpyDeviceToHost));
+      CK(hipMemcpy(f + B, c->q2, B * 4, hipMemcpyDeviceToHost));
+      break;
+    case SPZ_DBG_QPI:
+      CK(hipMemcpy(f, c->qp1, B * 4, hipMemcpyDeviceToHost));
+      CK(hipMemcpy(f + B, c->td3 ? c->qp1 : c->qp2, B * 4, hipMemcpyDeviceToHost));
+      break;
+    case SPZ_DBG_LOGPI: CK(hipMemcpy(f, c->logp, B * 4, hipMemcpyDeviceToHost)); break;
+    case SPZ_DBG_DACTION: {
+      // da1 [Bp, Ap] holds the whole gradient under the SAC row split (and for TD3);
+      // otherwise critic 2's part is in da2.
+      const bool two = !c->td3 && !c->row_split;
+      std::vector<float> d1((size_t)B * c->Ap), d2(two ? (size_t)B * c->Ap : 0);
+      CK(hipMemcpy(d1.data(), c->da1, d1.size() * 4, hipMemcpyDeviceToHost));
+      if (two) CK(hipMemcpy(d2.data(), c->da2, d2.size() * 4, hipMemcpyDeviceToHost));
+      for (int64_t b = 0; b < B; ++b)
+        for (int j = 0; j < c->A; ++j)
+          f[b * c->A + j] = d1[b * c->Ap + j] + (two ? d2[b * c->Ap + j] : 0.0f);
+      break;
+    }
+  }
   return SPZ_OK;
 }
 

@@ -24,6 +24,8 @@ SELECTORS = {
     "g_actor": 15, "g_critic1": 16, "g_critic2": 17, "g_log_alpha": 18,
 }
 DBG_INDICES = 0
+# Per-row values of the last step: selector -> rows of the array (None: act_dim columns).
+DEBUG_ROWS = {"td_target": (1, 1), "q": (2, 2), "qpi": (3, 2), "logpi": (4, 1), "daction": (5, None)}
 REC_WIDTH = 8
 EXPORTS = ["spz_hparams_default", "spz_create", "spz_destroy", "spz_buffer_push", "spz_buffer_size",
            "spz_update", "spz_synchronize", "spz_step", "spz_set_step", "spz_param_count",
@@ -257,6 +259,14 @@ class Spz:
         self._check(self.lib.spz_debug_read(self.ctx, DBG_INDICES, out.ctypes.data_as(ctypes.c_void_p),
                                             out.nbytes))
         return out
+
+    def debug_rows(self, what: str) -> np.ndarray:
+        """Per-row float32 values of the last step: "td_target" [batch], "q" and "qpi"
+        [2, batch], "logpi" [batch], "daction" [batch, act_dim]."""
+        sel, n = DEBUG_ROWS[what]
+        out = np.empty((self.batch, self.act_dim) if n is None else (n, self.batch), np.float32)
+        self._check(self.lib.spz_debug_read(self.ctx, sel, out.ctypes.data_as(ctypes.c_void_p), out.nbytes))
+        return out[0] if n == 1 else out
 
     def profile_enable(self, on: bool = True, reserve_launches: int = 0):
         self._check(self.lib.spz_profile_enable(self.ctx, 1 if on else 0, int(reserve_launches)))

@@ -55,6 +55,14 @@ def test_selector_table_matches_header(lib):
         assert m and int(m.group(1)) == val, name
 
 
+def test_debug_selectors_match_header(lib):
+    from paper_2312_06126_amd import spz
+    text = open(HEADER).read()
+    for name, (val, _) in spz.DEBUG_ROWS.items():
+        m = re.search(r"#define SPZ_DBG_%s (\d+)" % name.upper(), text)
+        assert m and int(m.group(1)) == val, name
+
+
 def test_null_arguments_fail_cleanly(lib):
     """Argument validation happens before any device call."""
     from paper_2312_06126_amd import spz

@@ -104,6 +104,75 @@ def test_indices_bit_exact_full_size_large():
     g.close()
 
 
+def _rms_err(gpu, ref):
+    ref = np.asarray(ref, np.float64)
+    return float(np.max(np.abs(np.asarray(gpu, np.float64) - ref)) / max(np.sqrt(np.mean(ref * ref)), 1e-30))
+
+
+# Per-row values differ by bf16 rounding flips between fp32 and float64 accumulation:
+# a flipped operand moves a 1024-term dot product by about 1e-4 of its size. Forward
+# values see about one flip per net (observed max error / rms 3e-7 to 4e-5); the action
+# gradient goes through three rounded layers of dz, one flip per 1024 elements each, and
+# its max runs over 17 components per row (observed 1.8e-3). A dropped term, a wrong
+# sign or a wrong critic for a row gives errors of order 1.
+ROW_TOL_BF16 = 1e-3
+ROW_TOL_BF16_GRAD = 1e-2
+
+
+def test_full_size_sampled_rows_large():
+    """The large workload at full size and in bench's launch configuration (batch 131072,
+    3x1024, bf16 operands, one stream, actor row split): after 3 steps the oracle takes
+    the GPU's state, and step 4's per-row values (TD target, q1, q2, the critics on
+    (s, a~), log pi, the actor loss's gradient to the action) are checked on 96 sampled
+    rows, each computed by the oracle on those rows alone."""
+    from oracle.nets import forward
+    from oracle.update import tanh_gaussian
+    from .helpers import fill_rows, state_keys
+    rows = 200_000
+    w = W["sac_large_bf16"].replace(capacity=rows)
+    log("sampled rows sac_large_bf16 full size")
+    g = make_gpu(w, n_streams=1)
+    fill_rows(w, rows, 0, [g.buffer_push])
+    g.update(3)
+    o = make_oracle(w, virtual_rows=rows)
+    for k in state_keys(o.algo):
+        o.set_params(k, g.read_params(k).astype(np.float64))
+    g.update(1)
+    t, B, A = 4, w.batch, w.act_dim
+    idx = philox.indices(1, t, B, rows)
+    assert np.array_equal(g.debug_indices(), idx.astype(np.int32))
+    got = {k: g.debug_rows(k) for k in ("td_target", "q", "qpi", "logpi", "daction")}
+    g.close()
+
+    R = np.sort(np.random.default_rng(5).choice(B, 96, replace=False))
+    s, a, r, d, s2 = o._gather(idx[R])
+    eps_tgt = philox.normals(1, t, philox.PURPOSE_NOISE_TGT, B * A).reshape(B, A)[R]
+    eps_pol = philox.normals(1, t, philox.PURPOSE_NOISE_POL, B * A).reshape(B, A)[R]
+    alpha = float(np.exp(o.log_alpha[0]))
+    y, _ = o.sac_target(s2, r, d, eps_tgt, alpha)
+    x = np.concatenate([s, a], axis=1)
+    q = [forward(o.net[k], x, o.rnd)[0][:, 0] for k in ("critic1", "critic2")]
+    z, _ = forward(o.net["actor"], s, o.rnd)
+    pol = tanh_gaussian(z, eps_pol, A, w.log_std_min, w.log_std_max)
+    xa = np.concatenate([s, pol["a"]], axis=1)
+    qp = [forward(o.net[k], xa, o.rnd)[0][:, 0] for k in ("critic1", "critic2")]
+    # The minimum critic is a floating-point decision: take the GPU's, and check that the
+    # oracle's own agrees wherever the two values are not within the bar of each other.
+    take1 = got["qpi"][0][R] <= got["qpi"][1][R]
+    close = np.abs(qp[0] - qp[1]) <= 2 * ROW_TOL_BF16 * np.sqrt(np.mean(qp[0] ** 2))
+    assert np.all((take1 == (qp[0] <= qp[1])) | close)
+    assert 0 < take1.sum() < len(R)
+    da = o._critic_action_grad(s, pol["a"], {"critic1": np.where(take1, -1.0 / B, 0.0),
+                                             "critic2": np.where(take1, 0.0, -1.0 / B)})
+    errs = {"td_target": _rms_err(got["td_target"][R], y),
+            "q1": _rms_err(got["q"][0][R], q[0]), "q2": _rms_err(got["q"][1][R], q[1]),
+            "qpi1": _rms_err(got["qpi"][0][R], qp[0]), "qpi2": _rms_err(got["qpi"][1][R], qp[1]),
+            "logpi": _rms_err(got["logpi"][R], pol["logp"]), "daction": _rms_err(got["daction"][R], da)}
+    log("  per-row max error / rms: " + " ".join("%s %.2e" % kv for kv in errs.items()))
+    for k, e in errs.items():
+        assert e <= (ROW_TOL_BF16_GRAD if k == "daction" else ROW_TOL_BF16), (k, e)
+
+
 # ---------------------------------------------------------------------------- teacher-forced steps
 def teacher_forced(w, n_rows, steps_before=0, virtual=False, tol_grad=FP32_TOL, tol_loss=FP32_TOL,
                    n_steps=1):
