@@ -119,18 +119,23 @@ ROW_TOL_BF16 = 1e-3
 ROW_TOL_BF16_GRAD = 1e-2
 
 
-def test_full_size_sampled_rows_large():
-    """The large workload at full size and in bench's launch configuration (batch 131072,
-    3x1024, bf16 operands, one stream, actor row split): after 3 steps the oracle takes
-    the GPU's state, and step 4's per-row values (TD target, q1, q2, the critics on
-    (s, a~), log pi, the actor loss's gradient to the action) are checked on 96 sampled
-    rows, each computed by the oracle on those rows alone."""
+@pytest.mark.parametrize("name", ["sac_large_bf16", "td3_ant"])
+def test_full_size_sampled_rows(name):
+    """A workload at its full batch and widths, in bench's launch configuration (one
+    stream; for SAC the actor row split): after 3 steps the oracle takes the GPU's
+    state, and step 4's per-row values (TD target, q1, q2, the critics on (s, a~),
+    log pi, the actor loss's gradient to the action) are checked on 96 sampled rows,
+    each computed by the oracle on those rows alone. The ring holds 200000 rows (the
+    ring size only changes which rows are drawn)."""
     from oracle.nets import forward
     from oracle.update import tanh_gaussian
     from .helpers import fill_rows, state_keys
     rows = 200_000
-    w = W["sac_large_bf16"].replace(capacity=rows)
-    log("sampled rows sac_large_bf16 full size")
+    w = W[name].replace(capacity=rows)
+    sac = w.algo == "sac"
+    tol = ROW_TOL_BF16 if w.prec == "bf16" else FP32_TOL
+    tol_grad = ROW_TOL_BF16_GRAD if w.prec == "bf16" else FP32_TOL
+    log("sampled rows %s full size" % name)
     g = make_gpu(w, n_streams=1)
     fill_rows(w, rows, 0, [g.buffer_push])
     g.update(3)
@@ -141,36 +146,46 @@ def test_full_size_sampled_rows_large():
     t, B, A = 4, w.batch, w.act_dim
     idx = philox.indices(1, t, B, rows)
     assert np.array_equal(g.debug_indices(), idx.astype(np.int32))
-    got = {k: g.debug_rows(k) for k in ("td_target", "q", "qpi", "logpi", "daction")}
+    got = {k: g.debug_rows(k) for k in ("td_target", "q", "qpi", "daction") + (("logpi",) if sac else ())}
     g.close()
 
     R = np.sort(np.random.default_rng(5).choice(B, 96, replace=False))
     s, a, r, d, s2 = o._gather(idx[R])
     eps_tgt = philox.normals(1, t, philox.PURPOSE_NOISE_TGT, B * A).reshape(B, A)[R]
-    eps_pol = philox.normals(1, t, philox.PURPOSE_NOISE_POL, B * A).reshape(B, A)[R]
-    alpha = float(np.exp(o.log_alpha[0]))
-    y, _ = o.sac_target(s2, r, d, eps_tgt, alpha)
     x = np.concatenate([s, a], axis=1)
     q = [forward(o.net[k], x, o.rnd)[0][:, 0] for k in ("critic1", "critic2")]
     z, _ = forward(o.net["actor"], s, o.rnd)
-    pol = tanh_gaussian(z, eps_pol, A, w.log_std_min, w.log_std_max)
-    xa = np.concatenate([s, pol["a"]], axis=1)
+    ref = {}
+    if sac:
+        alpha = float(np.exp(o.log_alpha[0]))
+        y, _ = o.sac_target(s2, r, d, eps_tgt, alpha)
+        eps_pol = philox.normals(1, t, philox.PURPOSE_NOISE_POL, B * A).reshape(B, A)[R]
+        pol = tanh_gaussian(z, eps_pol, A, w.log_std_min, w.log_std_max)
+        a_pi = pol["a"]
+        ref["logpi"] = (got["logpi"][R], pol["logp"])
+    else:
+        y, _ = o.td3_target(s2, r, d, eps_tgt)
+        a_pi = np.tanh(z)
+    xa = np.concatenate([s, a_pi], axis=1)
     qp = [forward(o.net[k], xa, o.rnd)[0][:, 0] for k in ("critic1", "critic2")]
-    # The minimum critic is a floating-point decision: take the GPU's, and check that the
-    # oracle's own agrees wherever the two values are not within the bar of each other.
-    take1 = got["qpi"][0][R] <= got["qpi"][1][R]
-    close = np.abs(qp[0] - qp[1]) <= 2 * ROW_TOL_BF16 * np.sqrt(np.mean(qp[0] ** 2))
-    assert np.all((take1 == (qp[0] <= qp[1])) | close)
-    assert 0 < take1.sum() < len(R)
-    da = o._critic_action_grad(s, pol["a"], {"critic1": np.where(take1, -1.0 / B, 0.0),
-                                             "critic2": np.where(take1, 0.0, -1.0 / B)})
-    errs = {"td_target": _rms_err(got["td_target"][R], y),
-            "q1": _rms_err(got["q"][0][R], q[0]), "q2": _rms_err(got["q"][1][R], q[1]),
-            "qpi1": _rms_err(got["qpi"][0][R], qp[0]), "qpi2": _rms_err(got["qpi"][1][R], qp[1]),
-            "logpi": _rms_err(got["logpi"][R], pol["logp"]), "daction": _rms_err(got["daction"][R], da)}
+    if sac:
+        # The minimum critic is a floating-point decision: take the GPU's, and check that
+        # the oracle's own agrees wherever the two values are not within the bar.
+        take1 = got["qpi"][0][R] <= got["qpi"][1][R]
+        close = np.abs(qp[0] - qp[1]) <= 2 * tol * np.sqrt(np.mean(qp[0] ** 2))
+        assert np.all((take1 == (qp[0] <= qp[1])) | close)
+        assert 0 < take1.sum() < len(R)
+        dq = {"critic1": np.where(take1, -1.0 / B, 0.0), "critic2": np.where(take1, 0.0, -1.0 / B)}
+        ref["qpi2"] = (got["qpi"][1][R], qp[1])
+    else:
+        dq = {"critic1": np.full(len(R), -1.0 / B)}
+    da = o._critic_action_grad(s, a_pi, dq)
+    ref.update(td_target=(got["td_target"][R], y), q1=(got["q"][0][R], q[0]), q2=(got["q"][1][R], q[1]),
+               qpi1=(got["qpi"][0][R], qp[0]), daction=(got["daction"][R], da))
+    errs = {k: _rms_err(gv, rv) for k, (gv, rv) in ref.items()}
     log("  per-row max error / rms: " + " ".join("%s %.2e" % kv for kv in errs.items()))
     for k, e in errs.items():
-        assert e <= (ROW_TOL_BF16_GRAD if k == "daction" else ROW_TOL_BF16), (k, e)
+        assert e <= (tol_grad if k == "daction" else tol), (k, e)
 
 
 # ---------------------------------------------------------------------------- teacher-forced steps
