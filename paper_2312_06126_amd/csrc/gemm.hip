@@ -236,6 +236,37 @@ __global__ void k_splitk_reduce(const float* __restrict__ part, int splits, int 
   *reinterpret_cast<float4*>(out + (int64_t)m * ldo + n) = s;
 }
 
+// The same for small outputs with many slices: RG_GROUPS threads per 16-byte output
+// piece take every RG_GROUPS-th slice, and the group sums are added in group order
+// (a fixed order, as above), so the grid has RG_GROUPS times more threads.
+constexpr int RG_GROUPS = 8;
+__global__ void __launch_bounds__(256) k_splitk_reduce_grouped(const float* __restrict__ part, int splits, int M,
+                                                               int N, int64_t ldc, float* __restrict__ out,
+                                                               int64_t ldo) {
+  constexpr int COLS = 256 / RG_GROUPS;
+  __shared__ float4 sh[RG_GROUPS][COLS];
+  const int nv = N / 4, grp = threadIdx.x / COLS, col = threadIdx.x % COLS;
+  const int64_t i = (int64_t)blockIdx.x * COLS + col;
+  const bool valid = i < (int64_t)M * nv;
+  const int m = valid ? (int)(i / nv) : 0, n = valid ? (int)(i % nv) * 4 : 0;
+  float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  if (valid) {
+    for (int z = grp; z < splits; z += RG_GROUPS) {
+      const float4 v = *reinterpret_cast<const float4*>(part + ((int64_t)z * M + m) * ldc + n);
+      s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
+  }
+  sh[grp][col] = s;
+  __syncthreads();
+  if (grp != 0 || !valid) return;
+#pragma unroll
+  for (int q = 1; q < RG_GROUPS; ++q) {
+    const float4 v = sh[q][col];
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  *reinterpret_cast<float4*>(out + (int64_t)m * ldo + n) = s;
+}
+
 int pick_tile(int n) { return n % 128 == 0 ? 128 : n % 64 == 0 ? 64 : n % 32 == 0 ? 32 : 0; }
 
 template <typename T, int MODE, int BM, int BN>
@@ -359,6 +390,12 @@ hipError_t splitk_reduce(const float* part, int splits, int M, int N, int64_t ld
                          int64_t ldo, hipStream_t s) {
   if (N % 4 || ldc % 4 || ldo % 4) return hipErrorInvalidValue;
   const int64_t n = (int64_t)M * (N / 4);
+  // Small outputs (under 64K 16-byte pieces) from many slices: split the slices too.
+  if (n < 4 * 256 * 64 && splits >= 4 * RG_GROUPS) {
+    constexpr int COLS = 256 / RG_GROUPS;
+    k_splitk_reduce_grouped<<<(unsigned)((n + COLS - 1) / COLS), 256, 0, s>>>(part, splits, M, N, ldc, out, ldo);
+    return hipGetLastError();
+  }
   k_splitk_reduce<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, splits, M, N, ldc, out, ldo);
   return hipGetLastError();
 }

@@ -100,7 +100,9 @@ def test_dgrad_bf16(env, M, N, K, masked):
 
 @pytest.mark.parametrize("M,N,K,splits", [(256, 256, 512, 1), (512, 1024, 2048, 4), (1024, 416, 1024, 2),
                                           (1024, 384, 512, 2), (64, 1024, 1024, 4), (256, 128, 256, 1),
-                                          (256, 160, 512, 2), (512, 264, 256, 1)])
+                                          (256, 160, 512, 2), (512, 264, 256, 1),
+                                          # many slices of a small output: grouped slice reduction
+                                          (64, 1024, 8192, 32), (128, 96, 5120, 40)])
 def test_wgrad_bf16(env, M, N, K, splits):
     run(env, True, 2, M, N, K, splits=splits)
 
