@@ -57,17 +57,19 @@ __device__ inline int block_sum_i32(int v, int* sh) {
 }
 
 // ------------------------------------------------------------------------------ replay
-// Copy `bytes` (a multiple of the element size) between 16-byte aligned segments,
-// 16 bytes per lane, the tail element by element.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Elements of a segment past its whole 16-byte pieces.
 template <typename T>
-__device__ inline void copy_seg(uint8_t* dst, const uint8_t* src, int bytes, int lane) {
-  const int nv = bytes >> 4;
-  for (int v = lane; v < nv; v += 64)
-    reinterpret_cast<uint4*>(dst)[v] = reinterpret_cast<const uint4*>(src)[v];
-  for (int e = (nv << 4) / (int)sizeof(T) + lane; e < bytes / (int)sizeof(T); e += 64)
+__device__ inline void copy_tail(uint8_t* dst, const uint8_t* src, int bytes, int lane) {
+  for (int e = ((bytes >> 4) << 4) / (int)sizeof(T) + lane; e < bytes / (int)sizeof(T); e += 64)
     reinterpret_cast<T*>(dst)[e] = reinterpret_cast<const T*>(src)[e];
 }
 
+// One wave per batch row. The ring row is read once: each lane loads its 16-byte
+// pieces of s, s' and a before any store, then s goes to both critic and actor
+// operands. (Non-temporal loads of data the previous kernel wrote gave wrong sums in
+// the column-sum kernel, so loads here stay plain.)
 template <typename T>
 __global__ void __launch_bounds__(256) k_gather(GatherArgs g) {
   const int lane = threadIdx.x & 63;
@@ -81,14 +83,42 @@ __global__ void __launch_bounds__(256) k_gather(GatherArgs g) {
   uint8_t* xsa = static_cast<uint8_t*>(g.xsa) + xrow;
   uint8_t* xsp = static_cast<uint8_t*>(g.xsp) + xrow;
   uint8_t* xs2 = static_cast<uint8_t*>(g.xs2) + xrow;
-  const int sb = g.O * (int)sizeof(T);
-  copy_seg<T>(xsa, src, sb, lane);
-  copy_seg<T>(xsp, src, sb, lane);
-  copy_seg<T>(xs2, src + g.off_s2, sb, lane);
-  copy_seg<T>(xsa + g.Ka * (int)sizeof(T), src + g.off_a, g.A * (int)sizeof(T), lane);
+  const int sb = g.O * (int)sizeof(T), ab = g.A * (int)sizeof(T);
+  const int ns = sb >> 4, na = ab >> 4;
+  const u32x4* __restrict__ s_in = reinterpret_cast<const u32x4*>(src);
+  const u32x4* __restrict__ s2_in = reinterpret_cast<const u32x4*>(src + g.off_s2);
+  const u32x4* __restrict__ a_in = reinterpret_cast<const u32x4*>(src + g.off_a);
+  u32x4* __restrict__ xsa4 = reinterpret_cast<u32x4*>(xsa);
+  u32x4* __restrict__ xsp4 = reinterpret_cast<u32x4*>(xsp);
+  u32x4* __restrict__ xs24 = reinterpret_cast<u32x4*>(xs2);
+  u32x4* __restrict__ xa4 = reinterpret_cast<u32x4*>(xsa + g.Ka * (int)sizeof(T));
+  float rv = 0.0f, dv = 0.0f;
   if (lane == 0) {
-    g.r[b] = *reinterpret_cast<const float*>(src + g.off_r);
-    g.d[b] = *reinterpret_cast<const float*>(src + g.off_d);
+    rv = *reinterpret_cast<const float*>(src + g.off_r);
+    dv = *reinterpret_cast<const float*>(src + g.off_d);
+  }
+  const int nmax = ns > na ? ns : na;
+  for (int v = lane; v < nmax; v += 64) {
+    u32x4 x = {0u, 0u, 0u, 0u}, y = x, z = x;
+    if (v < ns) {
+      x = s_in[v];
+      y = s2_in[v];
+    }
+    if (v < na) z = a_in[v];
+    if (v < ns) {
+      xsa4[v] = x;
+      xsp4[v] = x;
+      xs24[v] = y;
+    }
+    if (v < na) xa4[v] = z;
+  }
+  copy_tail<T>(xsa, src, sb, lane);
+  copy_tail<T>(xsp, src, sb, lane);
+  copy_tail<T>(xs2, src + g.off_s2, sb, lane);
+  copy_tail<T>(xsa + g.Ka * (int)sizeof(T), src + g.off_a, ab, lane);
+  if (lane == 0) {
+    g.r[b] = rv;
+    g.d[b] = dv;
     g.idx[b] = (int32_t)row;
   }
 }
