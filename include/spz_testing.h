@@ -47,6 +47,16 @@ int spzt_gemm_fused(int32_t mode, int32_t M, int32_t N, int32_t K, const void* A
                     int64_t ldb, void* C, int64_t ldc, const float* bias, uint32_t* bits_out, const uint32_t* bits,
                     int64_t ldbits, const void* rdot_w, float* rdot_part, int64_t ldrd, int32_t no_store,
                     float* colsum, int64_t ldcs);
+/*
+ * Input-gradient product C = (A . B) [* bit(r, c) with bits] restricted to the first
+ * m_rows rows by a device-side row count (the form the library's SAC actor row split
+ * uses; m_rows a multiple of 256, at most M): rows from m_rows on are not written.
+ * Same operand conventions as spzt_gemm mode 1 (bf16 builds B's transposed image).
+ * Synchronous.
+ */
+int spzt_gemm_dgrad_rows(int32_t bf16, int32_t M, int32_t N, int32_t K, const void* A, int64_t lda,
+                         const void* B, int64_t ldb, void* C, int64_t ldc, const uint32_t* bits, int64_t ldbits,
+                         int32_t out_f32, int32_t m_rows);
 /* Columns per row-dot partial of an N-column product. */
 int spzt_rdot_cols(int32_t N);
 /*

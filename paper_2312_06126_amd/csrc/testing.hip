@@ -89,6 +89,32 @@ extern "C" int spzt_gemm_fused(int32_t mode, int32_t M, int32_t N, int32_t K, co
   return e == hipSuccess ? SPZ_OK : SPZ_EHIP;
 }
 
+extern "C" int spzt_gemm_dgrad_rows(int32_t bf16, int32_t M, int32_t N, int32_t K, const void* A, int64_t lda,
+                                    const void* B, int64_t ldb, void* C, int64_t ldc, const uint32_t* bits,
+                                    int64_t ldbits, int32_t out_f32, int32_t m_rows) {
+  if (!A || !B || !C || m_rows < 0 || m_rows > M || m_rows % 256) return SPZ_EINVAL;
+  GemmArgs g{};
+  g.A = A; g.lda = lda; g.B = B; g.ldb = ldb; g.C = C; g.ldc = ldc;
+  g.M = M; g.N = N; g.K = K; g.out_f32 = out_f32;
+  g.bits = bits; g.ldbits = ldbits;
+  int32_t* rows = nullptr;
+  bf16_t* bt = nullptr;
+  hipError_t e = hipMalloc(reinterpret_cast<void**>(&rows), sizeof(int32_t));
+  if (e != hipSuccess) return SPZ_ENOMEM;
+  e = hipMemcpy(rows, &m_rows, sizeof(int32_t), hipMemcpyHostToDevice);
+  g.m_dyn = rows;
+  if (e == hipSuccess && bf16 && (e = make_bt(B, ldb, K, N, &bt)) == hipSuccess) {
+    g.Bt = bt;
+    g.ldbt = K;
+  }
+  if (e == hipSuccess) e = gemm(bf16 != 0, GEMM_DGRAD, g, nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (bt) (void)hipFree(bt);
+  (void)hipFree(rows);
+  if (e == hipErrorInvalidValue) return SPZ_EINVAL;
+  return e == hipSuccess ? SPZ_OK : SPZ_EHIP;
+}
+
 extern "C" int spzt_rdot_cols(int32_t N) { return gemm_rdot_cols(N); }
 
 // Rounding check of the device float32 -> bfloat16 conversion against an integer

@@ -258,3 +258,46 @@ def test_bf16_rounding_exhaustive(env):
     bad = ctypes.c_uint64(0)
     assert lib.spzt_bf16_round_check(0, 1 << 32, ctypes.byref(bad)) == 0
     assert bad.value == 0, bad.value
+
+
+# ----------------------------------------------------------------------------- device-side row count
+@pytest.mark.parametrize("bf16,M,N,K,bits,out_f32", [(True, 1024, 256, 512, True, False),
+                                                      (True, 1024, 1024, 256, True, False),
+                                                      (True, 1024, 128, 256, False, True),
+                                                      (True, 1024, 32, 1024, False, True),
+                                                      (False, 512, 64, 128, False, True)],
+                         ids=["large_bits", "large_bits_n1024", "large_f32", "generic_n32", "fp32"])
+def test_dgrad_device_row_count(env, bf16, M, N, K, bits, out_f32):
+    """An input-gradient product limited to the first m rows by a device-side count
+    gives exactly the rows of the unlimited product and leaves the other rows as they
+    were (m = 0, a middle multiple of 256, M); a count that is not a multiple of 256
+    is refused."""
+    torch, _ = env
+    from paper_2312_06126_amd import spz
+    lib = spz.load()
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    f = lib.spzt_gemm_dgrad_rows
+    f.argtypes = [I32, I32, I32, I32, P, I64, P, I64, P, I64, P, I64, I32, I32]
+    f.restype = ctypes.c_int
+    rng = np.random.default_rng(M + N + K)
+    dA = to_dev(torch, rng.standard_normal((M, K)), bf16)
+    dB = to_dev(torch, rng.standard_normal((K, N)), bf16)
+    dbits = (torch.from_numpy(rng.integers(0, 1 << 32, size=(N // 32, M), dtype=np.uint64).astype(np.uint32)
+                              .view(np.int32)).cuda() if bits else None)
+    ctype = torch.float32 if (out_f32 or not bf16) else torch.bfloat16
+    outs = {}
+    for m in (M, 0, 256 if M > 256 else 0, M // 2):
+        dC = torch.full((M, N), 3.0, dtype=ctype, device="cuda")
+        torch.cuda.synchronize()
+        rc = f(int(bf16), M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, dC.data_ptr(), N,
+               dbits.data_ptr() if bits else None, M, int(out_f32), m)
+        assert rc == 0, (m, rc)
+        outs[m] = dC.to(torch.float64).cpu().numpy()
+    full = outs[M]
+    assert not np.all(full == 3.0)
+    for m, got in outs.items():
+        assert np.array_equal(got[:m], full[:m]), m
+        assert np.all(got[m:] == 3.0), m
+    dC = torch.zeros((M, N), dtype=ctype, device="cuda")
+    assert f(int(bf16), M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, dC.data_ptr(), N,
+             dbits.data_ptr() if bits else None, M, int(out_f32), 128) == spz.SPZ_EINVAL
