@@ -20,7 +20,8 @@
 //   critic stream: target action, target critics, TD target, online critics,
 //                  critic loss, critic backward (weight and bias gradients)
 //   actor stream:  actor forward on s, critics on (s, a~), actor loss, critic
-//                  input-gradient to the action, head backward, actor backward
+//                  input-gradient to the action (SAC: each critic on the rows where
+//                  it attains min(Q1, Q2)), head backward, actor backward
 //   s0: join -> finish (loss record, temperature gradient, step counter) -> Adam + Polyak
 // Sequential ordering (the published algorithms' order) runs everything on s0 and
 // moves the critics' Adam + Polyak between the critic part and the actor part.
