@@ -433,8 +433,10 @@ def _split_runs(w, rows, steps, tie=False):
 
 @pytest.mark.parametrize("w,rows,steps,tie", [
     (FUSED_BF16, 5000, 4, False), (FUSED_BF16_DEEP, 5000, 3, False), (SEQ_BF16, 5000, 3, False),
-    (FUSED_BF16, 5000, 1, True), (W["sac_large_bf16"].replace(batch=2560, capacity=20_000), 20_000, 2, False)],
-    ids=["fused", "deep", "sequential", "all_ties", "large_b2560"])
+    (FUSED_BF16, 5000, 1, True), (W["sac_large_bf16"].replace(batch=2560, capacity=20_000), 20_000, 2, False),
+    # one row (one list empty); all 700 rows to critic 1 (padded length capped at Bp = 768)
+    (FUSED_BF16.replace(batch=1), 1000, 3, False), (FUSED_BF16.replace(batch=700), 5000, 1, True)],
+    ids=["fused", "deep", "sequential", "all_ties", "large_b2560", "batch1", "ties_b700_cap"])
 def test_actor_row_split_bit_exact(w, rows, steps, tie):
     """Each critic's gradient to the action taken only on the rows where it attains
     min(Q1, Q2) (padded row lists, device-side row counts) gives exactly what taking
