@@ -100,6 +100,10 @@ struct spz_ctx {
   int64_t rec_cap = 65536;
   // batch
   void *xsa = nullptr, *xs2 = nullptr, *xsp = nullptr;
+  // Critic input of the actor part in the step being enqueued: xsp when the two parts
+  // run on concurrent streams; xsa itself (action columns overwritten by the actor's
+  // sample) when they run in order on one stream and the critic part is done with it.
+  void* xs_act = nullptr;
   float *r = nullptr, *d = nullptr;
   int32_t* idx = nullptr;
   // critic-stream workspace
@@ -592,15 +596,15 @@ hipError_t actor_part(spz_ctx* c, hipStream_t s) {
   HK(forward(c, 0, false, c->xsa, c->Kc, c->ha.data(), c->bha.data(), true, nullptr, c->z, s));
   if (!c->td3) {
     SacHeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_POL, hp.log_std_min, hp.log_std_max,
-                  c->xsp, c->Kc, c->Ka, c->logp, c->th, c->se, c->lm};
+                  c->xs_act, c->Kc, c->Ka, c->logp, c->th, c->se, c->lm};
     HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, h, s); }));
   } else {
-    Td3HeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, 0, 0.0f, 0.0f, c->xsp, c->Kc, c->Ka, c->th};
+    Td3HeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, 0, 0.0f, 0.0f, c->xs_act, c->Kc, c->Ka, c->th};
     HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
-  HK(forward(c, 1, false, c->xsp, c->Kc, c->hpc[0].data(), c->bhpc[0].data(), false, c->a_rdot, c->qp1, s));
+  HK(forward(c, 1, false, c->xs_act, c->Kc, c->hpc[0].data(), c->bhpc[0].data(), false, c->a_rdot, c->qp1, s));
   if (!c->td3)
-    HK(forward(c, 2, false, c->xsp, c->Kc, c->hpc[1].data(), c->bhpc[1].data(), false, c->a_rdot, c->qp2, s));
+    HK(forward(c, 2, false, c->xs_act, c->Kc, c->hpc[1].data(), c->bhpc[1].data(), false, c->a_rdot, c->qp2, s));
   ActorLossArgs al{c->qp1, c->td3 ? nullptr : c->qp2, c->logp, log_alpha_ptr(c), c->dqp1,
                    c->td3 ? nullptr : c->dqp2, c->a_lpart, c->B, c->Bp, c->row_split ? c->rcnt : nullptr};
   HK(timed(c, "actor_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_actor_loss(al, s); }));
@@ -664,15 +668,17 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
     ~StepTiming() { c->pf_step = true; }
   } step_timing{c};
   c->pf_step = t % c->pf_stride == 0;
+  const bool two = c->hp.n_streams == 2 && !sequential;
+  c->xs_act = two ? c->xsp : c->xsa;
   GatherArgs g{c->buf, c->row_bytes, c->off_a, c->off_s2, c->off_r, c->off_d, c->O, c->A, c->Ka, c->Kc,
-               c->B, c->seed, (uint32_t)c->size, c->d_step, c->xsa, c->xs2, c->xsp, c->r, c->d, c->idx};
+               c->B, c->seed, (uint32_t)c->size, c->d_step, c->xsa, c->xs2, two ? c->xsp : nullptr, c->r, c->d,
+               c->idx};
   {
     const double e = (double)es(c);
     const double bytes = (double)c->B * ((2.0 * c->O + c->A) * e + 8.0 + (3.0 * c->O + c->A) * e + 12.0);
     CK(timed(c, "gather", c->B, c->O, c->A, 0.0, bytes, s0, [&] { return launch_gather(c->bf16, g, s0); }));
   }
   hipStream_t sc = s0, sa = s0;
-  const bool two = c->hp.n_streams == 2 && !sequential;
   if (two) {
     CK(hipEventRecord(c->ev_fork, s0));
     CK(hipStreamWaitEvent(c->sc, c->ev_fork, 0));

@@ -12,7 +12,7 @@ struct GatherArgs {
   int off_a, off_s2, off_r, off_d;   // byte offsets inside a ring row (obs at 0)
   int O, A, Ka, Kc, B;
   uint64_t seed; uint32_t size; const int64_t* step;
-  void* xsa; void* xs2; void* xsp;   // [Bp, Kc] operand tensors
+  void* xsa; void* xs2; void* xsp;   // [Bp, Kc] operand tensors (xsp may be null: not written)
   float* r; float* d; int32_t* idx;
 };
 

@@ -67,8 +67,8 @@ __device__ inline void copy_tail(uint8_t* dst, const uint8_t* src, int bytes, in
 }
 
 // One wave per batch row. The ring row is read once: each lane loads its 16-byte
-// pieces of s, s' and a before any store, then s goes to both critic and actor
-// operands. (Non-temporal loads of data the previous kernel wrote gave wrong sums in
+// pieces of s, s' and a before any store, then s goes to both critic operands (and to
+// the actor part's own copy when there is one). (Non-temporal loads of data the previous kernel wrote gave wrong sums in
 // the column-sum kernel, so loads here stay plain.)
 template <typename T>
 __global__ void __launch_bounds__(256) k_gather(GatherArgs g) {
@@ -81,7 +81,7 @@ __global__ void __launch_bounds__(256) k_gather(GatherArgs g) {
   const uint8_t* src = g.buf + (int64_t)row * g.row_bytes;
   const int64_t xrow = (int64_t)b * g.Kc * (int64_t)sizeof(T);
   uint8_t* xsa = static_cast<uint8_t*>(g.xsa) + xrow;
-  uint8_t* xsp = static_cast<uint8_t*>(g.xsp) + xrow;
+  uint8_t* xsp = g.xsp ? static_cast<uint8_t*>(g.xsp) + xrow : nullptr;
   uint8_t* xs2 = static_cast<uint8_t*>(g.xs2) + xrow;
   const int sb = g.O * (int)sizeof(T), ab = g.A * (int)sizeof(T);
   const int ns = sb >> 4, na = ab >> 4;
@@ -107,13 +107,13 @@ __global__ void __launch_bounds__(256) k_gather(GatherArgs g) {
     if (v < na) z = a_in[v];
     if (v < ns) {
       xsa4[v] = x;
-      xsp4[v] = x;
+      if (xsp4) xsp4[v] = x;
       xs24[v] = y;
     }
     if (v < na) xa4[v] = z;
   }
   copy_tail<T>(xsa, src, sb, lane);
-  copy_tail<T>(xsp, src, sb, lane);
+  if (g.xsp) copy_tail<T>(xsp, src, sb, lane);
   copy_tail<T>(xs2, src + g.off_s2, sb, lane);
   copy_tail<T>(xsa + g.Ka * (int)sizeof(T), src + g.off_a, ab, lane);
   if (lane == 0) {
