@@ -675,7 +675,8 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
                c->idx};
   {
     const double e = (double)es(c);
-    const double bytes = (double)c->B * ((2.0 * c->O + c->A) * e + 8.0 + (3.0 * c->O + c->A) * e + 12.0);
+    const double copies = two ? 3.0 : 2.0;   // s to xsa (and xsp), s' to xs2
+    const double bytes = (double)c->B * ((2.0 * c->O + c->A) * e + 8.0 + (copies * c->O + c->A) * e + 12.0);
     CK(timed(c, "gather", c->B, c->O, c->A, 0.0, bytes, s0, [&] { return launch_gather(c->bf16, g, s0); }));
   }
   hipStream_t sc = s0, sa = s0;
