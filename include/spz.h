@@ -6,7 +6,7 @@
  * training the actor and the double-Q critics with target networks; Section
  * 3.2.2: actor and critic updated independently, here as two concurrent HIP
  * streams on one GPU). SAC is the paper's worked example; TD3 is the
- * alternative algorithm of Section 4.3 / Fig. 8. One update step:
+ * alternative algorithm of Section 4.2.4, Fig. 8. One update step:
  *   1. Philox-sampled replay indices and a row gather from the HBM ring buffer;
  *   2. critic stream: target action (actor + tanh-Gaussian head, or TD3 target
  *      actor + smoothing), target critics, TD target, online critics, critic
@@ -86,6 +86,11 @@ typedef struct spz_ctx spz_ctx;
 #define SPZ_DBG_DACTION 5   /* [batch, act_dim]: gradient of the actor loss with respect
                                to the actor's action a~ (Section 3.2.2's twin minimum
                                for SAC, critic 1 for TD3)                              */
+#define SPZ_DBG_BATCH 6     /* [batch, 2*obs_dim + act_dim + 2]: the transitions the last
+                               step gathered from the replay pool (Section 3.3.2), one
+                               row (s | a | s' | r | d) per batch row, as the update's
+                               kernels read them (bf16 contexts: the stored bfloat16
+                               values, widened to float32 exactly)                      */
 
 /* Loss record of one step: 8 floats. */
 #define SPZ_REC_LQ 0        /* mean (q1-y)^2 + mean (q2-y)^2                      */
@@ -143,7 +148,9 @@ typedef struct spz_hparams {
  * snapshot ordering, actor row split on. */
 void spz_hparams_default(spz_hparams* hp);
 
-/* Create a learner. obs_dim, act_dim >= 1; hidden[0..n_hidden) >= 1 with
+/* Create a learner: the single network-update process of Section 3.2 (its actor
+ * and double-Q critics with target critics, Section 3.2.2; TD3 adds a target
+ * actor), on one GPU. obs_dim, act_dim >= 1; hidden[0..n_hidden) >= 1 with
  * 1 <= n_hidden <= 6; batch >= 1. Parameters are initialised on the host from
  * `seed` with the fan-in uniform rule U(-1/sqrt(fan_in), 1/sqrt(fan_in)) drawn
  * from Philox4x32-10 (counter = (i>>2, 0, 0, net*16 + layer*2 + {W:0,b:1}),
@@ -183,7 +190,10 @@ int spz_buffer_push_async(spz_ctx* ctx, const float* obs, const float* act, cons
 int64_t spz_buffer_size(const spz_ctx* ctx);
 
 /* Enqueue n_steps update steps on `hip_stream` (a hipStream_t; NULL = the null
- * stream) and return without waiting. Step t (1-based, counted across calls)
+ * stream) and return without waiting. One step is one large-batch update of the
+ * actor and the critics from a uniform sample of the replay pool (Section 3.2.1,
+ * with the two halves updated independently as in Section 3.2.2 and Fig. 3's SAC
+ * computation graph). Step t (1-based, counted across calls)
  * samples idx[b] = mulhi32(Philox(seed; b>>2, t, 1, 0)[b&3], size) with
  * replacement, draws its normal deviates from purposes 2 (target) and 3
  * (policy), and ends with the Adam/Polyak pass. Non-finite values do not make
@@ -253,20 +263,24 @@ int64_t spz_step(const spz_ctx* ctx);
 /* Set the step counter (checkpoint resume, teacher forcing). Waits first. */
 int spz_set_step(spz_ctx* ctx, int64_t step);
 
-/* Float count of the object `which` in the flat layout (negative code on error). */
+/* Float count of the object `which` in the flat layout of the published weights
+ * (Section 3.3.1; negative code on error). */
 int64_t spz_param_count(const spz_ctx* ctx, int32_t which);
 
-/* Copy object `which` to the host array out[0..n_floats). Waits for the
- * context's work first. SPZ_ESIZE if n_floats != spz_param_count(ctx, which);
+/* Copy object `which` to the host array out[0..n_floats): the network weights the
+ * update process publishes to the other processes and to checkpoints (Section
+ * 3.3.1), plus the optimizer state and gradients. Waits for the context's work first. SPZ_ESIZE if n_floats != spz_param_count(ctx, which);
  * SPZ_EINVAL for a selector the algorithm does not have. */
 int spz_read_params(spz_ctx* ctx, int32_t which, float* out, int64_t n_floats);
 
-/* Overwrite object `which` from the host array in[0..n_floats) (checkpoint
- * resume, teacher forcing). Gradient selectors are read only (SPZ_EINVAL). */
+/* Overwrite object `which` from the host array in[0..n_floats): weights read back
+ * from a published copy (Section 3.3.1: checkpoints; also teacher forcing). Gradient selectors are read only (SPZ_EINVAL). */
 int spz_write_params(spz_ctx* ctx, int32_t which, const float* in, int64_t n_floats);
 
 /* Copy the loss records of steps first_step .. first_step+n-1 (1-based) into
- * out[n * SPZ_REC_WIDTH]. The library keeps the last 65536 records; older or
+ * out[n * SPZ_REC_WIDTH]: the critic, actor and temperature losses of each update
+ * step of Section 3.2 (the training curves the test process of Section 3.1.2 is
+ * there to show), with the non-finite and actor-updated flags. The library keeps the last 65536 records; older or
  * not yet enqueued steps give SPZ_EINVAL. Waits first. */
 int spz_read_losses(spz_ctx* ctx, float* out, int64_t first_step, int32_t n);
 

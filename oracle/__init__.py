@@ -3,7 +3,7 @@
 A plain, slow, float64 NumPy implementation of one update step of the method's
 network-update process (Section 3.2: a single large-batch updater that trains
 the actor and the twin critics with their target networks; SAC is the worked
-example, TD3 the alternative of Section 4.3 / Fig. 8). The paper prints no update
+example, TD3 the alternative of Section 4.2.4, Fig. 8). The paper prints no update
 equations, so each step follows the published SAC (Haarnoja et al., 2018) and
 TD3 (Fujimoto et al., 2018) algorithms; the readings taken where the paper is
 silent are listed in the module docstrings.

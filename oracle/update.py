@@ -4,7 +4,7 @@ The paper's learner (Section 3.2) draws a large uniform batch from the shared
 replay pool (Section 3.3.2) and updates the actor and the double-Q critics with
 their target networks, the actor and the critics being updated independently
 (Section 3.2.2). SAC is its worked example; TD3 runs in the same framework
-(Section 4.3, Fig. 8). The paper prints no update equations, so the steps below
+(Section 4.2.4, Fig. 8). The paper prints no update equations, so the steps below
 follow the published algorithms:
 
   SAC  Haarnoja et al., "Soft Actor-Critic Algorithms and Applications", 2018:
@@ -150,6 +150,9 @@ class Oracle:
         self.last_idx = None
         self.last_batch = None
         self.last_grads = None
+        # optional callable(str), told when each part of a step is done (progress of
+        # long steps in tests; no effect on the arithmetic)
+        self.progress = None
         # replay ring
         self.capacity = int(hp["capacity"])
         self.row_source = row_source
@@ -267,6 +270,10 @@ class Oracle:
             else:
                 self._td3_step(self.t)
 
+    def _note(self, what: str):
+        if self.progress is not None:
+            self.progress(what)
+
     def _sample(self, t: int):
         B, A = self.B, self.A
         idx = philox.indices(self.seed, t, B, self.size)
@@ -375,10 +382,13 @@ class Oracle:
         alpha = math.exp(log_alpha)
 
         y, _ = self.sac_target(s2, r, d, eps_tgt, alpha)
+        self._note("step %d: TD target" % t)
         lq, cg = self._critic_grads(s, a, y)
+        self._note("step %d: critic gradients" % t)
         if self.sequential:
             self._step_critics(cg)
         lpi, ag, pol = self.sac_actor(s, eps_pol, alpha)
+        self._note("step %d: actor gradient" % t)
         mean_lp_h = float(np.mean(pol["logp"] + hp["target_entropy"]))
         l_alpha = -log_alpha * mean_lp_h
         g_alpha = -mean_lp_h

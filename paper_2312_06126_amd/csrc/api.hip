@@ -104,6 +104,7 @@ struct spz_ctx {
   // run on concurrent streams; xsa itself (action columns overwritten by the actor's
   // sample) when they run in order on one stream and the critic part is done with it.
   void* xs_act = nullptr;
+  void* abuf = nullptr;   // sampled actions [Bp, A] of a one-stream step (debug read of the batch)
   float *r = nullptr, *d = nullptr;
   int32_t* idx = nullptr;
   // critic-stream workspace
@@ -672,11 +673,12 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
   c->xs_act = two ? c->xsp : c->xsa;
   GatherArgs g{c->buf, c->row_bytes, c->off_a, c->off_s2, c->off_r, c->off_d, c->O, c->A, c->Ka, c->Kc,
                c->B, c->seed, (uint32_t)c->size, c->d_step, c->xsa, c->xs2, two ? c->xsp : nullptr, c->r, c->d,
-               c->idx};
+               c->idx, two ? nullptr : c->abuf};
   {
     const double e = (double)es(c);
-    const double copies = two ? 3.0 : 2.0;   // s to xsa (and xsp), s' to xs2
-    const double bytes = (double)c->B * ((2.0 * c->O + c->A) * e + 8.0 + (copies * c->O + c->A) * e + 12.0);
+    // s to xsa (and xsp on two streams), s' to xs2; a to xsa (and abuf on one stream)
+    const double copies = two ? 3.0 : 2.0, acopies = two ? 1.0 : 2.0;
+    const double bytes = (double)c->B * ((2.0 * c->O + c->A) * e + 8.0 + (copies * c->O + acopies * c->A) * e + 12.0);
     CK(timed(c, "gather", c->B, c->O, c->A, 0.0, bytes, s0, [&] { return launch_gather(c->bf16, g, s0); }));
   }
   hipStream_t sc = s0, sa = s0;
@@ -767,6 +769,7 @@ int setup(spz_ctx* c) {
   CK(dalloc(c, &c->xsa, xb));
   CK(dalloc(c, &c->xs2, xb));
   CK(dalloc(c, &c->xsp, xb));
+  CK(dalloc(c, &c->abuf, (size_t)Bp * c->A * e));
   CK(dalloc_t(c, &c->r, Bp * 4));
   CK(dalloc_t(c, &c->d, Bp * 4));
   CK(dalloc_t(c, &c->idx, Bp * 4));
@@ -1064,7 +1067,7 @@ namespace {
 constexpr int64_t INGEST_ROWS = 65536;   // rows per ingestion slot
 constexpr int INGEST_SLOTS = 4;
 
-int ingest_init(spz_ctx* c) {
+static int ingest_init(spz_ctx* c) {
   if (c->si) return SPZ_OK;
   const int64_t rowf = 2 * (int64_t)c->O + c->A + 2;
   const size_t bytes = (size_t)(INGEST_ROWS * rowf * 4);
@@ -1217,7 +1220,7 @@ constexpr char CKPT_MAGIC[8] = {'S', 'P', 'Z', 'C', 'K', 'P', 'T', '1'};
 constexpr size_t CKPT_CHUNK = (size_t)64 << 20;
 
 // Device <-> file through a host bounce buffer, in chunks.
-int dev_to_file(spz_ctx* c, FILE* f, const void* dev, size_t bytes, std::vector<uint8_t>& tmp) {
+static int dev_to_file(spz_ctx* c, FILE* f, const void* dev, size_t bytes, std::vector<uint8_t>& tmp) {
   for (size_t o = 0; o < bytes; o += CKPT_CHUNK) {
     const size_t n = std::min(CKPT_CHUNK, bytes - o);
     CK(hipMemcpy(tmp.data(), static_cast<const uint8_t*>(dev) + o, n, hipMemcpyDeviceToHost));
@@ -1225,7 +1228,7 @@ int dev_to_file(spz_ctx* c, FILE* f, const void* dev, size_t bytes, std::vector<
   }
   return SPZ_OK;
 }
-int file_to_dev(spz_ctx* c, FILE* f, void* dev, size_t bytes, std::vector<uint8_t>& tmp) {
+static int file_to_dev(spz_ctx* c, FILE* f, void* dev, size_t bytes, std::vector<uint8_t>& tmp) {
   for (size_t o = 0; o < bytes; o += CKPT_CHUNK) {
     const size_t n = std::min(CKPT_CHUNK, bytes - o);
     if (fread(tmp.data(), 1, n, f) != n) return set_err(c, SPZ_EIO, "spz_load: file truncated");
@@ -1234,7 +1237,7 @@ int file_to_dev(spz_ctx* c, FILE* f, void* dev, size_t bytes, std::vector<uint8_
   return SPZ_OK;
 }
 
-void fill_header(const spz_ctx* c, CkptHeader& h) {
+static void fill_header(const spz_ctx* c, CkptHeader& h) {
   memset(&h, 0, sizeof(h));
   memcpy(h.magic, CKPT_MAGIC, 8);
   h.version = 1;
@@ -1530,6 +1533,7 @@ int spz_debug_read(spz_ctx* c, int32_t what, void* out, int64_t bytes) {
       need = B * 4;
       break;
     case SPZ_DBG_DACTION: need = B * c->A * 4; break;
+    case SPZ_DBG_BATCH: need = B * (2 * (int64_t)c->O + c->A + 2) * 4; break;
     default: return set_err(c, SPZ_EINVAL, "spz_debug_read: bad selector");
   }
   if (bytes != need) return set_err(c, SPZ_ESIZE, "spz_debug_read: size mismatch");
@@ -1550,6 +1554,36 @@ int spz_debug_read(spz_ctx* c, int32_t what, void* out, int64_t bytes) {
       CK(hipMemcpy(f + B, c->td3 ? c->qp1 : c->qp2, B * 4, hipMemcpyDeviceToHost));
       break;
     case SPZ_DBG_LOGPI: CK(hipMemcpy(f, c->logp, B * 4, hipMemcpyDeviceToHost)); break;
+    case SPZ_DBG_BATCH: {
+      // s from xsa, s' from xs2 (their first O columns), the actions from xsa's action
+      // columns where the step ran on two streams (the actor part had its own operand)
+      // and from the gather's copy otherwise, r and d from the arrays the TD target reads.
+      const bool two = c->hp.n_streams == 2 && c->hp.ordering != SPZ_ORDER_SEQUENTIAL;
+      const size_t e = es(c);
+      std::vector<uint8_t> xa((size_t)B * c->Kc * e), x2((size_t)B * c->Kc * e), ab((size_t)B * c->A * e);
+      std::vector<float> rr(B), dd(B);
+      CK(hipMemcpy(xa.data(), c->xsa, xa.size(), hipMemcpyDeviceToHost));
+      CK(hipMemcpy(x2.data(), c->xs2, x2.size(), hipMemcpyDeviceToHost));
+      if (!two) CK(hipMemcpy(ab.data(), c->abuf, ab.size(), hipMemcpyDeviceToHost));
+      CK(hipMemcpy(rr.data(), c->r, B * 4, hipMemcpyDeviceToHost));
+      CK(hipMemcpy(dd.data(), c->d, B * 4, hipMemcpyDeviceToHost));
+      auto val = [&](const std::vector<uint8_t>& v, int64_t i) {
+        if (c->bf16) return bf2f(reinterpret_cast<const bf16_t*>(v.data())[i]);
+        return reinterpret_cast<const float*>(v.data())[i];
+      };
+      const int64_t w = 2 * (int64_t)c->O + c->A + 2;
+      for (int64_t b = 0; b < B; ++b) {
+        float* o = f + b * w;
+        for (int j = 0; j < c->O; ++j) {
+          o[j] = val(xa, b * c->Kc + j);
+          o[c->O + c->A + j] = val(x2, b * c->Kc + j);
+        }
+        for (int j = 0; j < c->A; ++j) o[c->O + j] = two ? val(xa, b * c->Kc + c->Ka + j) : val(ab, b * c->A + j);
+        o[w - 2] = rr[b];
+        o[w - 1] = dd[b];
+      }
+      break;
+    }
     case SPZ_DBG_DACTION: {
       // da1 [Bp, Ap] holds the whole gradient under the SAC row split (and for TD3);
       // otherwise critic 2's part is in da2.

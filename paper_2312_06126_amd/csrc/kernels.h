@@ -14,6 +14,9 @@ struct GatherArgs {
   uint64_t seed; uint32_t size; const int64_t* step;
   void* xsa; void* xs2; void* xsp;   // [Bp, Kc] operand tensors (xsp may be null: not written)
   float* r; float* d; int32_t* idx;
+  // When set, a copy of the sampled actions [B, A] (operand type): on one stream the
+  // actor part later overwrites xsa's action columns with its own sample.
+  void* abuf;
 };
 
 struct PackArgs {

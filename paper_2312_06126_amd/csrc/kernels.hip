@@ -16,6 +16,11 @@ constexpr float HALF_LN_2PI_F = 0.91893853320467274f;
 
 __device__ inline float softplusf(float x) { return x > 0.0f ? x + log1pf(expf(-x)) : log1pf(expf(x)); }
 
+// Clamp and minimum that keep a NaN operand (fminf / fmaxf would drop it), so that a
+// non-finite network output reaches the loss record as it does in exact arithmetic.
+__device__ inline float clamp_keep_nan(float x, float lo, float hi) { return x < lo ? lo : (x > hi ? hi : x); }
+__device__ inline float min_keep_nan(float a, float b) { return (a < b || a != a) ? a : b; }
+
 // Standard normal deviate for flat element i of the stream (seed, step, purpose):
 // Box-Muller on words (0,1) -> lanes 0,1 and (2,3) -> lanes 2,3 of each Philox block.
 __device__ inline float normal_at(uint64_t seed, uint64_t i, uint32_t step, uint32_t purpose) {
@@ -116,6 +121,10 @@ __global__ void __launch_bounds__(256) k_gather(GatherArgs g) {
   if (g.xsp) copy_tail<T>(xsp, src, sb, lane);
   copy_tail<T>(xs2, src + g.off_s2, sb, lane);
   copy_tail<T>(xsa + g.Ka * (int)sizeof(T), src + g.off_a, ab, lane);
+  if (g.abuf) {
+    const T* a_src = reinterpret_cast<const T*>(src + g.off_a);
+    for (int j = lane; j < g.A; j += 64) static_cast<T*>(g.abuf)[(int64_t)b * g.A + j] = a_src[j];
+  }
   if (lane == 0) {
     g.r[b] = rv;
     g.d[b] = dv;
@@ -165,7 +174,7 @@ __global__ void __launch_bounds__(256) k_sac_head(SacHeadArgs h) {
     const float* z = h.z + (int64_t)b * h.ldz;
     const float eps = normal_at(h.seed, (uint64_t)r0 * h.A + e, t, h.purpose);
     const float mu = z[j], l = z[h.A + j];
-    const float lc = fminf(fmaxf(l, h.lmin), h.lmax);
+    const float lc = clamp_keep_nan(l, h.lmin, h.lmax);
     const float sig = expf(lc);
     const float u = mu + sig * eps;
     const float a = tanhf(u);
@@ -197,8 +206,8 @@ __global__ void __launch_bounds__(256) k_td3_head(Td3HeadArgs h) {
   float a = tanhf(h.z[(int64_t)b * h.ldz + j]);
   if (h.smooth) {
     const float eps = normal_at(h.seed, (uint64_t)e, t, P_NOISE_TGT);
-    const float nz = fminf(fmaxf(h.noise * eps, -h.clip), h.clip);
-    a = fminf(fmaxf(a + nz, -1.0f), 1.0f);
+    const float nz = clamp_keep_nan(h.noise * eps, -h.clip, h.clip);
+    a = clamp_keep_nan(a + nz, -1.0f, 1.0f);
   }
   static_cast<T*>(h.x)[(int64_t)b * h.ldx + h.xoff + j] = from_f<T>(a);
   if (h.th) h.th[e] = a;
@@ -366,7 +375,7 @@ __global__ void __launch_bounds__(256) k_act_head(ActHeadArgs h) {
   float u = z[j];
   if (h.sac && h.stochastic) {
     const float eps = normal_at(h.seed, (uint64_t)(h.row0 * h.A + e), h.counter, P_ACT);
-    u += expf(fminf(fmaxf(z[h.A + j], h.lmin), h.lmax)) * eps;
+    u += expf(clamp_keep_nan(z[h.A + j], h.lmin, h.lmax)) * eps;
   }
   h.a[e] = tanhf(u);
 }
@@ -376,7 +385,7 @@ __global__ void __launch_bounds__(256) k_td_target(TdArgs a) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= a.Bp) return;
   if (b >= a.B) { a.y[b] = 0.0f; return; }
-  float m = fminf(a.q1[b], a.q2[b]);
+  float m = min_keep_nan(a.q1[b], a.q2[b]);
   if (a.logp) m -= expf(*a.log_alpha) * a.logp[b];
   a.y[b] = a.r[b] + a.gamma * (1.0f - a.d[b]) * m;
 }

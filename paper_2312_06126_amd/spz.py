@@ -24,6 +24,7 @@ SELECTORS = {
     "g_actor": 15, "g_critic1": 16, "g_critic2": 17, "g_log_alpha": 18,
 }
 DBG_INDICES = 0
+DBG_BATCH = 6
 # Per-row values of the last step: selector -> rows of the array (None: act_dim columns).
 DEBUG_ROWS = {"td_target": (1, 1), "q": (2, 2), "qpi": (3, 2), "logpi": (4, 1), "daction": (5, None)}
 REC_WIDTH = 8
@@ -259,6 +260,13 @@ class Spz:
         self._check(self.lib.spz_debug_read(self.ctx, DBG_INDICES, out.ctypes.data_as(ctypes.c_void_p),
                                             out.nbytes))
         return out
+
+    def debug_batch(self):
+        """The last step's gathered transitions as (s, a, s', r, d) float32 arrays."""
+        O, A = self.obs_dim, self.act_dim
+        out = np.empty((self.batch, 2 * O + A + 2), np.float32)
+        self._check(self.lib.spz_debug_read(self.ctx, DBG_BATCH, out.ctypes.data_as(ctypes.c_void_p), out.nbytes))
+        return out[:, :O], out[:, O:O + A], out[:, O + A:2 * O + A], out[:, -2], out[:, -1]
 
     def debug_rows(self, what: str) -> np.ndarray:
         """Per-row float32 values of the last step: "td_target" [batch], "q" and "qpi"

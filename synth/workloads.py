@@ -2,7 +2,7 @@
 hyper-parameters.
 
 The paper fixes neither network sizes nor algorithm constants (it cites SAC and
-TD3 by reference, Section 3.2.2 and Section 4.3); these values are the workload
+TD3 by reference, Section 3.2.2 and Section 4.2.4); these values are the workload
 definitions this implementation is measured on. Hyper-parameters follow the
 published SAC / TD3 defaults (discount 0.99, Polyak 0.005, Adam 3e-4 with
 betas 0.9/0.999, eps 1e-8, log-std clamp [-20, 2], TD3 smoothing noise 0.2

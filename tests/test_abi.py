@@ -61,6 +61,9 @@ def test_debug_selectors_match_header(lib):
     for name, (val, _) in spz.DEBUG_ROWS.items():
         m = re.search(r"#define SPZ_DBG_%s (\d+)" % name.upper(), text)
         assert m and int(m.group(1)) == val, name
+    for name, val in (("INDICES", spz.DBG_INDICES), ("BATCH", spz.DBG_BATCH)):
+        m = re.search(r"#define SPZ_DBG_%s (\d+)" % name, text)
+        assert m and int(m.group(1)) == val, name
 
 
 def test_null_arguments_fail_cleanly(lib):
@@ -76,3 +79,20 @@ def test_null_arguments_fail_cleanly(lib):
     assert lib.spz_profile_stride(None, 1) == spz.SPZ_EINVAL
     assert lib.spz_buffer_push(None, None, None, None, None, None, 0) == spz.SPZ_EINVAL
     assert lib.spz_param_count(None, 0) == spz.SPZ_EINVAL
+
+
+def test_only_the_c_abi_is_exported(lib):
+    """The dynamic symbol table holds the spz_* calls of include/spz.h and the spzt_*
+    test hooks of include/spz_testing.h, nothing else (no C++ internals, no helpers)."""
+    import shutil
+    import subprocess
+    from paper_2312_06126_amd import spz
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm (binutils) not installed")
+    out = subprocess.run([nm, "-D", "--defined-only", spz.LIB_PATH], capture_output=True, text=True, check=True)
+    names = sorted(line.split()[-1] for line in out.stdout.splitlines() if line.strip())
+    testing = open(os.path.join(ROOT, "include", "spz_testing.h")).read()
+    testing = re.sub(r"/\*.*?\*/", "", testing, flags=re.S)
+    hooks = sorted(set(re.findall(r"\b(spzt_[a-z0-9_]+)\s*\(", testing)))
+    assert names == sorted(declared_functions() + hooks), [n for n in names if not n.startswith("spz")]

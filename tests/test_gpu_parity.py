@@ -19,7 +19,7 @@ import synth
 from oracle import philox
 from synth.workloads import Workload
 
-from .helpers import (NET_KEYS, ambiguous_elements, check_param_parity, log, make_gpu, make_oracle, make_pair,
+from .helpers import (NET_KEYS, ambiguous_steps, check_param_parity, log, make_gpu, make_oracle, make_pair,
                       oracle_grad_flat, per_tensor_rel, state_keys, teacher_force)
 
 pytestmark = pytest.mark.gpu
@@ -269,6 +269,7 @@ def test_teacher_forced_log_std_clamp_active():
 # ---------------------------------------------------------------------------- 10-step runs
 def ten_steps(w, rows, steps=10, virtual=False, n_streams=2):
     g, o = make_pair(w, rows, virtual=virtual, n_streams=n_streams)
+    p0 = {k: o.params(k) for k in NET_KEYS}
     hist = {k: [] for k in NET_KEYS}
     for _ in range(steps):
         g.update(1)
@@ -277,21 +278,33 @@ def ten_steps(w, rows, steps=10, virtual=False, n_streams=2):
             if o.last_grads[k] is not None:
                 hist[k].append(oracle_grad_flat(o, k))
     rg, ro = g.read_losses(1, steps), o.losses()
-    out = {k: (g.read_params(k), o.params(k)) for k in state_keys(w.algo) if not k.startswith(("m_", "v_"))}
+    out = {k: (g.read_params(k), o.params(k)) for k in state_keys(w.algo)}
+    out["p0"] = p0
     g.close()
     return rg, ro, out, o, hist
 
 
 def check_ten_step_params(w, params, o, hist, steps):
-    for k, (pg, pr) in params.items():
-        if k == "log_alpha":
-            assert abs(pg[0] - pr[0]) <= FP32_TOL * max(abs(pr[0]), 1e-2), (pg, pr)
+    """Parameters and targets against the oracle (sign-ambiguous elements held to
+    their Adam bound), Adam's moments m and v per tensor with no exclusions."""
+    p0 = params.get("p0", {})
+    for k, val in params.items():
+        if k == "p0":
+            continue
+        pg, pr = val
+        if k in ("log_alpha", "m_log_alpha", "v_log_alpha"):
+            assert abs(pg[0] - pr[0]) <= FP32_TOL * max(abs(pr[0]), 1e-2 if k == "log_alpha" else 1e-12), (k, pg, pr)
+            continue
+        if k.startswith(("m_", "v_")):
+            e = per_tensor_rel(o, k[2:], pg, pr)
+            log("  %s %s rel %.2e" % (w.name, k, e))
+            assert e <= FP32_TOL, (k, e)
             continue
         net = k[1:] if k.startswith("t") else k
-        amb = ambiguous_elements(o, net, hist[net])
+        amb = ambiguous_steps(o, net, hist[net])
         lr = w.lr_actor if net == "actor" else w.lr_critic
-        e = check_param_parity(o, net, pg, pr, amb, FP32_TOL, steps, lr)
-        log("  %s %s param rel %.2e (ambiguous %d of %d)" % (w.name, k, e, amb.sum(), amb.size))
+        e = check_param_parity(o, net, pg, pr, amb, FP32_TOL, lr, steps, p0=p0.get(k))
+        log("  %s %s param rel %.2e (ambiguous %d of %d)" % (w.name, k, e, int((amb > 0).sum()), amb.size))
 
 
 @pytest.mark.parametrize("w,rows,virtual", [(W["sac_small"], 10_000, False), (RAGGED, 5000, False),
@@ -332,18 +345,25 @@ def test_bf16_loss_parity(w, rows, steps):
 
 
 # ---------------------------------------------------------------------------- invariances
-def test_stream_and_chunk_invariance_bit_exact():
-    w = RAGGED
-    log("invariance")
+@pytest.mark.parametrize("w,rows,steps", [
+    (RAGGED, 5000, 10), (FUSED_BF16, 5000, 4), (FUSED_TD3_BF16, 5000, 4),
+    (W["sac_large_bf16"].replace(batch=2560, capacity=20_000), 20_000, 3)],
+    ids=["ragged_fp32", "fused_bf16_row_split", "fused_td3_bf16", "large_b2560"])
+def test_stream_and_chunk_invariance_bit_exact(w, rows, steps):
+    """One stream (where the actor part reuses the critic operand and, for SAC bf16,
+    takes the row split) and two concurrent streams give bit-identical parameters,
+    targets, Adam moments and loss records; so do different update() chunkings."""
+    log("invariance %s" % w.name)
+    half = steps // 2
     runs = []
-    for n_streams, chunks in ((2, [10]), (1, [10]), (2, [5, 5]), (2, [3, 3, 4])):
+    for n_streams, chunks in ((2, [steps]), (1, [steps]), (2, [half, steps - half]), (1, [1] * steps)):
         g = make_gpu(w, n_streams=n_streams)
-        synth_rows = synth.workload_rows(w, 0, 5000, 0)
-        g.buffer_push(*synth_rows)
+        g.buffer_push(*synth.workload_rows(w, 0, rows, 0))
         for c in chunks:
             g.update(c)
-        runs.append({k: g.read_params(k) for k in ("actor", "critic1", "tcritic2", "log_alpha")})
-        runs[-1]["rec"] = g.read_losses(1, 10)
+        keys = ["actor", "critic1", "critic2", "tcritic1", "tcritic2", "log_alpha", "m_critic1", "v_actor"]
+        runs.append({k: g.read_params(k) for k in keys + (["tactor"] if w.algo == "td3" else [])})
+        runs[-1]["rec"] = g.read_losses(1, steps)
         g.close()
     for r in runs[1:]:
         for k in r:
@@ -475,6 +495,7 @@ def test_batch_changes_mid_run_parity():
     w = RAGGED.replace(batch=1000)
     log("batch changes %s" % w.name)
     g, o = make_pair(w, 5000)
+    p0 = {k: o.params(k) for k in NET_KEYS}
     hist = {k: [] for k in NET_KEYS}
     for b, n in ((1000, 2), (300, 2), (777, 1), (1000, 1), (40, 2)):
         g.set_batch(b)
@@ -486,7 +507,8 @@ def test_batch_changes_mid_run_parity():
             for k in NET_KEYS:
                 hist[k].append(oracle_grad_flat(o, k))
     check_losses(g.read_losses(1, o.t), o.losses(), FP32_TOL, w.name)
-    params = {k: (g.read_params(k), o.params(k)) for k in state_keys(w.algo) if not k.startswith(("m_", "v_"))}
+    params = {k: (g.read_params(k), o.params(k)) for k in state_keys(w.algo)}
+    params["p0"] = p0
     check_ten_step_params(w, params, o, hist, o.t)
     g.close()
 

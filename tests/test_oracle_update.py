@@ -450,3 +450,19 @@ def test_mutation_wrong_sign_in_target_is_caught():
     y, pol2 = o.sac_target(s2, r, d, eps, alpha)
     wrong = r + 0.99 * (1 - d) * (min(c1, c2) + alpha * pol2["logp"])   # sign flipped
     assert not np.allclose(y[d == 0], wrong[d == 0])
+
+
+def test_nan_reward_sets_nonfinite_flag():
+    """A NaN reward in a sampled row makes the step's losses NaN and sets the
+    non-finite flag (the loss record's contract); min(Q1', Q2') propagates a NaN."""
+    o = _filled(n=40)
+    idx = philox.indices(o.seed, 1, o.B, o.size)
+    o.buf_rew[idx[0]] = np.nan
+    with np.errstate(invalid="ignore"):
+        o.update(1)
+    rec = o.losses()[0]
+    assert np.isnan(rec[U.REC_LQ]) and rec[U.REC_NONFINITE] == 1.0
+    assert np.isnan(np.minimum(np.nan, 1.0)) and np.isnan(np.minimum(1.0, np.nan))
+    clean = _filled(n=40)
+    clean.update(1)
+    assert clean.losses()[0][U.REC_NONFINITE] == 0.0
