@@ -153,6 +153,14 @@ class Oracle:
         # optional callable(str), told when each part of a step is done (progress of
         # long steps in tests; no effect on the arithmetic)
         self.progress = None
+        # Test hook for a floating-point decision of a discrete choice: when set to a
+        # bool per batch row, the next SAC step's actor loss takes critic 1 on exactly
+        # those rows instead of deciding qp1 <= qp2 itself (the values differ only by
+        # accumulation order where two implementations disagree). The oracle's own
+        # decision and both critic values stay in last_min_choice / last_qpi.
+        self.forced_min_choice = None
+        self.last_min_choice = None
+        self.last_qpi = None
         # replay ring
         self.capacity = int(hp["capacity"])
         self.row_source = row_source
@@ -322,9 +330,10 @@ class Oracle:
         y = r + hp["gamma"] * (1.0 - d) * (np.minimum(qt1, qt2) - alpha * pol2["logp"])
         return y, pol2
 
-    def sac_actor(self, s, eps_pol, alpha):
+    def sac_actor(self, s, eps_pol, alpha, take1=None):
         """Actor loss and gradient: reparameterised sample on s, twin-Q minimum at the
         current critics (step-start under snapshot ordering, updated under sequential).
+        take1 (bool per row, optional) replaces the choice qp1 <= qp2 of the minimum.
         Returns (L_pi, actor grads, policy dict)."""
         hp, B, A, rnd = self.hp, self.B, self.A, self.rnd
         lmin, lmax = hp["log_std_min"], hp["log_std_max"]
@@ -333,7 +342,9 @@ class Oracle:
         xa = np.concatenate([s, pol["a"]], axis=1)
         qp1 = forward(self.net["critic1"], xa, rnd)[0][:, 0]
         qp2 = forward(self.net["critic2"], xa, rnd)[0][:, 0]
-        take1 = qp1 <= qp2
+        own = qp1 <= qp2
+        self.last_min_choice, self.last_qpi = own, (qp1, qp2)
+        take1 = own if take1 is None else np.asarray(take1, dtype=bool)
         lpi = float(np.mean(alpha * pol["logp"] - np.where(take1, qp1, qp2)))
         dq1 = np.where(take1, -1.0 / B, 0.0)
         dq2 = np.where(take1, 0.0, -1.0 / B)
@@ -387,7 +398,8 @@ class Oracle:
         self._note("step %d: critic gradients" % t)
         if self.sequential:
             self._step_critics(cg)
-        lpi, ag, pol = self.sac_actor(s, eps_pol, alpha)
+        forced, self.forced_min_choice = self.forced_min_choice, None
+        lpi, ag, pol = self.sac_actor(s, eps_pol, alpha, take1=forced)
         self._note("step %d: actor gradient" % t)
         mean_lp_h = float(np.mean(pol["logp"] + hp["target_entropy"]))
         l_alpha = -log_alpha * mean_lp_h

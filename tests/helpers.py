@@ -172,3 +172,27 @@ def check_param_parity(o, key, pg, pr, amb_steps, tol, lr, steps, p0=None, max_f
         assert not np.any(flipped & ~amb), (key, int(np.sum(flipped & ~amb)))
     assert worst <= tol, (key, worst)
     return worst
+
+
+# ---------------------------------------------------------------- the twin-minimum choice
+# The SAC actor loss's min(Q1, Q2) picks a critic per row: where the two values are
+# within accumulation-order error of each other, float32 and float64 can pick
+# differently, and the row's whole gradient then moves to the other critic (one such
+# row changes a first-layer weight gradient at batch 131072 by about 1/sqrt(batch) of
+# its size). Comparisons of one step take the GPU's choice into the oracle and check it.
+
+def gpu_min_choice(g):
+    """The GPU's twin-minimum choice (critic 1 where qp1 <= qp2) of its last actor step."""
+    qpi = g.debug_rows("qpi")
+    return qpi[0] <= qpi[1]
+
+
+def check_min_choice(o, take1, tol):
+    """The oracle's own choice of its last step agrees with take1 wherever its two critic
+    values differ by more than tol times their rms. Returns the number of rows taken over."""
+    own = o.last_min_choice
+    qp1, qp2 = o.last_qpi
+    scale = float(np.sqrt(np.mean(qp1 * qp1)))
+    diff = own != np.asarray(take1, bool)
+    assert np.all(np.abs(qp1 - qp2)[diff] <= tol * scale), np.abs(qp1 - qp2)[diff].max() / scale
+    return int(diff.sum())

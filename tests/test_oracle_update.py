@@ -466,3 +466,25 @@ def test_nan_reward_sets_nonfinite_flag():
     clean = _filled(n=40)
     clean.update(1)
     assert clean.losses()[0][U.REC_NONFINITE] == 0.0
+
+
+def test_forced_min_choice_hook():
+    """The twin-minimum test hook: forcing the oracle's own choice changes nothing;
+    forcing the opposite choice on every row changes the actor's step but not the
+    critics' (they do not see the actor loss), and the hook applies to one step only."""
+    a, b, c = _filled(n=40), _filled(n=40), _filled(n=40)
+    for o in (a, b, c):
+        o.set_batch(32)
+    a.update(1)
+    own = a.last_min_choice.copy()
+    b.forced_min_choice = own
+    b.update(1)
+    for k in ("actor", "critic1", "critic2", "log_alpha"):
+        assert np.array_equal(a.params(k), b.params(k)), k
+    c.forced_min_choice = ~own
+    c.update(1)
+    assert np.array_equal(c.last_min_choice, own)
+    assert not np.array_equal(a.params("actor"), c.params("actor"))
+    for k in ("critic1", "critic2", "log_alpha"):
+        assert np.array_equal(a.params(k), c.params(k)), k
+    assert c.forced_min_choice is None
