@@ -218,6 +218,26 @@ int spz_synchronize(spz_ctx* ctx);
  * Errors: SPZ_EINVAL, SPZ_EHIP. */
 int spz_act(spz_ctx* ctx, const float* obs, int64_t n, int32_t stochastic, uint32_t counter, float* act);
 
+/* spz_act without allocation, for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * obs: DEVICE float32 [n, obs_dim]; act: DEVICE float32 [n, act_dim]; both owned by
+ * the caller. Same actions as spz_act (same kernels, bit for bit), enqueued on
+ * `hip_stream` (a hipStream_t; NULL = the null stream) without waiting: the actor
+ * weights used are the ones current when the kernels run in that stream's order.
+ * Intermediate values (observation operand, hidden activations, head output) live
+ * in a 64 MiB device array of the library, one per GPU, held until the process ends
+ * and shared by every call on that GPU: calls that overlap on one GPU (other streams,
+ * other threads, other contexts) race, so order them on one stream or synchronize
+ * between them. The call writes every scratch byte it reads, so the previous call's
+ * contents do not matter. n is limited by that array: at most the largest multiple
+ * of 256 rows with e * (pad32(obs_dim) + 2 * max_l pad32(hidden[l])) + 4 * pad32(out)
+ * bytes per row (e = 2 for bf16 GEMM operands, 4 for fp32; out = 2*act_dim for SAC,
+ * act_dim for TD3), plus alignment, within 64 MiB; larger n gives SPZ_EINVAL with
+ * the limit in the message. Calls no hipMalloc / hipFree.
+ * Errors: SPZ_EINVAL, SPZ_EHIP. */
+int spz_act_noalloc(spz_ctx* ctx, const float* obs, int64_t n, int32_t stochastic, uint32_t counter, float* act,
+                    void* hip_stream);
+
 /* Checkpoints (the paper publishes weights through files, Section 3.3.1). A file
  * holds the whole learner state: online and target parameters, Adam moments,
  * log(alpha), the step counter, the Philox seed, the loss records and, with

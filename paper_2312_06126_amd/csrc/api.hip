@@ -29,15 +29,42 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "kernels.h"
 
 using namespace spz;
 
+// Device scratch of the allocation-free sampler-action call (spz_act_noalloc): the
+// observation operand, two hidden-activation buffers and the actor head output of
+// one call. One copy per GPU, held until the process ends; every call on a GPU uses
+// that GPU's copy. Host code never passes the array's name to a kernel: it uses the
+// device address taken by hipGetSymbolAddress (g_scratch_ptr below).
+constexpr size_t ACT_SCRATCH_BYTES = (size_t)64 << 20;
+static __device__ __align__(256) uint8_t scratch[ACT_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string tl_err;
+
+// Device address of `scratch` per device ordinal, taken once per device (with the
+// device current) by the first spz_create on it.
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+hipError_t scratch_init(int device) {
+  if (device < 0 || device >= MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[device]) return hipSuccess;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  if (!p) return hipErrorInvalidSymbol;
+  g_scratch_ptr[device] = p;
+  return hipSuccess;
+}
 
 struct Lay {
   int in_f, out_f, in_p, out_p;
@@ -139,7 +166,7 @@ struct spz_ctx {
   hipEvent_t ev_fork = nullptr, ev_c = nullptr, ev_a = nullptr;
   hipStream_t last = nullptr;
   bool has_last = false;   // an update was enqueued on `last` (which may be the null stream)
-  std::vector<void*> scratch;   // ping-pong view of cs_h, one entry per hidden layer
+  std::vector<void*> cs_hid;   // ping-pong view of cs_h, one entry per hidden layer
   std::vector<void*> allocs;
   // kernel timing
   struct ProfKey { std::string name; int M, N, K; double flops, bytes; int64_t launches; double ms; };
@@ -565,18 +592,18 @@ hipError_t critic_part(spz_ctx* c, hipStream_t s) {
   const int pa = c->net[0].L.back().out_p;
   const spz_hparams& hp = c->hp;
   if (!c->td3) {
-    HK(forward(c, 0, false, c->xs2, c->Kc, c->scratch.data(), nullptr, true, nullptr, c->z2, s));
+    HK(forward(c, 0, false, c->xs2, c->Kc, c->cs_hid.data(), nullptr, true, nullptr, c->z2, s));
     SacHeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_TGT, hp.log_std_min, hp.log_std_max,
                   c->xs2, c->Kc, c->Ka, c->logp2, nullptr, nullptr, nullptr};
     HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, h, s); }));
   } else {
-    HK(forward(c, 0, true, c->xs2, c->Kc, c->scratch.data(), nullptr, true, nullptr, c->z2, s));
+    HK(forward(c, 0, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, true, nullptr, c->z2, s));
     Td3HeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, 1, hp.policy_noise, hp.noise_clip,
                   c->xs2, c->Kc, c->Ka, nullptr};
     HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
-  HK(forward(c, 1, true, c->xs2, c->Kc, c->scratch.data(), nullptr, false, c->c_rdot, c->qt1, s));
-  HK(forward(c, 2, true, c->xs2, c->Kc, c->scratch.data(), nullptr, false, c->c_rdot, c->qt2, s));
+  HK(forward(c, 1, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, false, c->c_rdot, c->qt1, s));
+  HK(forward(c, 2, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, false, c->c_rdot, c->qt2, s));
   TdArgs td{c->qt1, c->qt2, c->r, c->d, c->td3 ? nullptr : c->logp2, log_alpha_ptr(c), c->y, hp.gamma,
             c->B, c->Bp};
   HK(timed(c, "td_target", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_td_target(td, s); }));
@@ -798,10 +825,10 @@ int setup(spz_ctx* c) {
     }
   }
   c->ha.assign(nh, nullptr);
-  c->scratch.assign(nh, nullptr);
+  c->cs_hid.assign(nh, nullptr);
   for (int l = 0; l < nh; ++l) {
     CK(dalloc(c, &c->ha[l], (size_t)Bp * pad32(c->hidden[l]) * e));
-    c->scratch[l] = c->cs_h[l & 1];
+    c->cs_hid[l] = c->cs_h[l & 1];
   }
   // ReLU masks as bits where the large-tile kernel produces and consumes them (the
   // same condition holds for every product that reads a layer's mask), and the
@@ -1010,6 +1037,13 @@ spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int
     return nullptr;
   }
   plan_layout(c);
+  const hipError_t se = scratch_init(hp->device);
+  if (se != hipSuccess) {
+    set_err(nullptr, SPZ_EHIP, std::string("spz_create: hipGetSymbolAddress of the scratch array: ") +
+                                   hipGetErrorString(se));
+    delete c;
+    return nullptr;
+  }
   const int rc = setup(c);
   if (rc != SPZ_OK) {
     const std::string msg = c->err;
@@ -1203,6 +1237,81 @@ int spz_act(spz_ctx* c, const float* obs, int64_t n, int32_t stochastic, uint32_
     if (e != hipSuccess) rc = set_err(c, SPZ_EHIP, std::string("spz_act: ") + hipGetErrorString(e));
   }
   return rc;
+}
+
+// ---------------------------------------------------------------------------- allocation-free actions
+namespace {
+inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Scratch layout of one spz_act_noalloc call over `rows` rows: observation operand
+// [rows, Ka], two hidden-activation buffers [rows, hmax] (operand type), head output
+// [rows, out_p] float32, each on a 256-byte boundary. Returns the bytes used.
+size_t act_scratch_layout(const spz_ctx* c, int64_t rows, size_t off[4]) {
+  const size_t e = es(c);
+  const int pa = c->net[0].L.back().out_p;
+  off[0] = 0;
+  off[1] = align256(off[0] + (size_t)rows * c->Ka * e);
+  off[2] = align256(off[1] + (size_t)rows * c->hmax * e);
+  off[3] = align256(off[2] + (size_t)rows * c->hmax * e);
+  return off[3] + (size_t)rows * pa * 4;
+}
+
+// Largest row count (a multiple of 256) whose layout fits the scratch array.
+int64_t act_scratch_rows(const spz_ctx* c) {
+  size_t off[4];
+  int64_t lo = 0, hi = (int64_t)(ACT_SCRATCH_BYTES / 256) + 1;   // in units of 256 rows
+  while (hi - lo > 1) {
+    const int64_t mid = (lo + hi) / 2;
+    if (act_scratch_layout(c, mid * 256, off) <= ACT_SCRATCH_BYTES) lo = mid;
+    else hi = mid;
+  }
+  return lo * 256;
+}
+}  // namespace
+
+int spz_act_noalloc(spz_ctx* c, const float* obs, int64_t n, int32_t stochastic, uint32_t counter, float* act,
+                    void* hip_stream) {
+  if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_act_noalloc: NULL context");
+  if (n < 0 || (n > 0 && (!obs || !act))) return set_err(c, SPZ_EINVAL, "spz_act_noalloc: bad arrays");
+  if (stochastic && c->td3) return set_err(c, SPZ_EINVAL, "spz_act_noalloc: TD3 policies are deterministic");
+  const int64_t max_rows = act_scratch_rows(c);
+  if (n > max_rows) {
+    char msg[160];
+    std::snprintf(msg, sizeof(msg), "spz_act_noalloc: %lld rows exceed the %lld rows this network fits in the %zu-byte scratch",
+                  (long long)n, (long long)max_rows, ACT_SCRATCH_BYTES);
+    return set_err(c, SPZ_EINVAL, msg);
+  }
+  if (n == 0) return SPZ_OK;
+  CK(hipSetDevice(c->hp.device));
+  uint8_t* base = static_cast<uint8_t*>(g_scratch_ptr[c->hp.device]);
+  if (!base) return set_err(c, SPZ_EHIP, "spz_act_noalloc: scratch address not initialised");
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const int rows = (int)((n + 255) / 256 * 256);
+  size_t off[4];
+  act_scratch_layout(c, rows, off);
+  void* xop = base + off[0];
+  void* hid[8];
+  for (int l = 0; l < 8; ++l) hid[l] = base + off[1 + (l & 1)];
+  float* z = reinterpret_cast<float*>(base + off[3]);
+  // Operand rows [n, rows) and columns [obs_dim, Ka) are written as zeros here: the
+  // scratch keeps the previous call's contents.
+  ObsArgs oa{obs, (int)n, rows, c->O, c->Ka, xop, c->Ka};
+  CK(launch_obs_operand(c->bf16, oa, s));
+  const int saveB = c->B, saveBp = c->Bp;
+  const bool saveProf = c->prof;
+  c->B = (int)n;
+  c->Bp = rows;
+  c->prof = false;
+  const hipError_t e = forward(c, 0, false, xop, c->Ka, hid, nullptr, true, nullptr, z, s);
+  c->B = saveB;
+  c->Bp = saveBp;
+  c->prof = saveProf;
+  CK(e);
+  const int pa = c->net[0].L.back().out_p;
+  ActHeadArgs ha{z, pa, c->A, (int)n, 0, c->td3 ? 0 : 1, stochastic ? 1 : 0, c->seed, counter,
+                 c->hp.log_std_min, c->hp.log_std_max, act};
+  CK(launch_act_head(ha, s));
+  return SPZ_OK;
 }
 
 // ---------------------------------------------------------------------------- checkpoints

@@ -32,7 +32,7 @@ EXPORTS = ["spz_hparams_default", "spz_create", "spz_destroy", "spz_buffer_push"
            "spz_update", "spz_synchronize", "spz_step", "spz_set_step", "spz_param_count",
            "spz_read_params", "spz_write_params", "spz_read_losses", "spz_debug_read", "spz_last_error",
            "spz_profile_enable", "spz_profile_only", "spz_profile_stride", "spz_profile_read", "spz_set_batch", "spz_batch", "spz_autotune_batch",
-           "spz_save", "spz_load", "spz_act", "spz_buffer_push_async"]
+           "spz_save", "spz_load", "spz_act", "spz_buffer_push_async", "spz_act_noalloc"]
 
 
 class SpzError(RuntimeError):
@@ -84,6 +84,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "spz_set_batch": (ctypes.c_int, [P, ctypes.c_int32]),
         "spz_save": (ctypes.c_int, [P, ctypes.c_char_p, ctypes.c_int32]),
         "spz_act": (ctypes.c_int, [P, fp, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, fp]),
+        "spz_act_noalloc": (ctypes.c_int, [P, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, P, P]),
         "spz_load": (ctypes.c_int, [P, ctypes.c_char_p]),
         "spz_batch": (ctypes.c_int32, [P]),
         "spz_autotune_batch": (ctypes.c_int, [P, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, P,
@@ -206,6 +207,13 @@ class Spz:
         self._check(self.lib.spz_act(self.ctx, _fptr(obs), n, 1 if stochastic else 0, int(counter) & 0xFFFFFFFF,
                                      _fptr(out)))
         return out
+
+    def act_noalloc(self, obs_ptr: int, n: int, act_ptr: int, stochastic: bool = False, counter: int = 0,
+                    stream=None):
+        """spz_act_noalloc on device buffers (addresses, e.g. torch tensors' data_ptr()):
+        obs float32 [n, obs_dim] in, act float32 [n, act_dim] out; asynchronous on stream."""
+        self._check(self.lib.spz_act_noalloc(self.ctx, obs_ptr, int(n), 1 if stochastic else 0,
+                                             int(counter) & 0xFFFFFFFF, act_ptr, _stream_handle(stream)))
 
     def save(self, path: str, ring: bool = True):
         """Whole learner state to a file (with the replay ring unless ring=False)."""
