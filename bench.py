@@ -132,18 +132,17 @@ def roofline(stats, prec: str):
     return r
 
 
-def sweep(w, args, stream, steps: int = 100):
-    """Frame rate at the geometric batch sizes 16384 .. the workload's batch; the knee
-    is the smallest batch within 5% of the best frame rate."""
+def sweep(g, w, stream, steps: int = 30, warm: int = 3):
+    """Frame rate at the geometric batch sizes 16384 .. the workload's batch (the
+    paper's batch-size enumeration, Section 3.4), on the timed context switched with
+    spz_set_batch (its buffers are sized for the largest batch); the knee is the
+    smallest batch within 5% of the best frame rate. Restores the workload's batch."""
     import torch
-    from paper_2312_06126_amd import Spz
     out = []
-    b = 16384
-    while b <= w.batch:
-        wb = w.replace(batch=b)
-        g = Spz(wb.obs_dim, wb.act_dim, wb.hidden, wb.batch, wb.hparams(), args.seed, n_streams=args.streams)
-        fill_ring(g, wb, args.data_seed, wb.capacity)
-        g.update(args.warmup, stream)
+    b = min(16384, w.batch)
+    while True:
+        g.set_batch(b)
+        g.update(warm, stream)
         torch.cuda.synchronize()
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0.record(stream)
@@ -151,13 +150,44 @@ def sweep(w, args, stream, steps: int = 100):
         t1.record(stream)
         torch.cuda.synchronize()
         ms = t0.elapsed_time(t1) / steps
-        g.close()
         out.append(dict(batch=b, ms_per_step=round(ms, 4), value=round(frames_per_second(b, steps, ms * steps / 1e3), 1)))
         progress("sweep batch %d: %.3f ms/step" % (b, ms))
-        b *= 2
+        if b >= w.batch:
+            break
+        b = min(2 * b, w.batch)
+    g.set_batch(w.batch)
     best = max(r["value"] for r in out)
     knee = min(r["batch"] for r in out if r["value"] >= 0.95 * best)
-    return dict(points=out, knee_batch=knee, steps=steps)
+    return dict(points=out, knee_batch=knee, steps=steps, note="one context created at the workload's batch, "
+                "spz_set_batch between points, %d untimed steps before each" % warm)
+
+
+def timed_rate(g, w, stream, steps: int, warmup: int):
+    """ms per step and frame rate of `steps` update steps after `warmup` (events on stream)."""
+    import torch
+    g.update(warmup, stream)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    g.update(steps, stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    return dict(ms_per_step=round(ms, 4), value=round(frames_per_second(w.batch, steps, ms * steps / 1e3), 1),
+                steps=steps, warmup=warmup)
+
+
+def hbm_kernels(survey, names=("gather", "adam_polyak")):
+    """Achieved HBM rate of the memory-bound kernels of the step (algorithmic bytes per
+    launch over the mean event-measured duration in the survey pass) against 8 TB/s."""
+    out = {}
+    for s in survey:
+        if s["name"] in names and s["name"] not in out and s["bytes"] > 0:
+            gbs = s["bytes"] / (s["avg_ms"] / 1e3) / 1e9
+            out[s["name"]] = dict(achieved=round(gbs, 1), peak=PEAK_HBM_GBS, unit="GB/s",
+                                  frac=round(gbs / PEAK_HBM_GBS, 4), bytes_per_launch=s["bytes"],
+                                  avg_launch_us=round(s["avg_ms"] * 1e3, 2))
+    return out
 
 
 def cpu_baseline(w, seed: int, data_seed: int, sample_batch: int):
@@ -191,8 +221,13 @@ def main():
     ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
                     help="2 runs the actor and critic halves on concurrent streams (per-kernel event "
                          "durations then overlap, so the roofline is taken from 1-stream runs)")
-    ap.add_argument("--sweep", action="store_true",
-                    help="also time the batch sizes 16384..131072 of the workload and report the knee")
+    ap.add_argument("--graphs", default="auto", choices=("auto", "0", "1"),
+                    help="replay update steps from captured HIP graphs (auto: on for every workload but "
+                         "the large one, whose roofline needs events on its kernels in the timed region)")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the batch sweep 16384..batch (default on for the large workload)")
+    ap.add_argument("--no-streams2", action="store_true",
+                    help="skip the two-stream rate reported beside the one-stream headline")
     ap.add_argument("--autotune", action="store_true",
                     help="also run the library's adaptive batch-size controller (spz_autotune_batch) "
                          "from batch 16384 on a context created with the workload's batch")
@@ -223,9 +258,12 @@ def main():
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
 
-    progress("workload %s batch %d ring %d prec %s streams %d" % (w.name, w.batch, w.capacity, w.prec,
-                                                                  args.streams))
-    g = Spz(w.obs_dim, w.act_dim, w.hidden, w.batch, w.hparams(), args.seed, n_streams=args.streams)
+    large = w.name == "sac_large_bf16"
+    graphs = (not large) if args.graphs == "auto" else args.graphs == "1"
+    progress("workload %s batch %d ring %d prec %s streams %d graphs %d" % (w.name, w.batch, w.capacity, w.prec,
+                                                                            args.streams, graphs))
+    g = Spz(w.obs_dim, w.act_dim, w.hidden, w.batch, dict(w.hparams(), graphs=int(graphs)), args.seed,
+            n_streams=args.streams)
     fill_ring(g, w, args.data_seed, w.capacity)
 
     g.update(args.warmup, stream)
@@ -243,11 +281,17 @@ def main():
         g.update(SURVEY_STEPS, stream)
         survey = g.profile_read()
         top = survey[0]
-        g.profile_enable(True, reserve_launches=40 * steps)
-        g.profile_only(top["name"], top["M"], top["N"], top["K"])
-        g.profile_stride(TIMED_STRIDE)
-        progress("survey %d steps; timing %s M=%d N=%d K=%d in every %dth step of the timed region" %
-                 (SURVEY_STEPS, top["name"], top["M"], top["N"], top["K"], TIMED_STRIDE))
+        if graphs:
+            # Graph replays carry no per-kernel events: the timed region runs without
+            # timing, and the roofline takes the dominant kernel's survey average.
+            g.profile_enable(False, 0)
+            progress("survey %d steps; timed region replays graphs, no kernel events" % SURVEY_STEPS)
+        else:
+            g.profile_enable(True, reserve_launches=40 * steps)
+            g.profile_only(top["name"], top["M"], top["N"], top["K"])
+            g.profile_stride(TIMED_STRIDE)
+            progress("survey %d steps; timing %s M=%d N=%d K=%d in every %dth step of the timed region" %
+                     (SURVEY_STEPS, top["name"], top["M"], top["N"], top["K"], TIMED_STRIDE))
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -259,10 +303,23 @@ def main():
     elapsed_ms = t_start.elapsed_time(t_end)
     progress("timed %d steps: %.3f ms/step" % (steps, elapsed_ms / steps))
 
-    stats = g.profile_read() if top else []
+    stats = (g.profile_read() if not graphs else [dict(top)]) if top else []
     rec = g.read_losses(g.step() - steps + 1, steps)
     finite = bool((rec[:, 6] == 0).all())
+    sweep_out = None
+    if large and not args.no_sweep:
+        g.profile_enable(False, 0)
+        sweep_out = sweep(g, w, stream)
     g.close()
+    streams2 = None
+    if large and args.streams == 1 and not args.no_streams2:
+        # The actor and critic halves on two concurrent streams (the one-GPU form of the
+        # paper's two-GPU actor/critic split), same workload, another context.
+        g2 = Spz(w.obs_dim, w.act_dim, w.hidden, w.batch, w.hparams(), args.seed, n_streams=2)
+        fill_ring(g2, w, args.data_seed, w.capacity)
+        streams2 = timed_rate(g2, w, stream, steps, args.warmup)
+        g2.close()
+        progress("two streams: %.3f ms/step" % streams2["ms_per_step"])
 
     value = frames_per_second(w.batch, steps, elapsed_ms / 1e3)
     prec = w.prec
@@ -273,9 +330,12 @@ def main():
                            act_dim=w.act_dim, hidden=list(w.hidden), replay_rows=w.capacity,
                            gemm_operands=prec, accumulate="fp32", master_weights="fp32",
                            streams=args.streams, seed=args.seed, data_seed=args.data_seed,
+                           graphs=int(graphs),
                            parallelism="single GPU; " + ("actor and critic on concurrent streams"
                                                          if args.streams == 2 else "one stream")),
                losses_finite=finite)
+    if not large:
+        out["us_per_step"] = round(elapsed_ms / steps * 1e3, 1)
     if stats:
         gemm_ms = sum(s["total_ms"] for s in survey if s["name"] in GEMMS)
         gemm_flops = sum(s["flops"] * s["launches"] for s in survey if s["name"] in GEMMS)
@@ -289,12 +349,19 @@ def main():
                  "Both leave out the row-restricted input-gradient products of the SAC actor path "
                  "(gemm_dgrad_rows: a data-dependent number of rows, about half the batch per critic)")
         out["roofline"] = roofline(stats, prec)
+        if graphs:
+            out["roofline"]["timed_every_steps"] = None
+            out["roofline"]["note"] = ("graph replays carry no kernel events: dominant kernel's mean event "
+                                       "duration over the survey pass")
+        out["hbm_kernels"] = hbm_kernels(survey)
         out["kernels"] = [dict(name=s["name"], M=s["M"], N=s["N"], K=s["K"], launches=s["launches"],
                                avg_ms=round(s["avg_ms"], 5), total_ms=round(s["total_ms"], 3))
                           for s in survey[:40]]
         out["kernels_note"] = "survey pass of %d untimed steps before the timed region" % SURVEY_STEPS
-    if args.sweep:
-        out["sweep"] = sweep(w, args, stream)
+    if sweep_out:
+        out["sweep"] = sweep_out
+    if streams2:
+        out["streams2"] = streams2
     if args.autotune:
         g = Spz(w.obs_dim, w.act_dim, w.hidden, w.batch, w.hparams(), args.seed, n_streams=args.streams)
         fill_ring(g, w, args.data_seed, w.capacity)

@@ -128,6 +128,14 @@ typedef struct spz_hparams {
                                      the same results as 0, which takes both critics
                                      over every row. Used where the ReLU masks are kept
                                      as bits (bf16 with 128-multiple hidden widths).  */
+  int32_t graphs;                 /* 1: spz_update replays each step from a captured HIP
+                                     graph (one per step kind: SAC has one, TD3 one with
+                                     and one without the delayed actor update) instead of
+                                     launching its kernels one by one; bit-identical
+                                     results. A graph is captured the first time a step
+                                     kind runs (that step itself runs eagerly) and again
+                                     after the batch size, the replay fill level or the
+                                     seed changed. Ignored while kernel timing is on.  */
 } spz_hparams;
 
 /* Update ordering within a step.
@@ -145,7 +153,7 @@ typedef struct spz_hparams {
 /* Defaults: SAC, fp32, capacity 1e6, gamma 0.99, tau 0.005, lr 3e-4, Adam
  * (0.9, 0.999, 1e-8), alpha_init 1, learned alpha, target_entropy 0, log-std
  * clamp [-20, 2], TD3 noise 0.2 clipped to 0.5, delay 2, device 0, 2 streams,
- * snapshot ordering, actor row split on. */
+ * snapshot ordering, actor row split on, no graphs. */
 void spz_hparams_default(spz_hparams* hp);
 
 /* Create a learner: the single network-update process of Section 3.2 (its actor

@@ -164,6 +164,12 @@ struct spz_ctx {
   // streams
   hipStream_t sc = nullptr, sa = nullptr;
   hipEvent_t ev_fork = nullptr, ev_c = nullptr, ev_a = nullptr;
+  // Captured update steps (hp.graphs): one executable graph per step kind (index:
+  // 1 when the step updates the actor), valid for the batch, fill level and seed it
+  // was captured with (they are kernel arguments); captured on stream sg.
+  struct GraphSlot { hipGraphExec_t exec = nullptr; int B = 0, Bp = 0; int64_t size = 0; uint64_t seed = 0; };
+  GraphSlot gslot[2];
+  hipStream_t sg = nullptr;
   hipStream_t last = nullptr;
   bool has_last = false;   // an update was enqueued on `last` (which may be the null stream)
   std::vector<void*> cs_hid;   // ping-pong view of cs_h, one entry per hidden layer
@@ -738,6 +744,53 @@ int enqueue_step(spz_ctx* c, hipStream_t s0) {
   return SPZ_OK;
 }
 
+// One update step from a captured graph (hp.graphs). Kernel arguments are fixed at
+// capture: buffer addresses, shapes (batch), the replay fill level and the seed; the
+// step number, which the kernels read from device memory, is not. A missing or stale
+// graph for this step kind is replaced: the step runs eagerly (which also performs
+// every first-launch set-up of its kernels outside the capture), then the same step
+// kind is captured on sg for the next time.
+int graph_step(spz_ctx* c, hipStream_t s0) {
+  const int64_t t = c->h_step + 1;
+  const int kind = (!c->td3 || t % c->hp.policy_delay == 0) ? 1 : 0;
+  spz_ctx::GraphSlot& gs = c->gslot[kind];
+  const bool fresh = gs.exec && gs.B == c->B && gs.Bp == c->Bp && gs.size == c->size && gs.seed == c->seed;
+  if (fresh) {
+    CK(hipGraphLaunch(gs.exec, s0));
+    c->h_step = t;
+    return SPZ_OK;
+  }
+  int rc = enqueue_step(c, s0);
+  if (rc) return rc;
+  if (gs.exec) {
+    CK(hipGraphExecDestroy(gs.exec));
+    gs.exec = nullptr;
+  }
+  // Capture step t's kind again (the capture enqueues nothing).
+  c->h_step = t - 1;
+  CK(hipStreamBeginCapture(c->sg, hipStreamCaptureModeThreadLocal));
+  rc = enqueue_step(c, c->sg);
+  hipGraph_t graph = nullptr;
+  const hipError_t ec = hipStreamEndCapture(c->sg, &graph);
+  c->h_step = t;
+  if (rc) {
+    if (graph) (void)hipGraphDestroy(graph);
+    return rc;
+  }
+  if (ec != hipSuccess) return fail_hip(c, ec, "hipStreamEndCapture");
+  const hipError_t ei = hipGraphInstantiate(&gs.exec, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  if (ei != hipSuccess) {
+    gs.exec = nullptr;
+    return fail_hip(c, ei, "hipGraphInstantiate");
+  }
+  gs.B = c->B;
+  gs.Bp = c->Bp;
+  gs.size = c->size;
+  gs.seed = c->seed;
+  return SPZ_OK;
+}
+
 int ctx_sync(spz_ctx* c) {
   if (c->has_last) CK(hipStreamSynchronize(c->last));
   if (c->si) CK(hipStreamSynchronize(c->si));
@@ -884,6 +937,7 @@ int setup(spz_ctx* c) {
   // streams (default priority)
   CK(hipStreamCreateWithFlags(&c->sc, hipStreamNonBlocking));
   CK(hipStreamCreateWithFlags(&c->sa, hipStreamNonBlocking));
+  if (c->hp.graphs) CK(hipStreamCreateWithFlags(&c->sg, hipStreamNonBlocking));
   CK(hipEventCreateWithFlags(&c->ev_fork, hipEventDisableTiming));
   CK(hipEventCreateWithFlags(&c->ev_c, hipEventDisableTiming));
   CK(hipEventCreateWithFlags(&c->ev_a, hipEventDisableTiming));
@@ -917,6 +971,9 @@ void release(spz_ctx* c) {
     if (sl.done) (void)hipEventDestroy(sl.done);
   }
   if (c->si) (void)hipStreamDestroy(c->si);
+  for (auto& gs : c->gslot)
+    if (gs.exec) (void)hipGraphExecDestroy(gs.exec);
+  if (c->sg) (void)hipStreamDestroy(c->sg);
   if (c->ev_commit) (void)hipEventDestroy(c->ev_commit);
   for (void* p : c->allocs) (void)hipFree(p);
   if (c->stage) (void)hipFree(c->stage);
@@ -988,6 +1045,7 @@ void spz_hparams_default(spz_hparams* hp) {
   hp->n_streams = 2;
   hp->ordering = SPZ_ORDER_SNAPSHOT;
   hp->actor_row_split = 1;
+  hp->graphs = 0;
 }
 
 spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int32_t n_hidden, int32_t batch,
@@ -1009,7 +1067,7 @@ spz_ctx* spz_create(int32_t obs_dim, int32_t act_dim, const int32_t* hidden, int
       (hp->algo == SPZ_ALGO_SAC && !(hp->alpha_init > 0.0f)) || hp->policy_delay < 1 ||
       (hp->n_streams != 1 && hp->n_streams != 2) || !(hp->log_std_min <= hp->log_std_max) ||
       (hp->ordering != SPZ_ORDER_SNAPSHOT && hp->ordering != SPZ_ORDER_SEQUENTIAL) ||
-      (hp->actor_row_split != 0 && hp->actor_row_split != 1)) {
+      (hp->actor_row_split != 0 && hp->actor_row_split != 1) || (hp->graphs != 0 && hp->graphs != 1)) {
     set_err(nullptr, SPZ_EINVAL, "spz_create: invalid hyper-parameters");
     return nullptr;
   }
@@ -1193,7 +1251,7 @@ int spz_update(spz_ctx* c, int32_t n_steps, void* hip_stream) {
   c->last = s0;
   c->has_last = true;
   for (int i = 0; i < n_steps; ++i) {
-    const int rc = enqueue_step(c, s0);
+    const int rc = c->hp.graphs && !c->prof ? graph_step(c, s0) : enqueue_step(c, s0);
     if (rc) return rc;
   }
   return SPZ_OK;

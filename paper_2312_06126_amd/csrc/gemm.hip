@@ -286,19 +286,40 @@ hipError_t launch_bn(const GemmArgs& g, int bn, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+// Largest K-split the weight-gradient product allows: K % (32 s) == 0 with at
+// least 256 batch rows per slice.
+int max_splits(int K) {
+  int s = 1;
+  while (K % (2 * s * BK) == 0 && K / (2 * s) >= 256) s *= 2;
+  return s;
+}
+
+// Tile of a generic-kernel product: the largest (up to 128 x 128) whose grid still
+// gives about two workgroups per CU (512), halving the larger side first. A 128 x 128
+// tile over a batch of 8192 and 256 features is only 128 workgroups of one wave per
+// SIMD: half the CUs idle and a quarter of the matrix-core issue slots used.
+constexpr int GEN_TARGET_WGS = 512;
+void generic_tiles(GemmMode mode, int M, int N, int K, int* bm, int* bn) {
+  *bm = mode == GEMM_WGRAD ? pick_tile(M) : 128;
+  *bn = pick_tile(N);
+  if (!*bm || !*bn) return;
+  const int64_t s = mode == GEMM_WGRAD ? max_splits(K) : 1;
+  while ((int64_t)(M / *bm) * (N / *bn) * s < GEN_TARGET_WGS && (*bm > 32 || *bn > 32)) {
+    if (*bm >= *bn && *bm > 32) *bm /= 2;
+    else *bn /= 2;
+  }
+}
+
 template <typename T, int MODE>
 hipError_t launch_mode(const GemmArgs& g, hipStream_t s) {
-  const int bn = pick_tile(g.N);
-  if constexpr (MODE == GEMM_WGRAD) {
-    switch (pick_tile(g.M)) {
-      case 128: return launch_bn<T, MODE, 128>(g, bn, s);
-      case 64: return launch_bn<T, MODE, 64>(g, bn, s);
-      case 32: return launch_bn<T, MODE, 32>(g, bn, s);
-    }
-    return hipErrorInvalidValue;
-  } else {
-    return launch_bn<T, MODE, 128>(g, bn, s);
+  int bm = 0, bn = 0;
+  generic_tiles((GemmMode)MODE, g.M, g.N, g.K, &bm, &bn);
+  switch (bm) {
+    case 128: return launch_bn<T, MODE, 128>(g, bn, s);
+    case 64: return launch_bn<T, MODE, 64>(g, bn, s);
+    case 32: return launch_bn<T, MODE, 32>(g, bn, s);
   }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
@@ -311,7 +332,8 @@ int wgrad_splits(bool bf16, int M, int N, int K) {
     tiles = (M / 256) * ((N + bn - 1) / bn);
     target = 256;
   } else {
-    const int bm = pick_tile(M), bn = pick_tile(N);
+    int bm = 0, bn = 0;
+    generic_tiles(GEMM_WGRAD, M, N, K, &bm, &bn);
     if (!bm || !bn) return 1;
     tiles = (M / bm) * (N / bn);
     target = 1024;

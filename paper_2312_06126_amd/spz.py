@@ -50,7 +50,7 @@ class Hparams(ctypes.Structure):
                 ("log_std_min", ctypes.c_float), ("log_std_max", ctypes.c_float),
                 ("policy_noise", ctypes.c_float), ("noise_clip", ctypes.c_float),
                 ("policy_delay", ctypes.c_int32), ("device", ctypes.c_int32), ("n_streams", ctypes.c_int32),
-                ("ordering", ctypes.c_int32), ("actor_row_split", ctypes.c_int32)]
+                ("ordering", ctypes.c_int32), ("actor_row_split", ctypes.c_int32), ("graphs", ctypes.c_int32)]
 
 
 class KernelStat(ctypes.Structure):
@@ -126,7 +126,7 @@ def make_hparams(d: dict, device: int = 0, n_streams: int = 2) -> Hparams:
             v = ALGOS[v]
         elif k == "gemm_prec":
             v = PRECS[v]
-        elif k in ("learn_alpha", "actor_row_split"):
+        elif k in ("learn_alpha", "actor_row_split", "graphs"):
             v = int(bool(v))
         elif k == "ordering":
             v = ORDERINGS[v]
