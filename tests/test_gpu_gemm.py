@@ -107,8 +107,12 @@ def test_wgrad_bf16(env, M, N, K, splits):
     run(env, True, 2, M, N, K, splits=splits)
 
 
+# Ragged last tiles (the widest tile wasting at most 10%): N = 416 and 352 take 64- and
+# 128-wide tiles past the last column, M = 416 / 320 weight-gradient row tiles likewise.
 @pytest.mark.parametrize("mode,M,N,K,splits", [(0, 256, 416, 96, 1), (1, 256, 320, 416, 1), (2, 416, 96, 512, 2),
-                                               (0, 128, 32, 32, 1), (2, 32, 64, 256, 1)])
+                                               (0, 128, 32, 32, 1), (2, 32, 64, 256, 1),
+                                               (1, 1024, 416, 320, 1), (0, 1024, 416, 160, 1), (1, 512, 352, 96, 1),
+                                               (2, 416, 160, 2048, 4), (2, 320, 416, 4096, 8), (0, 32768, 416, 160, 1)])
 def test_fp32_generic(env, mode, M, N, K, splits):
     run(env, False, mode, M, N, K, splits=splits, relu=mode == 0, use_bias=mode == 0, use_mask=mode == 1)
 
