@@ -35,7 +35,7 @@ int spzt_gemm(int32_t bf16, int32_t mode, int32_t M, int32_t N, int32_t K, int32
  *   mode 0: C = ReLU(A . B^T + bias) in bf16 (bias may be null);
  *           bits_out (or null): bits of C > 0;
  *           rdot_w [N] bf16 (or null): rdot_part[p * ldrd + r] = sum over columns c of
- *             group p (spzt_rdot_cols(N) columns each) of C[r, c] * rdot_w[c];
+ *             group p (spzt_rdot_cols(M, N) columns each) of C[r, c] * rdot_w[c];
  *           no_store: C is not written (requires rdot_w).
  *   mode 1: C = (A . B) * bit(r, c) in bf16 (bits required; the hook builds the
  *           transposed image of B that the kernel reads);
@@ -57,8 +57,8 @@ int spzt_gemm_fused(int32_t mode, int32_t M, int32_t N, int32_t K, const void* A
 int spzt_gemm_dgrad_rows(int32_t bf16, int32_t M, int32_t N, int32_t K, const void* A, int64_t lda,
                          const void* B, int64_t ldb, void* C, int64_t ldc, const uint32_t* bits, int64_t ldbits,
                          int32_t out_f32, int32_t m_rows);
-/* Columns per row-dot partial of an N-column product. */
-int spzt_rdot_cols(int32_t N);
+/* Columns per row-dot partial of an M x N forward product (its column tile over 2). */
+int spzt_rdot_cols(int32_t M, int32_t N);
 /*
  * Checks the device float32 -> bfloat16 rounding used by every kernel against an
  * integer round-to-nearest-even over the float bit patterns [begin, begin + count)

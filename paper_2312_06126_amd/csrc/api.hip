@@ -407,7 +407,7 @@ hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, 
              [&] { return gemm(c->bf16, GEMM_FWD, g, s); }));
     if (folded) {
       const Lay& H = n.L[nl - 1];
-      RdotFinalArgs f{rdot, L.out_p / gemm_rdot_cols(L.out_p), c->Bp, c->Bp, wf(c, target, H.b), head};
+      RdotFinalArgs f{rdot, L.out_p / gemm_rdot_cols(c->Bp, L.out_p), c->Bp, c->Bp, wf(c, target, H.b), head};
       return timed(c, "rdot_final", c->Bp, f.parts, 0, 0.0, 4.0 * c->Bp * (f.parts + 1), s,
                    [&] { return launch_rdot_final(f, s); });
     }
@@ -901,7 +901,7 @@ int setup(spz_ctx* c) {
       CK(dalloc_t(c, &c->bhpc[i][l], bb));
     }
     CK(dalloc_t(c, &c->bha[l], bb));
-    if (l == nh - 1) rd_parts = w / gemm_rdot_cols(w);
+    if (l == nh - 1) rd_parts = w / 64;   // the most partials any batch size gives (gemm_rdot_cols)
   }
   if (rd_parts) {
     CK(dalloc_t(c, &c->c_rdot, (size_t)rd_parts * Bp * 4));

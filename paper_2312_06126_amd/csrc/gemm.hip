@@ -356,7 +356,7 @@ int wgrad_splits(bool bf16, int M, int N, int K) {
   int tiles, target;
   if (bf16 && big_gemm_fits(GEMM_WGRAD, M, N, K, 1)) {
     // large-tile kernel: about one workgroup per CU
-    const int bn = big_bn(N, false);
+    const int bn = big_bn(GEMM_WGRAD, M, N, false);
     tiles = (M / 256) * ((N + bn - 1) / bn);
     target = 256;
   } else {

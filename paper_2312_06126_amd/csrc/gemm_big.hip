@@ -777,7 +777,7 @@ hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
 
 }  // namespace
 
-int gemm_rdot_cols(int N) { return (N % 256 == 0 ? 256 : 128) / WN; }
+int gemm_rdot_cols(int M, int N) { return big_bn(GEMM_FWD, M, N, true) / WN; }
 
 bool big_epilogue_supported(GemmMode mode, int f) {
   switch (mode) {
@@ -805,8 +805,10 @@ bool big_gemm_colsum(GemmMode mode, int M, int N, int K) {
   return mode == GEMM_DGRAD && big_gemm_fits(mode, M, N, K, 1);
 }
 
-int big_bn(int N, bool fused) {
-  if (N % 256 == 0) return 256;
+int big_bn(GemmMode mode, int M, int N, bool fused) {
+  // 256-wide unless that grid leaves CUs idle: a 16384 x 256 forward is 64 workgroups of
+  // 256 x 256 on 256 CUs (the weight gradient splits K to fill the GPU instead).
+  if (N % 256 == 0) return mode == GEMM_WGRAD || (int64_t)(M / BM) * (N / 256) >= 256 ? 256 : 128;
   if (fused) return 128;          // fused epilogues need whole column tiles (N % 128 == 0)
   return N > 256 ? 256 : 128;     // ragged last column tile
 }
@@ -833,7 +835,7 @@ hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s) {
   const int f = epilogue_flags(mode, g);
   const bool fused = f & (EPI_BITS | EPI_BITS_OUT | EPI_RDOT | EPI_CSUM | EPI_NOSTORE);
   if (fused && g.N % 128) return hipErrorInvalidValue;
-  const bool bn256 = big_bn(g.N, fused) == 256;
+  const bool bn256 = big_bn(mode, g.M, g.N, fused) == 256;
   switch (mode) {
     case GEMM_FWD: return bn256 ? launch_big<GEMM_FWD, 256>(g, s) : launch_big<GEMM_FWD, 128>(g, s);
     case GEMM_DGRAD: {

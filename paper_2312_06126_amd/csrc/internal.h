@@ -111,7 +111,7 @@ struct GemmArgs {
   const uint32_t* bits;        // DGRAD: C *= mask bit (instead of mask)
   int64_t ldbits;
   const void* rdot_w;          // FWD with relu: rdot_part[p, r] = sum over the p-th group of
-  float* rdot_part;            // gemm_rdot_cols(N) columns c of stored C[r, c] * rdot_w[c]
+  float* rdot_part;            // gemm_rdot_cols(M, N) columns c of stored C[r, c] * rdot_w[c]
   int64_t ldrd;
   int no_store;                // FWD with rdot_w: C is not written
   // DGRAD: when set, only rows [0, *m_dyn) of C are computed (a device-side count,
@@ -152,9 +152,10 @@ int wgrad_splits(bool bf16, int M, int N, int K);
 // Large-tile bf16 kernel (gemm_big.hip): M % 256 == 0, N >= 128 with N % 8 == 0 (a
 // ragged last column tile reads zeros and stores nothing past N), K slices of 32.
 bool big_gemm_fits(GemmMode mode, int M, int N, int K, int splits);
-// Its column tile: 256 when N % 256 == 0; with fused epilogue features 128 (they
+// Its column tile: 256 when N % 256 == 0 (forward and input gradient: only while the
+// grid still has a workgroup per CU, else 128); with fused epilogue features 128 (they
 // need N % 128 == 0); otherwise 256 above N = 256 and 128 below.
-int big_bn(int N, bool fused);
+int big_bn(GemmMode mode, int M, int N, bool fused);
 // True when gemm() with these arguments can produce the fused column sums (GemmArgs::colsum).
 bool gemm_colsum_fused(bool bf16, GemmMode mode, int M, int N, int K);
 bool big_gemm_colsum(GemmMode mode, int M, int N, int K);
@@ -165,8 +166,9 @@ hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s);
 // True when a product of this shape runs entirely on the large-tile kernel, so that
 // bits_out / bits / rdot_w / no_store / colsum may be used.
 bool gemm_fused_ok(bool bf16, GemmMode mode, int M, int N, int K);
-// Columns per row-dot partial for an N-column product (N / gemm_rdot_cols partials).
-int gemm_rdot_cols(int N);
+// Columns per row-dot partial for an M x N forward (N / gemm_rdot_cols partials; at
+// least N / 64, the most any shape uses).
+int gemm_rdot_cols(int M, int N);
 // True when the large-tile kernel has an epilogue for these flags.
 bool big_epilogue_supported(GemmMode mode, int flags);
 

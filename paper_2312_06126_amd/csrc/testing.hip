@@ -115,7 +115,7 @@ extern "C" int spzt_gemm_dgrad_rows(int32_t bf16, int32_t M, int32_t N, int32_t 
   return e == hipSuccess ? SPZ_OK : SPZ_EHIP;
 }
 
-extern "C" int spzt_rdot_cols(int32_t N) { return gemm_rdot_cols(N); }
+extern "C" int spzt_rdot_cols(int32_t M, int32_t N) { return gemm_rdot_cols(M, N); }
 
 // Rounding check of the device float32 -> bfloat16 conversion against an integer
 // round-to-nearest-even written out here: every input bit pattern in

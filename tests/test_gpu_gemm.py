@@ -133,7 +133,7 @@ def fused(env):
     f = lib.spzt_gemm_fused
     f.argtypes = [I32, I32, I32, I32, P, I64, P, I64, P, I64, P, P, P, I64, P, P, I64, I32, P, I64]
     f.restype = ctypes.c_int
-    lib.spzt_rdot_cols.argtypes = [I32]
+    lib.spzt_rdot_cols.argtypes = [I32, I32]
     lib.spzt_rdot_cols.restype = ctypes.c_int
     return torch, f, lib.spzt_rdot_cols
 
@@ -149,7 +149,9 @@ def dev_ptr(t):
     return t.data_ptr() if t is not None else None
 
 
-@pytest.mark.parametrize("M,N,K", [(512, 512, 96), (256, 384, 64), (768, 1024, 416)])
+# (16384, 1024, 256): a grid with a workgroup per CU, where the kernel takes 256-wide column
+# tiles; the smaller products take 128-wide ones.
+@pytest.mark.parametrize("M,N,K", [(512, 512, 96), (256, 384, 64), (768, 1024, 416), (16384, 1024, 256)])
 @pytest.mark.parametrize("bits,rdot,no_store", [(True, False, False), (False, True, False), (False, True, True),
                                                 (True, True, False), (True, True, True)])
 def test_forward_fused_epilogue(fused, M, N, K, bits, rdot, no_store):
@@ -167,15 +169,19 @@ def test_forward_fused_epilogue(fused, M, N, K, bits, rdot, no_store):
     dw = to_dev(torch, w, True)
     dC = torch.full((M, N), 7.0, dtype=torch.bfloat16, device="cuda")
     dbits = torch.zeros((N // 32, M), dtype=torch.int32, device="cuda") if bits else None
-    cols = rdot_cols(N)
+    cols = rdot_cols(M, N)
     parts = N // cols
     dpart = torch.zeros((parts, M), dtype=torch.float32, device="cuda") if rdot else None
     rc = f(0, M, N, K, dA.data_ptr(), K, dB.data_ptr(), K, dC.data_ptr(), N, dbias.data_ptr(), dev_ptr(dbits), None,
            M, dev_ptr(dw) if rdot else None, dev_ptr(dpart), M, int(no_store), None, 0)
     assert rc == 0, rc
-    ref = np.maximum(rounded(torch, A, True) @ rounded(torch, B, True).T + bias, 0.0)
+    pre = rounded(torch, A, True) @ rounded(torch, B, True).T + bias
+    ref = np.maximum(pre, 0.0)
     ref_b = rounded(torch, ref, True)
     got = dC.to(torch.float64).cpu().numpy()
+    # ReLU of a pre-activation within float32 accumulation error of zero may fall either
+    # way (a few of the 16.7M values of the largest shape)
+    near0 = np.abs(pre) <= 1e-4 * np.sqrt(np.mean(pre * pre))
     if no_store:
         assert np.all(got == 7.0)
         # the stored values the epilogue used are not visible: compare the row dots
@@ -183,7 +189,7 @@ def test_forward_fused_epilogue(fused, M, N, K, bits, rdot, no_store):
         cval = ref_b
     else:
         ulp = np.abs(ref_b) * 2.0 ** -7 + 1e-30
-        assert np.all(np.abs(got - ref_b) <= 2 * ulp + 1e-6)
+        assert np.all((np.abs(got - ref_b) <= 2 * ulp + 1e-6) | near0)
         cval = got
     if bits:
         words = dbits.cpu().numpy().view(np.uint32)
@@ -203,7 +209,7 @@ def test_forward_fused_epilogue(fused, M, N, K, bits, rdot, no_store):
         assert np.abs(part - want).max() <= tol * scale, np.abs(part - want).max() / scale
 
 
-@pytest.mark.parametrize("M,N,K", [(512, 512, 64), (256, 1024, 1024), (512, 384, 96)])
+@pytest.mark.parametrize("M,N,K", [(512, 512, 64), (256, 1024, 1024), (512, 384, 96), (16384, 1024, 256)])
 @pytest.mark.parametrize("colsum", [False, True])
 def test_dgrad_bits_equal_mask(env, fused, M, N, K, colsum):
     """A dgrad masked by bits is bit-identical to the same dgrad masked by a bf16
