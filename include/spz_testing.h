@@ -10,7 +10,9 @@
  *                                                        reduced in slice order)
  * bf16 != 0: A, B, mask (and C unless out_f32 or mode 2) are bfloat16; else float32.
  * bf16 mode 1: the hook also builds the transposed image of B (a temporary device
- * buffer), which the large-tile kernel reads.
+ * buffer), which the large-tile kernel reads. mode 3: mode 1 with B passed through its
+ * transposed image in either precision (the k-contiguous input-gradient path the
+ * library takes for hidden layers).
  * Leading dimensions are in elements. Shapes must satisfy the kernels' tiling
  * contract (M and N multiples of 32 with M % 128 == 0 for modes 0 and 1, K a
  * multiple of 32 * splits); otherwise SPZ_EINVAL. Synchronous.

@@ -97,11 +97,13 @@ struct spz_ctx {
   // parameters
   float *P = nullptr, *G = nullptr, *M = nullptr, *V = nullptr, *T = nullptr;
   bf16_t *Pb = nullptr, *Tb = nullptr;
-  // bf16 contexts: transposed images of the online weights the input-gradient
-  // products read (layer l >= 1 of each net, the critics' output layers aside), at
-  // the same arena offsets as Pb: PbT + L.w holds W^T [in_p, out_p]. Refreshed
-  // whenever Pb changes.
-  bf16_t* PbT = nullptr;
+  // bf16 contexts: transposed images of the online weights the input-gradient products
+  // read (layer l >= 1 of each net, the critics' output layers aside), at the same
+  // arena offsets as Pb: WT + L.w holds W^T [in_p, out_p], so that those products read
+  // both operands k-contiguous (the large-tile kernel needs it). Refreshed whenever P
+  // changes. float32 contexts read W itself: there the per-step transpose costs about
+  // what the k-contiguous reads save.
+  void* WT = nullptr;
   TransposeJob* tjobs = nullptr;
   int n_tjobs = 0, t_tiles = 0;
   double t_elems = 0.0;
@@ -352,12 +354,13 @@ const void* elem(const spz_ctx* c, const void* base, int64_t off) {
 
 // Transposed weight images (bf16 contexts) from Pb.
 hipError_t refresh_wt(spz_ctx* c, hipStream_t s) {
-  if (!c->bf16 || !c->n_tjobs) return hipSuccess;
+  if (!c->WT || !c->n_tjobs) return hipSuccess;
   return timed(c, "transpose", c->n_tjobs, 0, 0, 0.0, 4.0 * c->t_elems, s,
-               [&] { return launch_transpose_bf16(c->Pb, c->PbT, c->tjobs, c->n_tjobs, c->t_tiles, s); });
+               [&] { return launch_transpose(true, c->Pb, c->WT, c->tjobs, c->n_tjobs, c->t_tiles, s); });
 }
-// Transposed image of the online layer L (the B operand of its input-gradient product).
-const void* wt(const spz_ctx* c, const Lay& L) { return c->bf16 ? c->PbT + L.w : nullptr; }
+// Transposed image of the online layer L (the B operand of its input-gradient
+// product), or null (float32 contexts).
+const void* wt(const spz_ctx* c, const Lay& L) { return c->WT ? elem(c, c->WT, L.w) : nullptr; }
 
 // Forward of net ni. X: [Bp, ldx] operand tensor (the first in_p(0) columns are read).
 // hid[l] receives hidden layer l and, where bits[l] is set, its ReLU mask as bits;
@@ -438,8 +441,8 @@ hipError_t wgrad(spz_ctx* c, const void* dz, int64_t lddz, const void* X, int64_
 }
 
 // Input gradient through layer L: out[Bp, N] = (dz . W) masked by mask > 0 (or by
-// the mask bits when given). Wt (or null): the transposed image of W, which the
-// large-tile kernel reads. With
+// the mask bits when given). Wt (or null): the transposed image of W, which both
+// GEMM kernels read instead of W. With
 // bias_out, also the column sums of the stored out (the bias gradient of the layer
 // below): fused into the product's epilogue where the large-tile kernel covers it.
 // With m_dyn (a device-side count of leading rows), only those rows are computed.
@@ -822,7 +825,7 @@ int setup(spz_ctx* c) {
   if (c->bf16) {
     CK(dalloc_t(c, &c->Pb, (size_t)c->n_arena * 2));
     CK(dalloc_t(c, &c->Tb, (size_t)c->n_arena * 2));
-    CK(dalloc_t(c, &c->PbT, (size_t)c->n_arena * 2));
+    CK(dalloc(c, &c->WT, (size_t)c->n_arena * 2));
     std::vector<TransposeJob> jobs;
     int tiles = 0;
     for (int ni = 0; ni < 3; ++ni) {

@@ -118,12 +118,14 @@ template <int BM, int BN> struct Shape {
 
 // RG: a last row tile (weight gradient) or column tile may reach past M or N (both
 // multiples of 32); operand reads there are clamped and the epilogue stores nothing there.
-template <typename T, int MODE, int BM, int BN, bool RG>
+// BT (input gradient): B is the transposed weight image [N, K], read k-contiguous like
+// the forward's weight (16-byte fragment reads instead of element-wise ones).
+template <typename T, int MODE, int BM, int BN, bool RG, bool BT>
 __global__ void __launch_bounds__(gemm_threads(BM, BN)) k_gemm(GemmArgs g) {
   using S = Shape<BM, BN>;
   constexpr int TM = S::TM, TN = S::TN, NT = S::NT;
   constexpr bool AKC = MODE != GEMM_WGRAD;
-  constexpr bool BKC = MODE == GEMM_FWD;
+  constexpr bool BKC = MODE == GEMM_FWD || BT;
   using TA = Tile<T, AKC, BM, NT>;
   using TB = Tile<T, BKC, BN, NT>;
   __shared__ __attribute__((aligned(16))) T lds_a[TA::SIZE];
@@ -295,12 +297,25 @@ int fit_tile(int n) {
   return 32;
 }
 
+template <typename T, int MODE, int BM, int BN, bool BT>
+hipError_t launch_rg(const GemmArgs& g, hipStream_t s) {
+  dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, MODE == GEMM_WGRAD ? g.splits : 1);
+  if (g.N % BN || g.M % BM) k_gemm<T, MODE, BM, BN, true, BT><<<grid, Shape<BM, BN>::NT, 0, s>>>(g);
+  else k_gemm<T, MODE, BM, BN, false, BT><<<grid, Shape<BM, BN>::NT, 0, s>>>(g);
+  return hipGetLastError();
+}
+
 template <typename T, int MODE, int BM, int BN>
 hipError_t launch(const GemmArgs& g, hipStream_t s) {
-  dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, MODE == GEMM_WGRAD ? g.splits : 1);
-  if (g.N % BN || g.M % BM) k_gemm<T, MODE, BM, BN, true><<<grid, Shape<BM, BN>::NT, 0, s>>>(g);
-  else k_gemm<T, MODE, BM, BN, false><<<grid, Shape<BM, BN>::NT, 0, s>>>(g);
-  return hipGetLastError();
+  if constexpr (MODE == GEMM_DGRAD) {
+    if (g.Bt) {
+      GemmArgs t = g;
+      t.B = g.Bt;
+      t.ldb = g.ldbt;
+      return launch_rg<T, MODE, BM, BN, true>(t, s);
+    }
+  }
+  return launch_rg<T, MODE, BM, BN, false>(g, s);
 }
 
 template <typename T, int MODE, int BM>
@@ -379,6 +394,7 @@ hipError_t gemm_generic(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t
     if (!pick_tile(g.M) || g.splits < 1 || g.K % (g.splits * BK)) return hipErrorInvalidValue;
   } else {
     if (g.M % 128 || g.K % BK) return hipErrorInvalidValue;
+    if (mode == GEMM_DGRAD && g.Bt && (g.ldbt % (bf16 ? 8 : 4) || g.ldbt < g.K)) return hipErrorInvalidValue;
   }
   if (bf16) {
     switch (mode) {

@@ -91,9 +91,10 @@ enum GemmMode { GEMM_FWD = 0, GEMM_DGRAD = 1, GEMM_WGRAD = 2 };
 struct GemmArgs {
   const void* A; int64_t lda;
   const void* B; int64_t ldb;
-  // DGRAD (bf16 large-tile kernel): the same B operand transposed, Bt[N, K] (row n
-  // = column n of B), which that kernel reads instead of B. Without it the product
-  // runs on the generic kernel (and the large-tile epilogue features are refused).
+  // DGRAD: the same B operand transposed, Bt[N, K] (row n = column n of B), read
+  // instead of B (k-contiguous, like the forward's weight). The bf16 large-tile kernel
+  // needs it: without it the product runs on the generic kernel (and the large-tile
+  // epilogue features are refused).
   const void* Bt; int64_t ldbt;
   void* C; int64_t ldc;
   const float* bias;           // FWD: bias [N] (fp32)

@@ -166,12 +166,13 @@ hipError_t launch_adam(const AdamArgs& a, hipStream_t s);
 hipError_t launch_finish(const FinishArgs& f, hipStream_t s);
 hipError_t launch_to_bf16(const float* src, bf16_t* dst, int64_t n, hipStream_t s);
 
-// Transposed bf16 images: job j writes dst[dst_off + c * ldd + r] = src[src_off + r * lds + c]
+// Transposed weight images (operand type: bfloat16 or float32): job j writes
+// dst[dst_off + c * ldd + r] = src[src_off + r * lds + c]
 // for r < rows, c < cols (the [cols, rows] transpose of a [rows, cols] matrix); the
 // jobs' 64 x 64 tiles are numbered consecutively from tile0 (ascending with j).
 struct TransposeJob { int64_t src_off, dst_off, lds, ldd; int rows, cols, tile0; };
 inline int transpose_tiles(int rows, int cols) { return ((rows + 63) / 64) * ((cols + 63) / 64); }
-hipError_t launch_transpose_bf16(const bf16_t* src, bf16_t* dst, const TransposeJob* jobs, int njobs, int tiles,
-                                 hipStream_t s);
+hipError_t launch_transpose(bool bf16, const void* src, void* dst, const TransposeJob* jobs, int njobs, int tiles,
+                            hipStream_t s);
 
 }  // namespace spz

@@ -754,9 +754,10 @@ __global__ void __launch_bounds__(256) k_to_bf16(const float* __restrict__ src, 
 
 // One 64 x 64 tile of one transpose job per workgroup, through an LDS tile: reads of
 // 64 consecutive columns per row and writes of 64 consecutive rows per column.
-__global__ void __launch_bounds__(256) k_transpose_bf16(const bf16_t* __restrict__ src, bf16_t* __restrict__ dst,
-                                                        const TransposeJob* __restrict__ jobs, int njobs) {
-  __shared__ bf16_t tile[64][66];
+template <typename T>
+__global__ void __launch_bounds__(256) k_transpose(const T* __restrict__ src, T* __restrict__ dst,
+                                                   const TransposeJob* __restrict__ jobs, int njobs) {
+  __shared__ T tile[64][65 + (sizeof(T) == 2 ? 1 : 0)];
   const int t = blockIdx.x;
   int j = 0;
   while (j + 1 < njobs && jobs[j + 1].tile0 <= t) ++j;
@@ -911,10 +912,13 @@ hipError_t launch_to_bf16(const float* src, bf16_t* dst, int64_t n, hipStream_t 
   return hipGetLastError();
 }
 
-hipError_t launch_transpose_bf16(const bf16_t* src, bf16_t* dst, const TransposeJob* jobs, int njobs, int tiles,
-                                 hipStream_t s) {
+hipError_t launch_transpose(bool bf16, const void* src, void* dst, const TransposeJob* jobs, int njobs, int tiles,
+                            hipStream_t s) {
   if (njobs < 1 || tiles < 1) return hipErrorInvalidValue;
-  k_transpose_bf16<<<tiles, 256, 0, s>>>(src, dst, jobs, njobs);
+  if (bf16)
+    k_transpose<bf16_t><<<tiles, 256, 0, s>>>(static_cast<const bf16_t*>(src), static_cast<bf16_t*>(dst), jobs, njobs);
+  else
+    k_transpose<float><<<tiles, 256, 0, s>>>(static_cast<const float*>(src), static_cast<float*>(dst), jobs, njobs);
   return hipGetLastError();
 }
 

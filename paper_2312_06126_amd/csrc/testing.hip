@@ -5,18 +5,18 @@
 using namespace spz;
 
 namespace {
-// The transposed image Bt [N, K] of a bf16 input-gradient operand B [K, N] (ldb),
-// which the large-tile kernel reads; *bt must be freed by the caller.
-hipError_t make_bt(const void* B, int64_t ldb, int K, int N, bf16_t** bt) {
+// The transposed image Bt [N, K] of an input-gradient operand B [K, N] (ldb), which
+// the large-tile kernel and the generic kernel's k-contiguous input-gradient path read;
+// *bt must be freed by the caller.
+hipError_t make_bt(bool bf16, const void* B, int64_t ldb, int K, int N, void** bt) {
   *bt = nullptr;
   if (K <= 0 || N <= 0) return hipErrorInvalidValue;
   TransposeJob job{0, 0, ldb, K, K, N, 0};
   TransposeJob* dj = nullptr;
-  hipError_t e = hipMalloc(reinterpret_cast<void**>(bt), (size_t)K * N * 2);
+  hipError_t e = hipMalloc(bt, (size_t)K * N * (bf16 ? 2 : 4));
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&dj), sizeof(job));
   if (e == hipSuccess) e = hipMemcpy(dj, &job, sizeof(job), hipMemcpyHostToDevice);
-  if (e == hipSuccess)
-    e = launch_transpose_bf16(static_cast<const bf16_t*>(B), *bt, dj, 1, transpose_tiles(K, N), nullptr);
+  if (e == hipSuccess) e = launch_transpose(bf16, B, *bt, dj, 1, transpose_tiles(K, N), nullptr);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (dj) (void)hipFree(dj);
   if (e != hipSuccess && *bt) {
@@ -30,20 +30,24 @@ hipError_t make_bt(const void* B, int64_t ldb, int K, int N, bf16_t** bt) {
 extern "C" int spzt_gemm(int32_t bf16, int32_t mode, int32_t M, int32_t N, int32_t K, int32_t splits,
                          const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                          const float* bias, const void* mask, int64_t ldm, int32_t relu, int32_t out_f32) {
-  if (mode < 0 || mode > 2 || splits < 1 || !A || !B || !C) return SPZ_EINVAL;
+  if (mode < 0 || mode > 3 || splits < 1 || !A || !B || !C) return SPZ_EINVAL;
+  // mode 3: the input gradient with B passed as its transposed image (bf16 mode 1 does
+  // that always: the large-tile kernel needs it)
+  const bool via_bt = mode == 3 || (bf16 && mode == GEMM_DGRAD);
+  if (mode == 3) mode = GEMM_DGRAD;
   GemmArgs g{};
   g.A = A; g.lda = lda; g.B = B; g.ldb = ldb; g.C = C; g.ldc = ldc;
   g.bias = bias; g.mask = mask; g.ldm = ldm; g.M = M; g.N = N; g.K = K;
   g.relu = relu; g.out_f32 = out_f32; g.splits = splits;
   float* part = nullptr;
-  bf16_t* bt = nullptr;
+  void* bt = nullptr;
   if (mode == GEMM_WGRAD) {
     if (hipMalloc(&part, (size_t)splits * M * N * 4) != hipSuccess) return SPZ_ENOMEM;
     g.C = part;
     g.ldc = N;
   }
   hipError_t e = hipSuccess;
-  if (bf16 && mode == GEMM_DGRAD && (e = make_bt(B, ldb, K, N, &bt)) == hipSuccess) {
+  if (via_bt && (e = make_bt(bf16 != 0, B, ldb, K, N, &bt)) == hipSuccess) {
     g.Bt = bt;
     g.ldbt = K;
   }
@@ -76,9 +80,9 @@ extern "C" int spzt_gemm_fused(int32_t mode, int32_t M, int32_t N, int32_t K, co
   }
   g.ldbits = ldbits;
   if (!gemm_fused_ok(true, (GemmMode)mode, M, N, K)) return SPZ_EINVAL;
-  bf16_t* bt = nullptr;
+  void* bt = nullptr;
   hipError_t e = hipSuccess;
-  if (mode == GEMM_DGRAD && (e = make_bt(B, ldb, K, N, &bt)) == hipSuccess) {
+  if (mode == GEMM_DGRAD && (e = make_bt(true, B, ldb, K, N, &bt)) == hipSuccess) {
     g.Bt = bt;
     g.ldbt = K;
   }
@@ -98,12 +102,12 @@ extern "C" int spzt_gemm_dgrad_rows(int32_t bf16, int32_t M, int32_t N, int32_t 
   g.M = M; g.N = N; g.K = K; g.out_f32 = out_f32;
   g.bits = bits; g.ldbits = ldbits;
   int32_t* rows = nullptr;
-  bf16_t* bt = nullptr;
+  void* bt = nullptr;
   hipError_t e = hipMalloc(reinterpret_cast<void**>(&rows), sizeof(int32_t));
   if (e != hipSuccess) return SPZ_ENOMEM;
   e = hipMemcpy(rows, &m_rows, sizeof(int32_t), hipMemcpyHostToDevice);
   g.m_dyn = rows;
-  if (e == hipSuccess && bf16 && (e = make_bt(B, ldb, K, N, &bt)) == hipSuccess) {
+  if (e == hipSuccess && bf16 && (e = make_bt(true, B, ldb, K, N, &bt)) == hipSuccess) {
     g.Bt = bt;
     g.ldbt = K;
   }

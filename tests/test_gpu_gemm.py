@@ -66,7 +66,7 @@ def run(env, bf16, mode, M, N, K, splits=1, relu=0, out_f32=0, use_bias=False, u
             ref = ref + bias
         if relu:
             ref = np.maximum(ref, 0.0)
-    elif mode == 1:
+    elif mode in (1, 3):
         ref = Ar @ Br
         if use_mask:
             ref = ref * (rounded(torch, mask, bf16) > 0)
@@ -115,6 +115,13 @@ def test_wgrad_bf16(env, M, N, K, splits):
                                                (2, 416, 160, 2048, 4), (2, 320, 416, 4096, 8), (0, 32768, 416, 160, 1)])
 def test_fp32_generic(env, mode, M, N, K, splits):
     run(env, False, mode, M, N, K, splits=splits, relu=mode == 0, use_bias=mode == 0, use_mask=mode == 1)
+
+
+# bf16 shapes the large-tile kernel refuses (M % 256, N < 128): the generic kernel
+# with the transposed image.
+@pytest.mark.parametrize("M,N,K", [(128, 416, 96), (384, 64, 256), (128, 1024, 64)])
+def test_bf16_dgrad_transposed_generic(env, M, N, K):
+    run(env, True, 3, M, N, K, use_mask=True)
 
 
 def test_rejects_bad_shapes(env):
