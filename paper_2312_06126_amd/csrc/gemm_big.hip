@@ -34,7 +34,9 @@
 //   * Epilogue: the forward's bias starts the accumulators; blocks leave in pairs
 //     through a per-wave LDS scratch as 16-byte row pieces (whole 128-byte lines per
 //     store); ReLU, mask bits, column sums and row dots work on rounded bf16 pairs
-//     (the epilogue is VALU-heavy); see epi_pair.
+//     (the epilogue is VALU-heavy); see epi_pair. Forward products that do not store
+//     C take transposed accumulators instead (each lane holds a row) and need no
+//     scratch; see epilogue_trans.
 #include "internal.h"
 
 namespace spz {
@@ -465,6 +467,101 @@ __device__ inline void epilogue(const GemmArgs& g, const f32x16 (&acc)[BM / WM /
   }
 }
 
+// Forward products that do not store C (row dots with the output layer, mask bits) take
+// the transposed accumulator layout: the MFMA computes the 32 x 32 block of C^T
+// (operands swapped), so lane l holds row l % 32 of the block and register q column
+// 8 (q / 4) + 4 (l / 32) + q % 4, and a row's dot product and mask word need no LDS
+// round trip (the scratch path costs these variants about 7% of the kernel). With a
+// stored C the same layout would write each 128-byte line in four 32-byte pieces from
+// four instructions, which measured 15-75% slower than whole-line stores (non-temporal
+// or plain), so those variants keep the scratch path.
+__host__ __device__ constexpr bool trans_epilogue(int mode, int f) {
+  return mode == GEMM_FWD && (f & EPI_NOSTORE);
+}
+
+// Swap the upper half-wave's x with the lower half-wave's y (v_permlane32_swap).
+__device__ inline void swap_halves(uint32_t& x, uint32_t& y) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, y, false, false);
+  x = r[0];
+  y = r[1];
+}
+
+template <int BN, int F, bool RG>
+__device__ inline void epilogue_trans(const GemmArgs& g, const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0,
+                                      int n0, int wm, int wn, int lane, uint32_t* in) {
+  using L = EpiLds<BN>;
+  constexpr int TM = BM / WM / 32, TN = BN / WN / 32, WCOLS = BN / WN;
+  constexpr bool RELU = F & EPI_RELU, BITS_OUT = F & EPI_BITS_OUT, RDOT = F & EPI_RDOT;
+  static_assert(F & EPI_NOSTORE, "C is not stored in this layout");
+  static_assert(!BITS_OUT || RELU, "mask bits out are taken of ReLU outputs");
+  static_assert(!RG, "fused epilogue features need whole column tiles");
+  const int h = lane >> 5, r = lane & 31;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int rl = wm * (BM / WM) + 32 * i + r;   // row within the tile
+    float rd = 0.0f;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int cb = wn * WCOLS + 32 * j;   // block's first column within the tile
+      // w[2 q4 + t]: columns 8 q4 + 4 h + 2 t and + 1, rounded to bf16 as a stored C
+      // would be (ReLU on the rounded pair: a bf16 is negative exactly when its bits are
+      // as int16)
+      uint32_t w[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        w[e] = pack_bf16x2(acc[i][j][2 * e], acc[i][j][2 * e + 1]);
+        if constexpr (RELU)
+          w[e] = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(i16x2, w[e]), i16x2{0, 0}));
+      }
+      if constexpr (RDOT) {
+        // Output-layer weights of the lane's 16 columns, packed bf16 pairs.
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const uint2 ww = *reinterpret_cast<const uint2*>(in + L::RDW + (cb + 8 * q4 + 4 * h) / 2);
+          rd = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[2 * q4]), __builtin_bit_cast(bf16x2, ww.x),
+                                               rd, false);
+          rd = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[2 * q4 + 1]),
+                                               __builtin_bit_cast(bf16x2, ww.y), rd, false);
+        }
+      }
+      if constexpr (BITS_OUT) {
+        // After ReLU a value is > 0 exactly when its bits are nonzero: halves clamped to
+        // 0 / 1 by one packed min, column c of the block at bit c.
+        uint32_t t = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          uint32_t m;
+          asm("v_pk_min_u16 %0, %1, %2" : "=v"(m) : "v"(w[e]), "s"(0x00010001u));
+          const int c = 8 * (e >> 1) + 4 * h + 2 * (e & 1);
+          t |= ((m & 1u) << c) | ((m >> 16) << (c + 1));
+        }
+        uint32_t u = t;
+        swap_halves(t, u);   // lower half-wave: own word in t, the upper's in u
+        if (h == 0) in[L::BITS + (cb >> 5) * BM + rl] = t | u;
+      }
+    }
+    if constexpr (RDOT) {
+      // per row, the sum over the wave's WCOLS columns; one partial per (column tile,
+      // wave column)
+      uint32_t a = __builtin_bit_cast(uint32_t, rd), b = a;
+      swap_halves(a, b);
+      const float o = __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+      const int part = (n0 + wn * WCOLS) / WCOLS;
+      if (h == 0) g.rdot_part[(int64_t)part * g.ldrd + m0 + rl] = o;
+    }
+  }
+  if constexpr (BITS_OUT) {
+    // The tile's mask words, one 16-byte piece per thread, row-contiguous per word column.
+    __syncthreads();
+    constexpr int NB = (BN / 32) * BM / 4;
+    for (int t = threadIdx.x; t < NB; t += NT) {
+      const int wc = t / (BM / 4), r4 = (t % (BM / 4)) * 4;
+      *reinterpret_cast<u32x4*>(g.bits_out + (int64_t)(n0 / 32 + wc) * g.ldbits + m0 + r4) =
+          *reinterpret_cast<const u32x4*>(in + L::BITS + 4 * t);
+    }
+  }
+}
+
 // Chunked main loop of the forward and input-gradient products, C = A . B^T with A
 // [M, K] and B [N, K] both k-contiguous (the input gradient takes the transposed
 // weight image): 64-deep chunks in two LDS stages, one barrier per chunk. Chunk c
@@ -480,7 +577,7 @@ struct ChunkLds {
   static constexpr int BYTES = ABYTES + FwdChunk<BN>::BYTES;
 };
 
-template <int BN, bool RG>
+template <int BN, bool RG, bool TRANS>
 __device__ inline void chunk_main_loop(const GemmArgs& g, f32x16 (&acc)[BM / WM / 32][BN / WN / 32], int m0,
                                        int n0, int wm, int wn, int wave, int lane, uint8_t* smem) {
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
@@ -512,7 +609,8 @@ __device__ inline void chunk_main_loop(const GemmArgs& g, f32x16 (&acc)[BM / WM 
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = TRANS ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0)
+                          : __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
   // One LDS read per MFMA (sched_group_barrier masks: 0x008 MFMA, 0x020 global load,
   // 0x100 LDS read).
@@ -569,6 +667,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   using TB = BigTile<BKC, BN>;
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
   constexpr int SE = TA::ELEMS + TB::ELEMS;   // elements per stage: A tile then B tile
+  constexpr bool TRANS = trans_epilogue(MODE, F);
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   bf16_t* S = reinterpret_cast<bf16_t*>(smem);
 
@@ -599,24 +698,41 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.A);
   const bf16_t* __restrict__ B = static_cast<const bf16_t*>(g.B);
 
-  // The forward's bias starts the accumulators (accumulator column = lane % 32).
+  // The forward's bias starts the accumulators (accumulator column = lane % 32; with
+  // transposed accumulators, register q holds column 8 (q / 4) + 4 (lane / 32) + q % 4).
   f32x16 acc[TM][TN];
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
-    float b = 0.0f;
-    if constexpr (MODE == GEMM_FWD) {
-      const int n = n0 + wn * (BN / WN) + 32 * j + (lane & 31);
-      if (g.bias && n < g.N) b = g.bias[n];
+    if constexpr (TRANS) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int n = n0 + wn * (BN / WN) + 32 * j + 8 * q4 + 4 * (lane >> 5);
+        float4 b = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (g.bias && n < g.N) b = *reinterpret_cast<const float4*>(g.bias + n);   // N % 8 == 0
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          acc[i][j][4 * q4] = b.x;
+          acc[i][j][4 * q4 + 1] = b.y;
+          acc[i][j][4 * q4 + 2] = b.z;
+          acc[i][j][4 * q4 + 3] = b.w;
+        }
+      }
+    } else {
+      float b = 0.0f;
+      if constexpr (MODE == GEMM_FWD) {
+        const int n = n0 + wn * (BN / WN) + 32 * j + (lane & 31);
+        if (g.bias && n < g.N) b = g.bias[n];
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[i][j][q] = b;
     }
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int q = 0; q < 16; ++q) acc[i][j][q] = b;
   }
 
   EpiPrefetch<MODE, BN, F> pre;
   if constexpr (MODE != GEMM_WGRAD) {
-    chunk_main_loop<BN, RG>(g, acc, m0, n0, wm, wn, wave, lane, smem);
+    chunk_main_loop<BN, RG, TRANS>(g, acc, m0, n0, wm, wn, wave, lane, smem);
     pre.load(g, m0, n0, tid);
     sync_loads<0>();   // the trailing (unused) chunk loads must land before LDS is reused
   } else {
@@ -715,7 +831,10 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
     pre.store(in, tid);
     __syncthreads();
   }
-  epilogue<MODE, BN, F>(g, acc, m0, n0, wm, wn, lane, wave, z, mt, scratch, in);
+  if constexpr (TRANS)
+    epilogue_trans<BN, F, RG>(g, acc, m0, n0, wm, wn, lane, in);
+  else
+    epilogue<MODE, BN, F>(g, acc, m0, n0, wm, wn, lane, wave, z, mt, scratch, in);
 }
 
 template <int MODE, int BN, int F, bool RG>
@@ -832,6 +951,8 @@ bool big_gemm_ld_ok(GemmMode mode, const GemmArgs& g) {
 
 hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s) {
   if (!big_gemm_ld_ok(mode, g)) return hipErrorInvalidValue;
+  // The forward reads its bias four columns at a time.
+  if (mode == GEMM_FWD && g.bias && ((uintptr_t)g.bias & 15)) return hipErrorInvalidValue;
   const int f = epilogue_flags(mode, g);
   const bool fused = f & (EPI_BITS | EPI_BITS_OUT | EPI_RDOT | EPI_CSUM | EPI_NOSTORE);
   if (fused && g.N % 128) return hipErrorInvalidValue;

@@ -97,7 +97,7 @@ struct GemmArgs {
   // epilogue features are refused).
   const void* Bt; int64_t ldbt;
   void* C; int64_t ldc;
-  const float* bias;           // FWD: bias [N] (fp32)
+  const float* bias;           // FWD: bias [N] (fp32; 16-byte aligned for the large-tile kernel)
   const void* mask; int64_t ldm;  // DGRAD: C *= (mask > 0) when non-null (operand type)
   int M, N, K;                 // WGRAD: K is the batch extent split over gridDim.z
   int relu;                    // FWD
