@@ -86,7 +86,6 @@ struct spz_ctx {
   // configuration
   int O = 0, A = 0, B = 0, Bp = 0, Ka = 0, Ap = 0, Kc = 0;
   int Bmax = 0, Bpmax = 0;   // batch given to spz_create: sizes every batch buffer
-  int64_t wpart_cap = 0;     // floats of each split-K partial buffer
   std::vector<int> hidden;
   spz_hparams hp{};
   uint64_t seed = 0;
@@ -142,9 +141,8 @@ struct spz_ctx {
   float *q1 = nullptr, *q2 = nullptr, *dq1 = nullptr, *dq2 = nullptr;
   std::vector<void*> hc[2];
   std::vector<uint32_t*> bhc[2];     // ReLU masks of hc as bits (null where not fused)
-  float* c_rdot = nullptr;           // row-dot partials of the critic stream
+  float* c_rdot[2] = {nullptr, nullptr};   // row-dot partials of the critic stream (two heads in flight)
   void* c_dz[2] = {nullptr, nullptr};
-  float *c_wpart = nullptr, *c_cpart = nullptr, *c_cextra = nullptr;
   double* c_lpart = nullptr;
   // actor-stream workspace
   std::vector<void*> ha;
@@ -152,7 +150,7 @@ struct spz_ctx {
   float *qp1 = nullptr, *qp2 = nullptr, *dqp1 = nullptr, *dqp2 = nullptr, *da1 = nullptr, *da2 = nullptr;
   std::vector<void*> hpc[2];
   std::vector<uint32_t*> bha, bhpc[2];
-  float* a_rdot = nullptr;
+  float* a_rdot[2] = {nullptr, nullptr};
   // SAC row split of the actor's gradient through the critics: two row maps [Bp]
   // and their padded lengths (device side), the actor loss's per-block critic-1
   // counts, and one layer's mask bits gathered by a map.
@@ -161,8 +159,12 @@ struct spz_ctx {
   uint32_t* rbits = nullptr;
   void* a_dz[2] = {nullptr, nullptr};
   void* dzh = nullptr;
-  float *a_wpart = nullptr, *a_cpart = nullptr;
   double* a_lpart = nullptr;
+  // Deferred gradient reductions of the critic part (0) and the actor part (1): the
+  // split-K and column-sum partials of every layer go to consecutive slots of the
+  // part's workspace and one launch at the end of the part reduces them all.
+  struct RedQueue { float* base = nullptr; int64_t cap = 0, off = 0; double bytes = 0.0; ReduceJobs jobs{}; };
+  RedQueue red[2];
   // streams
   hipStream_t sc = nullptr, sa = nullptr;
   hipEvent_t ev_fork = nullptr, ev_c = nullptr, ev_a = nullptr;
@@ -362,16 +364,80 @@ hipError_t refresh_wt(spz_ctx* c, hipStream_t s) {
 // product), or null (float32 contexts).
 const void* wt(const spz_ctx* c, const Lay& L) { return c->WT ? elem(c, c->WT, L.w) : nullptr; }
 
+// Deferred reductions: partial buffers come from the part's workspace in enqueue
+// order (the same addresses every step, as graph replay needs); a full job list is
+// reduced early (same stream, so the slots may then be reused).
+float* red_alloc(spz_ctx* c, int q, int64_t n) {
+  spz_ctx::RedQueue& r = c->red[q];
+  const int64_t need = (n + 63) / 64 * 64;
+  if (r.off + need > r.cap) return nullptr;
+  float* p = r.base + r.off;
+  r.off += need;
+  return p;
+}
+
+hipError_t red_flush(spz_ctx* c, int q, hipStream_t s) {
+  spz_ctx::RedQueue& r = c->red[q];
+  if (r.jobs.n) {
+    HK(timed(c, "grad_reduce", r.jobs.n, 0, 0, 0.0, r.bytes, s, [&] { return launch_reduce_jobs(r.jobs, s); }));
+  }
+  r.jobs.n = 0;
+  r.off = 0;
+  r.bytes = 0.0;
+  return hipSuccess;
+}
+
+hipError_t red_job(spz_ctx* c, int q, const ReduceJob& j, hipStream_t s) {
+  spz_ctx::RedQueue& r = c->red[q];
+  if (r.jobs.n == MAX_REDUCE_JOBS) return hipErrorInvalidValue;   // callers flush before allocating
+  r.jobs.j[r.jobs.n++] = j;
+  r.bytes += 4.0 * j.rows * j.cols * (j.slices + 1.0);
+  return hipSuccess;
+}
+
+// Room for `jobs` more jobs (flushing what is queued otherwise).
+hipError_t red_room(spz_ctx* c, int q, int jobs, hipStream_t s) {
+  return c->red[q].jobs.n + jobs > MAX_REDUCE_JOBS ? red_flush(c, q, s) : hipSuccess;
+}
+
+// Reduction of column-sum partials part[slices, N] into out[N] (and of the extra
+// scalars part_extra[slices] into *out_extra), in the order of the standalone pass.
+hipError_t red_colsum(spz_ctx* c, int q, const float* part, int slices, int N, float* out, const float* part_extra,
+                      float* out_extra, hipStream_t s) {
+  HK(red_job(c, q, ReduceJob{part, out, N, 0, 0, 1, N, slices, colsum_groups(), 4, 0}, s));
+  if (!part_extra) return hipSuccess;
+  return red_job(c, q, ReduceJob{part_extra, out_extra, 1, 0, 0, 1, 1, slices, colsum_groups(), 1, 0}, s);
+}
+
+int colsum_rows(const spz_ctx* c, int Bp) {
+  return std::max({colsum_chunks(Bp), Bp / 256, head_bwd_blocks(Bp)});
+}
+
+// Workspace floats a part's deferred reductions may need at padded batch Bp.
+int64_t red_need(const spz_ctx* c, int q, int Bp) {
+  const int chunks = colsum_rows(c, Bp);
+  int64_t n = 0;
+  for (int ni = (q == 0 ? 1 : 0); ni <= (q == 0 ? 2 : 0); ++ni)
+    for (const Lay& L : c->net[ni].L) {
+      n += (int64_t)wgrad_splits(c->bf16, L.out_p, L.in_p, Bp) * L.out_p * L.in_p + 64;
+      n += 2 * ((int64_t)chunks * (std::max(L.out_p, L.in_p) + 1) + 64);
+    }
+  return n;
+}
+
 // Forward of net ni. X: [Bp, ldx] operand tensor (the first in_p(0) columns are read).
 // hid[l] receives hidden layer l and, where bits[l] is set, its ReLU mask as bits;
-// critic heads write q [Bp], the actor head z [Bp, out_p]. Where the large-tile
-// kernel covers the last hidden layer of a critic, the output layer is folded into
-// that product's epilogue (row-dot partials in rdot, summed in order afterwards);
-// the last hidden layer is then stored only when keep_last.
+// the actor head writes z [Bp, out_p] to head. A critic's output is described by *qs
+// for the kernel that consumes it: where the large-tile kernel covers the last hidden
+// layer, the output layer is folded into that product's epilogue (row-dot partials in
+// rdot, which the consumer sums in order and stores to head); otherwise a row-dot
+// kernel writes q [Bp] to head. The last hidden layer is then stored only when keep_last.
 bool fused_layer(const spz_ctx* c, const Lay& L) { return gemm_fused_ok(c->bf16, GEMM_FWD, c->Bp, L.out_p, L.in_p); }
 
 hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, void* const* hid,
-                   uint32_t* const* bits, bool keep_last, float* rdot, float* head, hipStream_t s) {
+                   uint32_t* const* bits, bool keep_last, float* rdot, float* head, hipStream_t s,
+                   QSrc* qs = nullptr) {
+  if (ni != 0 && !qs) return hipErrorInvalidValue;
   const Net& n = c->net[ni];
   const int nl = (int)n.L.size();
   const void* in = X;
@@ -379,6 +445,7 @@ hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, 
   for (int l = 0; l < nl; ++l) {
     const Lay& L = n.L[l];
     if (l == nl - 1 && ni != 0) {
+      *qs = QSrc{head, nullptr, 0, 0, nullptr};
       RowdotArgs r{in, ld, L.in_p, c->Bp, wop(c, target, L.w), wf(c, target, L.b), head};
       return timed(c, "rowdot", c->Bp, 1, L.in_p, 2.0 * c->Bp * L.in_p,
                    (double)c->Bp * L.in_p * es(c) + 4.0 * c->Bp, s, [&] { return launch_rowdot(c->bf16, r, s); });
@@ -410,9 +477,8 @@ hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, 
              [&] { return gemm(c->bf16, GEMM_FWD, g, s); }));
     if (folded) {
       const Lay& H = n.L[nl - 1];
-      RdotFinalArgs f{rdot, L.out_p / gemm_rdot_cols(c->Bp, L.out_p), c->Bp, c->Bp, wf(c, target, H.b), head};
-      return timed(c, "rdot_final", c->Bp, f.parts, 0, 0.0, 4.0 * c->Bp * (f.parts + 1), s,
-                   [&] { return launch_rdot_final(f, s); });
+      *qs = QSrc{head, rdot, L.out_p / gemm_rdot_cols(c->Bp, L.out_p), c->Bp, wf(c, target, H.b)};
+      return hipSuccess;
     }
     in = g.C;
     ld = L.out_p;
@@ -420,35 +486,44 @@ hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, 
   return hipSuccess;
 }
 
-// Weight gradient of layer L (split-K over the batch, slices reduced in order) and,
-// when `bias`, its bias gradient as the column sums of dz.
-hipError_t wgrad(spz_ctx* c, const void* dz, int64_t lddz, const void* X, int64_t ldx, const Lay& L,
-                 float* part, float* cpart, bool bias, hipStream_t s) {
+// Weight gradient of layer L (split-K over the batch, slices reduced in order by the
+// part's deferred reduction q) and, when `bias`, its bias gradient as the column sums of dz.
+hipError_t wgrad(spz_ctx* c, int q, const void* dz, int64_t lddz, const void* X, int64_t ldx, const Lay& L,
+                 bool bias, hipStream_t s) {
+  HK(red_room(c, q, 2, s));
   GemmArgs g{};
   g.A = dz; g.lda = lddz;
   g.B = X; g.ldb = ldx;
   g.M = L.out_p; g.N = L.in_p; g.K = c->Bp;
   g.splits = wgrad_splits(c->bf16, g.M, g.N, g.K);
+  float* part = red_alloc(c, q, (int64_t)g.splits * g.M * g.N);
+  if (!part) return hipErrorOutOfMemory;
   g.C = part; g.ldc = L.in_p;
   HK(timed(c, "gemm_wgrad", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
            [&] { return gemm(c->bf16, GEMM_WGRAD, g, s); }));
-  HK(timed(c, "splitk_reduce", g.M, g.N, g.splits, 0.0, 4.0 * g.M * g.N * (g.splits + 1), s,
-           [&] { return splitk_reduce(part, g.splits, g.M, g.N, g.ldc, c->G + L.w, L.in_p, s); }));
+  HK(red_job(c, q, ReduceJob{part, c->G + L.w, (int64_t)g.M * g.ldc, g.ldc, L.in_p, g.M, g.N, g.splits,
+                             splitk_groups(g.M, g.N, g.splits), 4, 0}, s));
   if (!bias) return hipSuccess;
+  const int chunks = colsum_chunks(c->Bp);
+  float* cpart = red_alloc(c, q, (int64_t)chunks * L.out_p);
+  if (!cpart) return hipErrorOutOfMemory;
   ColsumArgs cs{dz, lddz, L.out_p, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
-  return timed(c, "colsum", c->Bp, L.out_p, 0, 0.0, (double)c->Bp * L.out_p * es(c), s,
-               [&] { return launch_colsum(c->bf16, cs, c->G + L.b, nullptr, s); });
+  HK(timed(c, "colsum", c->Bp, L.out_p, 0, 0.0, (double)c->Bp * L.out_p * es(c), s,
+           [&] { return launch_colsum_partial(c->bf16, cs, s); }));
+  return red_colsum(c, q, cpart, chunks, L.out_p, c->G + L.b, nullptr, nullptr, s);
 }
 
 // Input gradient through layer L: out[Bp, N] = (dz . W) masked by mask > 0 (or by
 // the mask bits when given). Wt (or null): the transposed image of W, which both
 // GEMM kernels read instead of W. With
 // bias_out, also the column sums of the stored out (the bias gradient of the layer
-// below): fused into the product's epilogue where the large-tile kernel covers it.
+// below): fused into the product's epilogue where the large-tile kernel covers it,
+// the partial sums reduced by the part's deferred reduction q.
 // With m_dyn (a device-side count of leading rows), only those rows are computed.
 hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_t ldw, const void* Wt, int N,
                  const void* mask, const uint32_t* bits, void* out, int64_t ldo, bool out_f32, float* bias_out,
-                 float* cpart, hipStream_t s, const int32_t* m_dyn = nullptr) {
+                 int q, hipStream_t s, const int32_t* m_dyn = nullptr) {
+  if (bias_out) HK(red_room(c, q, 1, s));
   GemmArgs g{};
   g.m_dyn = m_dyn;
   g.A = dz; g.lda = L.out_p;
@@ -464,6 +539,9 @@ hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_
   }
   g.M = c->Bp; g.N = N; g.K = L.out_p;
   const bool fused = bias_out && gemm_colsum_fused(c->bf16, GEMM_DGRAD, g.M, g.N, g.K);
+  const int chunks = fused ? c->Bp / 256 : colsum_chunks(c->Bp);
+  float* cpart = nullptr;
+  if (bias_out && !(cpart = red_alloc(c, q, (int64_t)chunks * N))) return hipErrorOutOfMemory;
   if (fused) {
     g.colsum = cpart;
     g.ldcs = N;
@@ -473,12 +551,12 @@ hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_
   HK(timed(c, m_dyn ? "gemm_dgrad_rows" : "gemm_dgrad", g.M, g.N, g.K, m_dyn ? 0.0 : 2.0 * g.M * g.N * g.K, 0.0, s,
            [&] { return gemm(c->bf16, GEMM_DGRAD, g, s); }));
   if (!bias_out) return hipSuccess;
-  if (fused)
-    return timed(c, "colsum_final", c->Bp / 256, N, 0, 0.0, 4.0 * (c->Bp / 256) * N, s,
-                 [&] { return launch_colsum_final(cpart, c->Bp / 256, N, bias_out, s); });
-  ColsumArgs cs{out, ldo, N, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
-  return timed(c, "colsum", c->Bp, N, 0, 0.0, (double)c->Bp * N * es(c), s,
-               [&] { return launch_colsum(c->bf16, cs, bias_out, nullptr, s); });
+  if (!fused) {
+    ColsumArgs cs{out, ldo, N, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
+    HK(timed(c, "colsum", c->Bp, N, 0, 0.0, (double)c->Bp * N * es(c), s,
+             [&] { return launch_colsum_partial(c->bf16, cs, s); }));
+  }
+  return red_colsum(c, q, cpart, chunks, N, bias_out, nullptr, nullptr, s);
 }
 
 // Critic ni in {1, 2}: weight and bias gradients of L = sum_b dq[b] q[b] given the
@@ -488,33 +566,36 @@ hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, v
   const Net& n = c->net[ni];
   const int nl = (int)n.L.size();
   const Lay& H = n.L[nl - 1];
-  ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, c->c_cpart, c->c_cextra};
+  HK(red_room(c, 0, 3, s));
+  const int chunks = colsum_chunks(c->Bp);
+  float* cpart = red_alloc(c, 0, (int64_t)chunks * H.in_p);
+  float* cextra = red_alloc(c, 0, chunks);
+  if (!cpart || !cextra) return hipErrorOutOfMemory;
+  ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, cpart, cextra};
   HK(timed(c, "colsum", c->Bp, H.in_p, 1, 0.0, (double)c->Bp * H.in_p * es(c), s,
-           [&] { return launch_colsum(c->bf16, cs, c->G + H.w, c->G + H.b, s); }));
+           [&] { return launch_colsum_partial(c->bf16, cs, s); }));
+  HK(red_colsum(c, 0, cpart, chunks, H.in_p, c->G + H.w, cextra, c->G + H.b, s));
   // dz of the last hidden layer comes from the head backward, which (with the mask
   // as bits) also takes its column sums, the bias gradient; otherwise that is a
   // separate column sum in the weight gradient. Every later dz comes from a dgrad
   // that also produces its bias gradient.
   const bool hb_sums = bits[nl - 2] != nullptr;
-  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp,
-                 hb_sums ? c->c_cpart : nullptr};
+  const int hblocks = head_bwd_blocks(c->Bp);
+  float* hpart = hb_sums ? red_alloc(c, 0, (int64_t)hblocks * n.L[nl - 2].out_p) : nullptr;
+  if (hb_sums && !hpart) return hipErrorOutOfMemory;
+  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp, hpart};
   HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, head_bwd_bytes(c, H.in_p, bits[nl - 2]), s,
            [&] { return launch_head_bwd(c->bf16, hb, s); }));
-  if (hb_sums) {
-    const int blocks = head_bwd_blocks(c->Bp);
-    const Lay& Ll = n.L[nl - 2];
-    HK(timed(c, "colsum_final", blocks, Ll.out_p, 0, 0.0, 4.0 * blocks * Ll.out_p, s,
-             [&] { return launch_colsum_final(c->c_cpart, blocks, Ll.out_p, c->G + Ll.b, s); }));
-  }
+  if (hb_sums) HK(red_colsum(c, 0, hpart, hblocks, n.L[nl - 2].out_p, c->G + n.L[nl - 2].b, nullptr, nullptr, s));
   int cur = 0;
   for (int l = nl - 2; l >= 0; --l) {
     const Lay& L = n.L[l];
     const void* Xl = l == 0 ? X : hid[l - 1];
     const int64_t ldx = l == 0 ? c->Kc : L.in_p;
-    HK(wgrad(c, c->c_dz[cur], L.out_p, Xl, ldx, L, c->c_wpart, c->c_cpart, l == nl - 2 && !hb_sums, s));
+    HK(wgrad(c, 0, c->c_dz[cur], L.out_p, Xl, ldx, L, l == nl - 2 && !hb_sums, s));
     if (l > 0) {
       HK(dgrad(c, c->c_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, hid[l - 1], bits[l - 1],
-               c->c_dz[cur ^ 1], L.in_p, false, c->G + n.L[l - 1].b, c->c_cpart, s));
+               c->c_dz[cur ^ 1], L.in_p, false, c->G + n.L[l - 1].b, 0, s));
       cur ^= 1;
     }
   }
@@ -535,12 +616,12 @@ hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* 
   for (int l = nl - 2; l >= 1; --l) {
     const Lay& L = n.L[l];
     HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, hid[l - 1], bits[l - 1],
-             c->a_dz[cur ^ 1], L.in_p, false, nullptr, nullptr, s));
+             c->a_dz[cur ^ 1], L.in_p, false, nullptr, 1, s));
     cur ^= 1;
   }
   const Lay& L0 = n.L[0];
   return dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, nullptr, c->Ap, nullptr, nullptr, da,
-               c->Ap, true, nullptr, nullptr, s);
+               c->Ap, true, nullptr, 1, s);
 }
 
 // The same restricted to the rows listed in map (padded with -1 to the device-side
@@ -562,13 +643,13 @@ hipError_t critic_action_grad_rows(spz_ctx* c, int ni, const float* dq, void* co
     RowBitsGatherArgs gb{bits[l - 1], c->rbits, c->Bp, L.in_p / 32, map, rows, c->Bp};
     HK(timed(c, "row_bits_gather", c->Bp, L.in_p, 0, 0.0, 0.0, s, [&] { return launch_row_bits_gather(gb, s); }));
     HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, nullptr, c->rbits, c->a_dz[cur ^ 1],
-             L.in_p, false, nullptr, nullptr, s, rows));
+             L.in_p, false, nullptr, 1, s, rows));
     cur ^= 1;
   }
   // The action gradient of the listed rows lands in da2 (free here) and then in da.
   const Lay& L0 = n.L[0];
   HK(dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, nullptr, c->Ap, nullptr, nullptr,
-           c->da2, c->Ap, true, nullptr, nullptr, s, rows));
+           c->da2, c->Ap, true, nullptr, 1, s, rows));
   RowScatterArgs sa{c->da2, da, c->Ap, c->Ap, map, rows, c->Bp};
   return timed(c, "row_scatter", c->Bp, c->Ap, 0, 0.0, 0.0, s, [&] { return launch_row_scatter(sa, s); });
 }
@@ -582,10 +663,10 @@ hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
     const Lay& L = n.L[l];
     const void* Xl = l == 0 ? c->xsa : c->ha[l - 1];
     const int64_t ldx = l == 0 ? c->Kc : L.in_p;
-    HK(wgrad(c, cur, L.out_p, Xl, ldx, L, c->a_wpart, c->a_cpart, l == nl - 1, s));
+    HK(wgrad(c, 1, cur, L.out_p, Xl, ldx, L, l == nl - 1, s));
     if (l > 0) {
       HK(dgrad(c, cur, L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, c->ha[l - 1], c->bha[l - 1], c->a_dz[nxt],
-               L.in_p, false, c->G + n.L[l - 1].b, c->a_cpart, s));
+               L.in_p, false, c->G + n.L[l - 1].b, 1, s));
       cur = c->a_dz[nxt];
       nxt ^= 1;
     }
@@ -611,18 +692,22 @@ hipError_t critic_part(spz_ctx* c, hipStream_t s) {
                   c->xs2, c->Kc, c->Ka, nullptr};
     HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
-  HK(forward(c, 1, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, false, c->c_rdot, c->qt1, s));
-  HK(forward(c, 2, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, false, c->c_rdot, c->qt2, s));
-  TdArgs td{c->qt1, c->qt2, c->r, c->d, c->td3 ? nullptr : c->logp2, log_alpha_ptr(c), c->y, hp.gamma,
-            c->B, c->Bp};
+  QSrc q1, q2;
+  HK(forward(c, 1, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, false, c->c_rdot[0], c->qt1, s, &q1));
+  HK(forward(c, 2, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, false, c->c_rdot[1], c->qt2, s, &q2));
+  TdArgs td{q1, q2, c->r, c->d, c->td3 ? nullptr : c->logp2, log_alpha_ptr(c), c->y, hp.gamma, c->B, c->Bp};
   HK(timed(c, "td_target", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_td_target(td, s); }));
-  HK(forward(c, 1, false, c->xsa, c->Kc, c->hc[0].data(), c->bhc[0].data(), true, c->c_rdot, c->q1, s));
-  HK(forward(c, 2, false, c->xsa, c->Kc, c->hc[1].data(), c->bhc[1].data(), true, c->c_rdot, c->q2, s));
-  CriticLossArgs cl{c->q1, c->q2, c->y, c->dq1, c->dq2, c->c_lpart, c->B, c->Bp};
+  // the target critics' partials were consumed by the TD target: their buffers are free
+  HK(forward(c, 1, false, c->xsa, c->Kc, c->hc[0].data(), c->bhc[0].data(), true, c->c_rdot[0], c->q1, s, &q1));
+  HK(forward(c, 2, false, c->xsa, c->Kc, c->hc[1].data(), c->bhc[1].data(), true, c->c_rdot[1], c->q2, s, &q2));
+  CriticLossArgs cl{q1, q2, c->y, c->dq1, c->dq2, c->c_lpart, c->B, c->Bp};
   HK(timed(c, "critic_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_critic_loss(cl, s); }));
+  c->red[0].jobs.n = 0;
+  c->red[0].off = 0;
+  c->red[0].bytes = 0.0;
   HK(critic_backward(c, 1, c->dq1, c->xsa, c->hc[0].data(), c->bhc[0].data(), s));
   HK(critic_backward(c, 2, c->dq2, c->xsa, c->hc[1].data(), c->bhc[1].data(), s));
-  return hipSuccess;
+  return red_flush(c, 0, s);
 }
 
 // Actor stream: reparameterised action on s, critics at their step-start values on
@@ -639,10 +724,13 @@ hipError_t actor_part(spz_ctx* c, hipStream_t s) {
     Td3HeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, 0, 0.0f, 0.0f, c->xs_act, c->Kc, c->Ka, c->th};
     HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
-  HK(forward(c, 1, false, c->xs_act, c->Kc, c->hpc[0].data(), c->bhpc[0].data(), false, c->a_rdot, c->qp1, s));
+  QSrc qp1, qp2{};
+  HK(forward(c, 1, false, c->xs_act, c->Kc, c->hpc[0].data(), c->bhpc[0].data(), false, c->a_rdot[0], c->qp1, s,
+             &qp1));
   if (!c->td3)
-    HK(forward(c, 2, false, c->xs_act, c->Kc, c->hpc[1].data(), c->bhpc[1].data(), false, c->a_rdot, c->qp2, s));
-  ActorLossArgs al{c->qp1, c->td3 ? nullptr : c->qp2, c->logp, log_alpha_ptr(c), c->dqp1,
+    HK(forward(c, 2, false, c->xs_act, c->Kc, c->hpc[1].data(), c->bhpc[1].data(), false, c->a_rdot[1], c->qp2, s,
+               &qp2));
+  ActorLossArgs al{qp1, qp2, c->td3 ? 0 : 1, c->logp, log_alpha_ptr(c), c->dqp1,
                    c->td3 ? nullptr : c->dqp2, c->a_lpart, c->B, c->Bp, c->row_split ? c->rcnt : nullptr};
   HK(timed(c, "actor_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_actor_loss(al, s); }));
   if (c->row_split) {
@@ -660,7 +748,11 @@ hipError_t actor_part(spz_ctx* c, hipStream_t s) {
   ActorHeadBwdArgs hb{c->da1, c->td3 || c->row_split ? nullptr : c->da2, c->Ap, c->th, c->se, c->lm,
                       log_alpha_ptr(c), c->dzh, pa, c->A, c->B, c->td3 ? 0 : 1};
   HK(timed(c, "actor_head_bwd", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_actor_head_bwd(c->bf16, hb, s); }));
-  return actor_backward(c, s);
+  c->red[1].jobs.n = 0;
+  c->red[1].off = 0;
+  c->red[1].bytes = 0.0;
+  HK(actor_backward(c, s));
+  return red_flush(c, 1, s);
 }
 
 // Adam (+ Polyak) over the parameter arena. critics / actor select the optimizer
@@ -907,8 +999,10 @@ int setup(spz_ctx* c) {
     if (l == nh - 1) rd_parts = w / 64;   // the most partials any batch size gives (gemm_rdot_cols)
   }
   if (rd_parts) {
-    CK(dalloc_t(c, &c->c_rdot, (size_t)rd_parts * Bp * 4));
-    CK(dalloc_t(c, &c->a_rdot, (size_t)rd_parts * Bp * 4));
+    for (int i = 0; i < 2; ++i) {
+      CK(dalloc_t(c, &c->c_rdot[i], (size_t)rd_parts * Bp * 4));
+      CK(dalloc_t(c, &c->a_rdot[i], (size_t)rd_parts * Bp * 4));
+    }
   }
   // The row split needs every hidden mask of both critics as bits.
   c->row_split = !c->td3 && c->hp.actor_row_split;
@@ -919,22 +1013,12 @@ int setup(spz_ctx* c) {
     CK(dalloc_t(c, &c->rcnt, (size_t)(Bp / 256) * 4));
     CK(dalloc_t(c, &c->rbits, (size_t)Bp * (c->hmax / 32) * 4));
   }
-  // reduction workspaces
-  int64_t wmax = 0, cmax = 0;
-  for (int ni = 0; ni < 3; ++ni)
-    for (const Lay& L : c->net[ni].L) {
-      wmax = std::max<int64_t>(wmax, (int64_t)wgrad_splits(c->bf16, L.out_p, L.in_p, (int)Bp) * L.out_p * L.in_p);
-      cmax = std::max<int64_t>(cmax, (int64_t)std::max(L.out_p, L.in_p) + 1);
-    }
-  // column-sum partials: first-pass chunks of the standalone kernel, or one row per
-  // 256-row tile of a fused dgrad epilogue
-  const int chunks = std::max({colsum_chunks((int)Bp), (int)(Bp / 256), head_bwd_blocks((int)Bp)});
-  c->wpart_cap = wmax;
-  CK(dalloc_t(c, &c->c_wpart, (size_t)wmax * 4));
-  CK(dalloc_t(c, &c->a_wpart, (size_t)wmax * 4));
-  CK(dalloc_t(c, &c->c_cpart, (size_t)chunks * cmax * 4));
-  CK(dalloc_t(c, &c->a_cpart, (size_t)chunks * cmax * 4));
-  CK(dalloc_t(c, &c->c_cextra, (size_t)chunks * 4));
+  // deferred-reduction workspaces, sized for the created batch (spz_set_batch checks
+  // that a smaller one fits)
+  for (int q = 0; q < 2; ++q) {
+    c->red[q].cap = red_need(c, q, (int)Bp);
+    CK(dalloc_t(c, &c->red[q].base, (size_t)c->red[q].cap * 4));
+  }
   CK(dalloc_t(c, &c->c_lpart, (size_t)loss_blocks((int)Bp) * 3 * 8));
   CK(dalloc_t(c, &c->a_lpart, (size_t)loss_blocks((int)Bp) * 2 * 8));
   // streams (default priority)
@@ -1504,10 +1588,9 @@ int spz_set_batch(spz_ctx* c, int32_t batch) {
   if (!c) return set_err(nullptr, SPZ_EINVAL, "spz_set_batch: NULL context");
   if (batch < 1 || batch > c->Bmax) return set_err(c, SPZ_EINVAL, "spz_set_batch: batch out of [1, created batch]");
   const int Bp = (batch + 255) / 256 * 256;
-  for (int ni = 0; ni < 3; ++ni)
-    for (const Lay& L : c->net[ni].L)
-      if ((int64_t)wgrad_splits(c->bf16, L.out_p, L.in_p, Bp) * L.out_p * L.in_p > c->wpart_cap)
-        return set_err(c, SPZ_EINVAL, "spz_set_batch: split-K workspace too small for this batch");
+  for (int q = 0; q < 2; ++q)
+    if (red_need(c, q, Bp) > c->red[q].cap)
+      return set_err(c, SPZ_EINVAL, "spz_set_batch: reduction workspace too small for this batch");
   CK(hipSetDevice(c->hp.device));
   int rc = ctx_sync(c);
   if (rc) return rc;

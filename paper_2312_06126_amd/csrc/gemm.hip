@@ -452,12 +452,16 @@ hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   return gemm_generic(bf16, mode, g, s);
 }
 
+int splitk_groups(int M, int N, int splits) {
+  // Small outputs (under 64K 16-byte pieces) from many slices: split the slices too.
+  return (int64_t)M * (N / 4) < 4 * 256 * 64 && splits >= 4 * RG_GROUPS ? RG_GROUPS : 1;
+}
+
 hipError_t splitk_reduce(const float* part, int splits, int M, int N, int64_t ldc, float* out,
                          int64_t ldo, hipStream_t s) {
   if (N % 4 || ldc % 4 || ldo % 4) return hipErrorInvalidValue;
   const int64_t n = (int64_t)M * (N / 4);
-  // Small outputs (under 64K 16-byte pieces) from many slices: split the slices too.
-  if (n < 4 * 256 * 64 && splits >= 4 * RG_GROUPS) {
+  if (splitk_groups(M, N, splits) > 1) {
     constexpr int COLS = 256 / RG_GROUPS;
     k_splitk_reduce_grouped<<<(unsigned)((n + COLS - 1) / COLS), 256, 0, s>>>(part, splits, M, N, ldc, out, ldo);
     return hipGetLastError();

@@ -145,6 +145,9 @@ __host__ __device__ inline int epilogue_flags(GemmMode mode, const GemmArgs& g) 
 // C = A B with A: [M, K] k-contiguous (FWD, DGRAD) or [K, M] (WGRAD),
 // B: [N, K] (FWD) or [K, N] (DGRAD, WGRAD). Returns a hipError_t.
 hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s);
+// Threads per output piece of the split-K reduction of an M x N product from `splits`
+// slices (the grouping ReduceJob::groups reproduces).
+int splitk_groups(int M, int N, int splits);
 // Sum `splits` float slices [splits, M, ldc] into out [M, ldo].
 hipError_t splitk_reduce(const float* part, int splits, int M, int N, int64_t ldc, float* out,
                          int64_t ldo, hipStream_t s);

@@ -74,21 +74,25 @@ struct ActHeadArgs {
   float* a;
 };
 
-// q[r] = bias + sum over p < parts in order of part[p * ld + r], r < rows.
-struct RdotFinalArgs {
-  const float* part; int parts; int64_t ld; int rows; const float* bias; float* q;
+// A critic's output q [Bp]. With parts > 0 the output layer was folded into the last
+// hidden product (row-dot partials): q[r] = *bias + sum over p < parts in order of
+// part[p * ld + r], computed by the kernel that consumes q, which also stores it to q
+// (for the kernels and debug reads after it). Otherwise q[r] is read as stored.
+struct QSrc {
+  float* q; const float* part; int parts; int64_t ld; const float* bias;
 };
 
 struct TdArgs {
-  const float *q1, *q2, *r, *d, *logp, *log_alpha; float* y; float gamma; int B, Bp;
+  QSrc q1, q2; const float *r, *d, *logp, *log_alpha; float* y; float gamma; int B, Bp;
 };
 
 struct CriticLossArgs {
-  const float *q1, *q2, *y; float *dq1, *dq2; double* part; int B, Bp;
+  QSrc q1, q2; const float* y; float *dq1, *dq2; double* part; int B, Bp;
 };
 
+// TD3: has_qp2 = 0 (the loss takes critic 1 only).
 struct ActorLossArgs {
-  const float *qp1, *qp2, *logp, *log_alpha; float *dqp1, *dqp2; double* part; int B, Bp;
+  QSrc qp1, qp2; int has_qp2; const float *logp, *log_alpha; float *dqp1, *dqp2; double* part; int B, Bp;
   // With qp2, when set: cnt1[k] = the rows b < B of the k-th 256-row block whose
   // minimum critic is critic 1 (qp1[b] <= qp2[b], the loss's own choice).
   int32_t* cnt1;
@@ -146,7 +150,6 @@ hipError_t launch_sac_head(bool bf16, const SacHeadArgs& h, hipStream_t s);
 hipError_t launch_td3_head(bool bf16, const Td3HeadArgs& h, hipStream_t s);
 hipError_t launch_rowdot(bool bf16, const RowdotArgs& r, hipStream_t s);
 hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s);
-hipError_t launch_rdot_final(const RdotFinalArgs& a, hipStream_t s);
 hipError_t launch_obs_operand(bool bf16, const ObsArgs& a, hipStream_t s);
 hipError_t launch_act_head(const ActHeadArgs& a, hipStream_t s);
 hipError_t launch_td_target(const TdArgs& a, hipStream_t s);
@@ -160,6 +163,25 @@ hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream
 int colsum_chunks(int rows);
 int head_bwd_blocks(int rows);
 hipError_t launch_colsum(bool bf16, const ColsumArgs& a, float* out, float* out_extra, hipStream_t s);
+// The first pass alone: a.part[chunks, N] (and a.part_extra[chunks]) for a deferred
+// reduction (ReduceJob with colsum_groups()).
+hipError_t launch_colsum_partial(bool bf16, const ColsumArgs& a, hipStream_t s);
+int colsum_groups();
+
+// Deferred reduction: out[r * ldo + c] = sum over slices z < slices of
+// part[z * zstride + r * ld + c], for r < rows, c < cols. A piece of vec (4 or 1)
+// output columns is summed by `groups` threads (a power of two): thread g takes
+// z = g, g + groups, ... in order, then the group sums are added in g order -- a
+// fixed order for a fixed job, the same as the split-K and column-sum reductions
+// that launch on their own. block0: first block of the job (set by the launch).
+struct ReduceJob {
+  const float* part; float* out; int64_t zstride, ld, ldo;
+  int rows, cols, slices, groups, vec, block0;
+};
+constexpr int MAX_REDUCE_JOBS = 24;
+struct ReduceJobs { ReduceJob j[MAX_REDUCE_JOBS]; int n; };
+// All jobs in one launch (n <= MAX_REDUCE_JOBS).
+hipError_t launch_reduce_jobs(ReduceJobs& jobs, hipStream_t s);
 // out[n] = sum over c in order of part[c, n] (c < chunks), n < N.
 hipError_t launch_colsum_final(const float* part, int chunks, int N, float* out, hipStream_t s);
 hipError_t launch_adam(const AdamArgs& a, hipStream_t s);

@@ -349,12 +349,15 @@ __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
   }
 }
 
-__global__ void __launch_bounds__(256) k_rdot_final(RdotFinalArgs a) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= a.rows) return;
-  float s = 0.0f;
-  for (int p = 0; p < a.parts; ++p) s += a.part[(int64_t)p * a.ld + r];
-  a.q[r] = s + *a.bias;
+// q[r] of a critic output (QSrc); row-dot partials are summed in part order, then the
+// bias is added, and the value is stored for later readers.
+__device__ inline float q_value(const QSrc& s, int r) {
+  if (!s.parts) return s.q[r];
+  float v = 0.0f;
+  for (int p = 0; p < s.parts; ++p) v += s.part[(int64_t)p * s.ld + r];
+  v += *s.bias;
+  s.q[r] = v;
+  return v;
 }
 
 // ------------------------------------------------------------------------------ sampler actions
@@ -384,8 +387,9 @@ __global__ void __launch_bounds__(256) k_act_head(ActHeadArgs h) {
 __global__ void __launch_bounds__(256) k_td_target(TdArgs a) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= a.Bp) return;
+  const float q1 = q_value(a.q1, b), q2 = q_value(a.q2, b);
   if (b >= a.B) { a.y[b] = 0.0f; return; }
-  float m = min_keep_nan(a.q1[b], a.q2[b]);
+  float m = min_keep_nan(q1, q2);
   if (a.logp) m -= expf(*a.log_alpha) * a.logp[b];
   a.y[b] = a.r[b] + a.gamma * (1.0f - a.d[b]) * m;
 }
@@ -397,13 +401,14 @@ __global__ void __launch_bounds__(256) k_critic_loss(CriticLossArgs a) {
   double e1s = 0.0, e2s = 0.0, q1s = 0.0;
   if (b < a.Bp) {
     float d1 = 0.0f, d2 = 0.0f;
+    const float q1 = q_value(a.q1, b), q2 = q_value(a.q2, b);
     if (b < a.B) {
-      const float e1 = a.q1[b] - a.y[b], e2 = a.q2[b] - a.y[b];
+      const float e1 = q1 - a.y[b], e2 = q2 - a.y[b];
       d1 = 2.0f * e1 / (float)a.B;
       d2 = 2.0f * e2 / (float)a.B;
       e1s = (double)e1 * e1;
       e2s = (double)e2 * e2;
-      q1s = a.q1[b];
+      q1s = q1;
     }
     a.dq1[b] = d1;
     a.dq2[b] = d2;
@@ -424,13 +429,14 @@ __global__ void __launch_bounds__(256) k_actor_loss(ActorLossArgs a) {
   __shared__ double sh[256];
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   double l0 = 0.0, l1 = 0.0;
+  bool take1 = false;
   if (b < a.Bp) {
     float g1 = 0.0f, g2 = 0.0f;
+    const float q1 = q_value(a.qp1, b), q2 = a.has_qp2 ? q_value(a.qp2, b) : 0.0f;
     if (b < a.B) {
       const float inv = -1.0f / (float)a.B;
-      if (a.qp2) {
-        const float q1 = a.qp1[b], q2 = a.qp2[b];
-        const bool take1 = q1 <= q2;
+      if (a.has_qp2) {
+        take1 = q1 <= q2;
         g1 = take1 ? inv : 0.0f;
         g2 = take1 ? 0.0f : inv;
         const float alpha = expf(*a.log_alpha);
@@ -438,7 +444,7 @@ __global__ void __launch_bounds__(256) k_actor_loss(ActorLossArgs a) {
         l1 = a.logp[b];
       } else {
         g1 = inv;
-        l0 = a.qp1[b];
+        l0 = q1;
       }
     }
     a.dqp1[b] = g1;
@@ -452,7 +458,7 @@ __global__ void __launch_bounds__(256) k_actor_loss(ActorLossArgs a) {
   }
   if (a.cnt1) {
     __shared__ int shi[4];
-    const int n1 = block_sum_i32(b < a.B && a.qp1[b] <= a.qp2[b] ? 1 : 0, shi);
+    const int n1 = block_sum_i32(b < a.B && take1 ? 1 : 0, shi);
     if (threadIdx.x == 0) a.cnt1[blockIdx.x] = n1;
   }
 }
@@ -645,6 +651,51 @@ __global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ 
   }
 }
 
+// Deferred reductions (ReduceJob): a block belongs to the last job whose block0 it has
+// reached; 256 / groups pieces per block, `groups` threads per piece.
+__global__ void __launch_bounds__(256) k_reduce_jobs(ReduceJobs J) {
+  __shared__ float4 sh[256];
+  int k = 0;
+  for (int i = 1; i < J.n; ++i)
+    if ((int)blockIdx.x >= J.j[i].block0) k = i;
+  const ReduceJob& jb = J.j[k];
+  const int G = jb.groups, P = 256 / G;
+  const int grp = threadIdx.x / P, pc = threadIdx.x % P;
+  const int cv = jb.cols / jb.vec;
+  const int64_t piece = (int64_t)((int)blockIdx.x - jb.block0) * P + pc;
+  const bool valid = piece < (int64_t)jb.rows * cv;
+  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  int64_t r = 0;
+  int col = 0;
+  if (valid) {
+    r = piece / cv;
+    col = (int)(piece - r * cv) * jb.vec;
+    const float* src = jb.part + r * jb.ld + col;
+    if (jb.vec == 4) {
+#pragma unroll 4
+      for (int z = grp; z < jb.slices; z += G) {
+        const float4 v = *reinterpret_cast<const float4*>(src + (int64_t)z * jb.zstride);
+        acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+      }
+    } else {
+      for (int z = grp; z < jb.slices; z += G) acc.x += src[(int64_t)z * jb.zstride];
+    }
+  }
+  if (G > 1) {   // uniform per block
+    sh[threadIdx.x] = acc;
+    __syncthreads();
+    if (grp != 0) return;
+    for (int q = 1; q < G; ++q) {
+      const float4 v = sh[q * P + pc];
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+  }
+  if (!valid) return;
+  float* dst = jb.out + r * jb.ldo + col;
+  if (jb.vec == 4) *reinterpret_cast<float4*>(dst) = acc;
+  else *dst = acc.x;
+}
+
 // ------------------------------------------------------------------------------ optimizer
 // Adam (bias-corrected, one counter per optimizer) on the actor range, the critic
 // range and log(alpha); then Polyak tbar <- (1 - tau) tbar + tau theta on the
@@ -829,11 +880,6 @@ hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 int head_bwd_blocks(int rows) { return (int)blocks(rows, HB_ROWS); }
-hipError_t launch_rdot_final(const RdotFinalArgs& a, hipStream_t s) {
-  if (a.parts < 1 || a.ld < a.rows) return hipErrorInvalidValue;
-  k_rdot_final<<<blocks(a.rows, 256), 256, 0, s>>>(a);
-  return hipGetLastError();
-}
 hipError_t launch_obs_operand(bool bf16, const ObsArgs& a, hipStream_t s) {
   if (a.n < 0 || a.n > a.rows || a.cols < a.O || a.ldx < a.cols) return hipErrorInvalidValue;
   SPZ_LAUNCH_T(bf16, k_obs_operand, blocks((int64_t)a.rows * a.cols, 256), 256, s, a);
@@ -854,7 +900,7 @@ hipError_t launch_critic_loss(const CriticLossArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 hipError_t launch_actor_loss(const ActorLossArgs& a, hipStream_t s) {
-  if (a.cnt1 && !a.qp2) return hipErrorInvalidValue;
+  if (a.cnt1 && !a.has_qp2) return hipErrorInvalidValue;
   k_actor_loss<<<blocks(a.Bp, 256), 256, 0, s>>>(a);
   return hipGetLastError();
 }
@@ -892,6 +938,34 @@ hipError_t launch_colsum(bool bf16, const ColsumArgs& a, float* out, float* out_
   dim3 grid(blocks(nvec, ct), chunks);
   SPZ_LAUNCH_T(bf16, k_colsum, grid, 256, s, a);
   k_colsum_final<<<blocks(a.N, CSF_COLS), 256, 0, s>>>(a.part, a.part_extra, chunks, a.N, a.extra, out, out_extra);
+  return hipGetLastError();
+}
+hipError_t launch_colsum_partial(bool bf16, const ColsumArgs& a, hipStream_t s) {
+  const int vec = bf16 ? 8 : 4;
+  if (a.N % vec || a.ld % vec || a.N % 4) return hipErrorInvalidValue;
+  const int nvec = a.N / vec, ct = nvec < 32 ? nvec : 32;
+  dim3 grid(blocks(nvec, ct), blocks(a.rows, a.chunk));
+  SPZ_LAUNCH_T(bf16, k_colsum, grid, 256, s, a);
+  return hipGetLastError();
+}
+int colsum_groups() { return CSF_G; }
+hipError_t launch_reduce_jobs(ReduceJobs& J, hipStream_t s) {
+  if (J.n < 1 || J.n > MAX_REDUCE_JOBS) return hipErrorInvalidValue;
+  int nb = 0;
+  for (int i = 0; i < J.n; ++i) {
+    ReduceJob& jb = J.j[i];
+    if (jb.groups < 1 || jb.groups > 256 || (jb.groups & (jb.groups - 1)) || (jb.vec != 1 && jb.vec != 4) ||
+        jb.cols % jb.vec || jb.rows < 0 || jb.slices < 1)
+      return hipErrorInvalidValue;
+    if (jb.vec == 4 && (jb.ld % 4 || jb.ldo % 4 || jb.zstride % 4 || ((uintptr_t)jb.part & 15) ||
+                        ((uintptr_t)jb.out & 15)))
+      return hipErrorInvalidValue;
+    jb.block0 = nb;
+    const int64_t pieces = (int64_t)jb.rows * (jb.cols / jb.vec);
+    nb += (int)blocks(pieces, 256 / jb.groups);
+  }
+  if (nb == 0) return hipSuccess;
+  k_reduce_jobs<<<nb, 256, 0, s>>>(J);
   return hipGetLastError();
 }
 hipError_t launch_colsum_final(const float* part, int chunks, int N, float* out, hipStream_t s) {
