@@ -566,27 +566,41 @@ hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, v
   const Net& n = c->net[ni];
   const int nl = (int)n.L.size();
   const Lay& H = n.L[nl - 1];
-  HK(red_room(c, 0, 3, s));
-  const int chunks = colsum_chunks(c->Bp);
-  float* cpart = red_alloc(c, 0, (int64_t)chunks * H.in_p);
-  float* cextra = red_alloc(c, 0, chunks);
-  if (!cpart || !cextra) return hipErrorOutOfMemory;
-  ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, cpart, cextra};
-  HK(timed(c, "colsum", c->Bp, H.in_p, 1, 0.0, (double)c->Bp * H.in_p * es(c), s,
-           [&] { return launch_colsum_partial(c->bf16, cs, s); }));
-  HK(red_colsum(c, 0, cpart, chunks, H.in_p, c->G + H.w, cextra, c->G + H.b, s));
-  // dz of the last hidden layer comes from the head backward, which (with the mask
-  // as bits) also takes its column sums, the bias gradient; otherwise that is a
-  // separate column sum in the weight gradient. Every later dz comes from a dgrad
-  // that also produces its bias gradient.
+  // dz of the last hidden layer comes from the head backward. With the mask as bits,
+  // that kernel also takes the column sums of dz (the last hidden layer's bias
+  // gradient) and, reading the stored last hidden layer in the same pass, the output
+  // layer's weight and bias gradients; otherwise those come from a column-sum pass and
+  // the weight gradient. Every later dz comes from a dgrad that also produces its bias
+  // gradient.
   const bool hb_sums = bits[nl - 2] != nullptr;
+  HK(red_room(c, 0, 3, s));
+  if (!hb_sums) {
+    const int chunks = colsum_chunks(c->Bp);
+    float* cpart = red_alloc(c, 0, (int64_t)chunks * H.in_p);
+    float* cextra = red_alloc(c, 0, chunks);
+    if (!cpart || !cextra) return hipErrorOutOfMemory;
+    ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, cpart, cextra};
+    HK(timed(c, "colsum", c->Bp, H.in_p, 1, 0.0, (double)c->Bp * H.in_p * es(c), s,
+             [&] { return launch_colsum_partial(c->bf16, cs, s); }));
+    HK(red_colsum(c, 0, cpart, chunks, H.in_p, c->G + H.w, cextra, c->G + H.b, s));
+  }
   const int hblocks = head_bwd_blocks(c->Bp);
-  float* hpart = hb_sums ? red_alloc(c, 0, (int64_t)hblocks * n.L[nl - 2].out_p) : nullptr;
-  if (hb_sums && !hpart) return hipErrorOutOfMemory;
-  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp, hpart};
-  HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0, head_bwd_bytes(c, H.in_p, bits[nl - 2]), s,
+  float *hpart = nullptr, *wpart = nullptr, *wextra = nullptr;
+  if (hb_sums) {
+    hpart = red_alloc(c, 0, (int64_t)hblocks * H.in_p);
+    wpart = red_alloc(c, 0, (int64_t)hblocks * H.in_p);
+    wextra = red_alloc(c, 0, hblocks);
+    if (!hpart || !wpart || !wextra) return hipErrorOutOfMemory;
+  }
+  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp, hpart,
+                 nullptr, nullptr, wpart, wextra};
+  HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0,
+           head_bwd_bytes(c, H.in_p, bits[nl - 2]) + (hb_sums ? (double)c->Bp * H.in_p * es(c) : 0.0), s,
            [&] { return launch_head_bwd(c->bf16, hb, s); }));
-  if (hb_sums) HK(red_colsum(c, 0, hpart, hblocks, n.L[nl - 2].out_p, c->G + n.L[nl - 2].b, nullptr, nullptr, s));
+  if (hb_sums) {
+    HK(red_colsum(c, 0, hpart, hblocks, H.in_p, c->G + n.L[nl - 2].b, nullptr, nullptr, s));
+    HK(red_colsum(c, 0, wpart, hblocks, H.in_p, c->G + H.w, wextra, c->G + H.b, s));
+  }
   int cur = 0;
   for (int l = nl - 2; l >= 0; --l) {
     const Lay& L = n.L[l];

@@ -59,6 +59,10 @@ struct HeadBwdArgs {
   // map[r] of the product (dq, bits read there), a zero row where map[r] < 0; rows
   // from *m_dyn on are not written. Row maps come from launch_minq_split.
   const int32_t* map; const int32_t* m_dyn;
+  // With colpart, when set: the output layer's weight and bias gradients over each
+  // block of rows, wpart[block, k] = sum of rnd(dq[b]) H[b, k] and wpart_extra[block] =
+  // sum of rnd(dq[b]) (H: the stored last hidden layer, read in the same pass).
+  float* wpart; float* wpart_extra;
 };
 
 // Sampler observations -> actor operand rows: x[r, c] = obs[r, c] for r < n, c < O;

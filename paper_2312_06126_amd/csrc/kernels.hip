@@ -291,18 +291,22 @@ __global__ void __launch_bounds__(256) k_head_bwd(HeadBwdArgs a) {
 // (kv = K / 8) in rows t / kv, t / kv + rpi, ... (rpi = 256 / kv). With colpart,
 // the column sums of the stored (rounded) values over the block's rows go to
 // colpart[block, :]: per thread over its rows, then over the rpi threads of a
-// column group in order.
+// column group in order. With wpart, the output layer's weight-gradient sums of the
+// block's rows are taken the same way from H, read in the same pass.
 constexpr int HB_ROWS = 64;
 __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
   extern __shared__ uint32_t wsh[];   // [K / 32][HB_ROWS], then [rpi][K] floats for the sums
   __shared__ int src_row[HB_ROWS];    // product row of each dH row of the block, -1: zero row
+  __shared__ float dq_row[HB_ROWS];   // rnd(dq) of each row
   const int nw = a.K / 32, kv = a.K / 8, rpi = 256 / kv;
   const int r0 = blockIdx.x * HB_ROWS;
   const int rows = a.m_dyn ? min(a.rows, *a.m_dyn) : a.rows;
   if (r0 >= rows) return;
   if (threadIdx.x < HB_ROWS) {
     const int b = r0 + threadIdx.x;
-    src_row[threadIdx.x] = b < rows ? (a.map ? a.map[b] : b) : -1;
+    const int src = b < rows ? (a.map ? a.map[b] : b) : -1;
+    src_row[threadIdx.x] = src;
+    dq_row[threadIdx.x] = src >= 0 ? bf2f(f2bf(a.dq[src])) : 0.0f;
   }
   __syncthreads();
   for (int t = threadIdx.x; t < nw * HB_ROWS; t += blockDim.x) {
@@ -313,14 +317,23 @@ __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
   const bf16_t* w = static_cast<const bf16_t*>(a.w);
   const int cg = threadIdx.x % kv, rs = threadIdx.x / kv, k = cg * 8;
   float cs[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+  float ws[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
   if (rs < rpi) {
     const uint4 w4 = *reinterpret_cast<const uint4*>(w + k);
     const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
     for (int r = rs; r < HB_ROWS; r += rpi) {
       const int b = r0 + r;
       if (b >= rows) break;
-      const int src = src_row[r];
-      const float dq = src >= 0 ? bf2f(f2bf(a.dq[src])) : 0.0f;
+      const float dq = dq_row[r];
+      if (a.wpart) {
+        const uint4 h4 = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(a.H) + (int64_t)b * a.ld + k);
+        const uint32_t hh[4] = {h4.x, h4.y, h4.z, h4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          ws[2 * e] = fmaf(dq, bf2f((bf16_t)(hh[e] & 0xFFFFu)), ws[2 * e]);
+          ws[2 * e + 1] = fmaf(dq, bf2f((bf16_t)(hh[e] >> 16)), ws[2 * e + 1]);
+        }
+      }
       const uint32_t wd = wsh[(k >> 5) * HB_ROWS + r] >> (k & 31);
       uint32_t o[4];
 #pragma unroll
@@ -346,6 +359,23 @@ __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
     float t = 0.0f;
     for (int q = 0; q < rpi; ++q) t += ssh[q * a.K + c];
     a.colpart[(int64_t)blockIdx.x * a.K + c] = t;
+  }
+  if (!a.wpart) return;   // uniform per block
+  __syncthreads();
+  if (rs < rpi) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ssh[rs * a.K + k + e] = ws[e];
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < a.K; c += blockDim.x) {
+    float t = 0.0f;
+    for (int q = 0; q < rpi; ++q) t += ssh[q * a.K + c];
+    a.wpart[(int64_t)blockIdx.x * a.K + c] = t;
+  }
+  if (threadIdx.x == 0) {
+    float t = 0.0f;
+    for (int r = 0; r < HB_ROWS; ++r) t += dq_row[r];
+    a.wpart_extra[blockIdx.x] = t;
   }
 }
 
@@ -868,6 +898,7 @@ hipError_t launch_head_bwd(bool bf16, const HeadBwdArgs& a, hipStream_t s) {
   const int vec = bf16 ? 8 : 4;
   if (a.K % vec || a.ld % vec) return hipErrorInvalidValue;
   if ((a.map || a.m_dyn) && (!a.bits || a.colpart)) return hipErrorInvalidValue;
+  if (a.wpart && (!a.colpart || !a.wpart_extra)) return hipErrorInvalidValue;
   if (a.bits) {
     if (!bf16 || a.K % 32 || a.K / 8 > 256 || a.ldbits < a.rows) return hipErrorInvalidValue;
     const size_t lds = (size_t)(a.K / 32) * HB_ROWS * 4 + (a.colpart ? (size_t)(256 / (a.K / 8)) * a.K * 4 : 0);
