@@ -137,12 +137,14 @@ struct spz_ctx {
   int32_t* idx = nullptr;
   // critic-stream workspace
   void* cs_h[2] = {nullptr, nullptr};
+  void* cs_h2[2] = {nullptr, nullptr};   // target critic 2 (the twins run layer by layer)
   float *z2 = nullptr, *logp2 = nullptr, *qt1 = nullptr, *qt2 = nullptr, *y = nullptr;
   float *q1 = nullptr, *q2 = nullptr, *dq1 = nullptr, *dq2 = nullptr;
   std::vector<void*> hc[2];
   std::vector<uint32_t*> bhc[2];     // ReLU masks of hc as bits (null where not fused)
   float* c_rdot[2] = {nullptr, nullptr};   // row-dot partials of the critic stream (two heads in flight)
   void* c_dz[2] = {nullptr, nullptr};
+  void* c_dz2[2] = {nullptr, nullptr};   // critic 2
   double* c_lpart = nullptr;
   // actor-stream workspace
   std::vector<void*> ha;
@@ -156,8 +158,9 @@ struct spz_ctx {
   // counts, and one layer's mask bits gathered by a map.
   bool row_split = false;
   int32_t *rmap = nullptr, *rrows = nullptr, *rcnt = nullptr;
-  uint32_t* rbits = nullptr;
+  uint32_t *rbits = nullptr, *rbits2 = nullptr;
   void* a_dz[2] = {nullptr, nullptr};
+  void* a_dz2[2] = {nullptr, nullptr};   // critic 2's action-gradient chain
   void* dzh = nullptr;
   double* a_lpart = nullptr;
   // Deferred gradient reductions of the critic part (0) and the actor part (1): the
@@ -176,7 +179,7 @@ struct spz_ctx {
   hipStream_t sg = nullptr;
   hipStream_t last = nullptr;
   bool has_last = false;   // an update was enqueued on `last` (which may be the null stream)
-  std::vector<void*> cs_hid;   // ping-pong view of cs_h, one entry per hidden layer
+  std::vector<void*> cs_hid, cs_hid2;   // ping-pong views of cs_h, cs_h2, one entry per hidden layer
   std::vector<void*> allocs;
   // kernel timing
   struct ProfKey { std::string name; int M, N, K; double flops, bytes; int64_t launches; double ms; };
@@ -425,191 +428,259 @@ int64_t red_need(const spz_ctx* c, int q, int Bp) {
   return n;
 }
 
-// Forward of net ni. X: [Bp, ldx] operand tensor (the first in_p(0) columns are read).
-// hid[l] receives hidden layer l and, where bits[l] is set, its ReLU mask as bits;
-// the actor head writes z [Bp, out_p] to head. A critic's output is described by *qs
-// for the kernel that consumes it: where the large-tile kernel covers the last hidden
-// layer, the output layer is folded into that product's epilogue (row-dot partials in
-// rdot, which the consumer sums in order and stores to head); otherwise a row-dot
-// kernel writes q [Bp] to head. The last hidden layer is then stored only when keep_last.
+// A matrix product, or the same product of both twin critics (g1): one launch where
+// gemm_pairs holds (recorded as one product of the stacked rows), else two.
+hipError_t gemm2(spz_ctx* c, const char* name, GemmMode mode, const GemmArgs& g0, const GemmArgs* g1, bool flops,
+                 hipStream_t s) {
+  auto fl = [&](const GemmArgs& g) { return flops ? 2.0 * g.M * g.N * g.K : 0.0; };
+  if (g1 && gemm_pairs(c->bf16, mode, g0, *g1))
+    return timed(c, name, 2 * g0.M, g0.N, g0.K, fl(g0) + fl(*g1), 0.0, s,
+                 [&] { return gemm_pair(c->bf16, mode, g0, *g1, s); });
+  HK(timed(c, name, g0.M, g0.N, g0.K, fl(g0), 0.0, s, [&] { return gemm(c->bf16, mode, g0, s); }));
+  if (!g1) return hipSuccess;
+  return timed(c, name, g1->M, g1->N, g1->K, fl(*g1), 0.0, s, [&] { return gemm(c->bf16, mode, *g1, s); });
+}
+
+// Per-net outputs of a forward: hidden layers (and their ReLU masks as bits where
+// set), the row-dot partials of a folded critic output layer, the head output (actor:
+// z [Bp, out_p]; critic: q [Bp]) and, for a critic, where q comes from.
+struct NetOut {
+  void* const* hid;
+  uint32_t* const* bits;
+  float* rdot;
+  float* head;
+  QSrc* qs;
+};
+
 bool fused_layer(const spz_ctx* c, const Lay& L) { return gemm_fused_ok(c->bf16, GEMM_FWD, c->Bp, L.out_p, L.in_p); }
 
-hipError_t forward(spz_ctx* c, int ni, bool target, const void* X, int64_t ldx, void* const* hid,
-                   uint32_t* const* bits, bool keep_last, float* rdot, float* head, hipStream_t s,
-                   QSrc* qs = nullptr) {
-  if (ni != 0 && !qs) return hipErrorInvalidValue;
-  const Net& n = c->net[ni];
-  const int nl = (int)n.L.size();
-  const void* in = X;
+// Forward of nets ni .. ni + nn - 1 on the same operand tensor X [Bp, ldx] (the first
+// in_p(0) columns are read), net k's outputs in o[k]; nn = 2 runs both critics layer
+// by layer, so that a layer's two products can share a launch. Where the large-tile
+// kernel covers the last hidden layer of a critic, the output layer is folded into
+// that product's epilogue (row-dot partials in o[k].rdot, which the kernel consuming q
+// sums in order and stores to o[k].head); otherwise a row-dot kernel writes q to
+// o[k].head. The last hidden layer is then stored only when keep_last.
+hipError_t forward(spz_ctx* c, int ni, int nn, bool target, const void* X, int64_t ldx, const NetOut* o,
+                   bool keep_last, hipStream_t s) {
+  if (nn < 1 || nn > 2 || (ni == 0 && nn != 1) || ni + nn > 3) return hipErrorInvalidValue;
+  for (int k = 0; k < nn; ++k)
+    if (ni != 0 && !o[k].qs) return hipErrorInvalidValue;
+  const int nl = (int)c->net[ni].L.size();
+  const void* in[2] = {X, X};
   int64_t ld = ldx;
   for (int l = 0; l < nl; ++l) {
-    const Lay& L = n.L[l];
+    const Lay& L = c->net[ni].L[l];   // the twin critics have the same shapes
     if (l == nl - 1 && ni != 0) {
-      *qs = QSrc{head, nullptr, 0, 0, nullptr};
-      RowdotArgs r{in, ld, L.in_p, c->Bp, wop(c, target, L.w), wf(c, target, L.b), head};
-      return timed(c, "rowdot", c->Bp, 1, L.in_p, 2.0 * c->Bp * L.in_p,
-                   (double)c->Bp * L.in_p * es(c) + 4.0 * c->Bp, s, [&] { return launch_rowdot(c->bf16, r, s); });
-    }
-    GemmArgs g{};
-    g.A = in; g.lda = ld;
-    g.B = wop(c, target, L.w); g.ldb = L.in_p;
-    g.bias = wf(c, target, L.b);
-    g.M = c->Bp; g.N = L.out_p; g.K = L.in_p;
-    bool folded = false;
-    if (l == nl - 1) {
-      g.C = head; g.ldc = L.out_p; g.relu = 0; g.out_f32 = 1;
-    } else {
-      g.C = hid[l]; g.ldc = L.out_p; g.relu = 1; g.out_f32 = 0;
-      if (bits && bits[l]) {
-        g.bits_out = bits[l];
-        g.ldbits = c->Bp;
+      for (int k = 0; k < nn; ++k) {
+        const Lay& Lk = c->net[ni + k].L[l];
+        *o[k].qs = QSrc{o[k].head, nullptr, 0, 0, nullptr};
+        RowdotArgs r{in[k], ld, L.in_p, c->Bp, wop(c, target, Lk.w), wf(c, target, Lk.b), o[k].head};
+        HK(timed(c, "rowdot", c->Bp, 1, L.in_p, 2.0 * c->Bp * L.in_p, (double)c->Bp * L.in_p * es(c) + 4.0 * c->Bp, s,
+                 [&] { return launch_rowdot(c->bf16, r, s); }));
       }
-      if (ni != 0 && l == nl - 2 && fused_layer(c, L)) {
-        const Lay& H = n.L[nl - 1];
-        g.rdot_w = wop(c, target, H.w);
-        g.rdot_part = rdot;
-        g.ldrd = c->Bp;
-        g.no_store = keep_last ? 0 : 1;
-        folded = true;
-      }
-    }
-    HK(timed(c, "gemm_fwd", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
-             [&] { return gemm(c->bf16, GEMM_FWD, g, s); }));
-    if (folded) {
-      const Lay& H = n.L[nl - 1];
-      *qs = QSrc{head, rdot, L.out_p / gemm_rdot_cols(c->Bp, L.out_p), c->Bp, wf(c, target, H.b)};
       return hipSuccess;
     }
-    in = g.C;
+    const bool folded = ni != 0 && l == nl - 2 && fused_layer(c, L);
+    GemmArgs g[2]{};
+    for (int k = 0; k < nn; ++k) {
+      const Lay& Lk = c->net[ni + k].L[l];
+      GemmArgs& gk = g[k];
+      gk.A = in[k]; gk.lda = ld;
+      gk.B = wop(c, target, Lk.w); gk.ldb = L.in_p;
+      gk.bias = wf(c, target, Lk.b);
+      gk.M = c->Bp; gk.N = L.out_p; gk.K = L.in_p;
+      if (l == nl - 1) {
+        gk.C = o[k].head; gk.ldc = L.out_p; gk.relu = 0; gk.out_f32 = 1;
+        continue;
+      }
+      gk.C = o[k].hid[l]; gk.ldc = L.out_p; gk.relu = 1; gk.out_f32 = 0;
+      if (o[k].bits && o[k].bits[l]) {
+        gk.bits_out = o[k].bits[l];
+        gk.ldbits = c->Bp;
+      }
+      if (folded) {
+        gk.rdot_w = wop(c, target, c->net[ni + k].L[nl - 1].w);
+        gk.rdot_part = o[k].rdot;
+        gk.ldrd = c->Bp;
+        gk.no_store = keep_last ? 0 : 1;
+      }
+    }
+    HK(gemm2(c, "gemm_fwd", GEMM_FWD, g[0], nn > 1 ? &g[1] : nullptr, true, s));
+    if (folded) {
+      for (int k = 0; k < nn; ++k)
+        *o[k].qs = QSrc{o[k].head, o[k].rdot, L.out_p / gemm_rdot_cols(c->Bp, L.out_p), c->Bp,
+                        wf(c, target, c->net[ni + k].L[nl - 1].b)};
+      return hipSuccess;
+    }
+    for (int k = 0; k < nn; ++k) in[k] = g[k].C;
     ld = L.out_p;
   }
   return hipSuccess;
 }
 
-// Weight gradient of layer L (split-K over the batch, slices reduced in order by the
-// part's deferred reduction q) and, when `bias`, its bias gradient as the column sums of dz.
-hipError_t wgrad(spz_ctx* c, int q, const void* dz, int64_t lddz, const void* X, int64_t ldx, const Lay& L,
+// Weight gradients of layer l of nets ni .. ni + nn - 1 from dz[k] [Bp, out_p] and the
+// layer inputs X[k] [Bp, ldx] (split-K over the batch, slices reduced in order by the
+// part's deferred reduction q) and, when `bias`, the bias gradients as the column sums
+// of dz[k].
+hipError_t wgrad(spz_ctx* c, int q, int ni, int nn, int l, const void* const* dz, const void* const* X, int64_t ldx,
                  bool bias, hipStream_t s) {
-  HK(red_room(c, q, 2, s));
-  GemmArgs g{};
-  g.A = dz; g.lda = lddz;
-  g.B = X; g.ldb = ldx;
-  g.M = L.out_p; g.N = L.in_p; g.K = c->Bp;
-  g.splits = wgrad_splits(c->bf16, g.M, g.N, g.K);
-  float* part = red_alloc(c, q, (int64_t)g.splits * g.M * g.N);
-  if (!part) return hipErrorOutOfMemory;
-  g.C = part; g.ldc = L.in_p;
-  HK(timed(c, "gemm_wgrad", g.M, g.N, g.K, 2.0 * g.M * g.N * g.K, 0.0, s,
-           [&] { return gemm(c->bf16, GEMM_WGRAD, g, s); }));
-  HK(red_job(c, q, ReduceJob{part, c->G + L.w, (int64_t)g.M * g.ldc, g.ldc, L.in_p, g.M, g.N, g.splits,
-                             splitk_groups(g.M, g.N, g.splits), 4, 0}, s));
+  HK(red_room(c, q, 2 * nn, s));
+  const Lay& L = c->net[ni].L[l];
+  GemmArgs g[2]{};
+  float* part[2] = {nullptr, nullptr};
+  for (int k = 0; k < nn; ++k) {
+    GemmArgs& gk = g[k];
+    gk.A = dz[k]; gk.lda = L.out_p;
+    gk.B = X[k]; gk.ldb = ldx;
+    gk.M = L.out_p; gk.N = L.in_p; gk.K = c->Bp;
+    gk.splits = wgrad_splits(c->bf16, gk.M, gk.N, gk.K);
+    if (!(part[k] = red_alloc(c, q, (int64_t)gk.splits * gk.M * gk.N))) return hipErrorOutOfMemory;
+    gk.C = part[k]; gk.ldc = L.in_p;
+  }
+  HK(gemm2(c, "gemm_wgrad", GEMM_WGRAD, g[0], nn > 1 ? &g[1] : nullptr, true, s));
+  for (int k = 0; k < nn; ++k)
+    HK(red_job(c, q, ReduceJob{part[k], c->G + c->net[ni + k].L[l].w, (int64_t)g[k].M * g[k].ldc, g[k].ldc, L.in_p,
+                               g[k].M, g[k].N, g[k].splits, splitk_groups(g[k].M, g[k].N, g[k].splits), 4, 0}, s));
   if (!bias) return hipSuccess;
   const int chunks = colsum_chunks(c->Bp);
-  float* cpart = red_alloc(c, q, (int64_t)chunks * L.out_p);
-  if (!cpart) return hipErrorOutOfMemory;
-  ColsumArgs cs{dz, lddz, L.out_p, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
-  HK(timed(c, "colsum", c->Bp, L.out_p, 0, 0.0, (double)c->Bp * L.out_p * es(c), s,
-           [&] { return launch_colsum_partial(c->bf16, cs, s); }));
-  return red_colsum(c, q, cpart, chunks, L.out_p, c->G + L.b, nullptr, nullptr, s);
+  for (int k = 0; k < nn; ++k) {
+    float* cpart = red_alloc(c, q, (int64_t)chunks * L.out_p);
+    if (!cpart) return hipErrorOutOfMemory;
+    ColsumArgs cs{dz[k], L.out_p, L.out_p, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
+    HK(timed(c, "colsum", c->Bp, L.out_p, 0, 0.0, (double)c->Bp * L.out_p * es(c), s,
+             [&] { return launch_colsum_partial(c->bf16, cs, s); }));
+    HK(red_colsum(c, q, cpart, chunks, L.out_p, c->G + c->net[ni + k].L[l].b, nullptr, nullptr, s));
+  }
+  return hipSuccess;
 }
 
-// Input gradient through layer L: out[Bp, N] = (dz . W) masked by mask > 0 (or by
-// the mask bits when given). Wt (or null): the transposed image of W, which both
-// GEMM kernels read instead of W. With
-// bias_out, also the column sums of the stored out (the bias gradient of the layer
-// below): fused into the product's epilogue where the large-tile kernel covers it,
-// the partial sums reduced by the part's deferred reduction q.
-// With m_dyn (a device-side count of leading rows), only those rows are computed.
-hipError_t dgrad(spz_ctx* c, const void* dz, const Lay& L, const void* W, int64_t ldw, const void* Wt, int N,
-                 const void* mask, const uint32_t* bits, void* out, int64_t ldo, bool out_f32, float* bias_out,
-                 int q, hipStream_t s, const int32_t* m_dyn = nullptr) {
-  if (bias_out) HK(red_room(c, q, 1, s));
-  GemmArgs g{};
-  g.m_dyn = m_dyn;
-  g.A = dz; g.lda = L.out_p;
-  g.B = W; g.ldb = ldw;
-  g.Bt = Wt; g.ldbt = L.out_p;
-  g.C = out; g.ldc = ldo; g.out_f32 = out_f32 ? 1 : 0;
-  if (bits) {
-    g.bits = bits;
-    g.ldbits = c->Bp;
-  } else if (mask) {
-    g.mask = mask;
-    g.ldm = ldo;
-  }
-  g.M = c->Bp; g.N = N; g.K = L.out_p;
-  const bool fused = bias_out && gemm_colsum_fused(c->bf16, GEMM_DGRAD, g.M, g.N, g.K);
+// One net's operands of an input-gradient product through a layer: dz [Bp, out_p], the
+// ReLU mask of the layer below (stored tensor, or bits), the output, where the column
+// sums of the output go (the bias gradient of the layer below; or null) and a
+// device-side count of leading rows (or null: every row).
+struct DgradIn {
+  const void* dz;
+  const void* mask;
+  const uint32_t* bits;
+  void* out;
+  float* bias_out;
+  const int32_t* m_dyn;
+};
+
+// Input gradients through layer l of nets ni .. ni + nn - 1: out = (dz . W) masked by
+// mask > 0 (or by the mask bits), N columns of W from column col0 on (row stride ldw),
+// or, with `transposed`, the layer's transposed weight image, which both GEMM kernels
+// then read instead (bf16 contexts; float32 contexts have none and read W). Column sums
+// of the stored out go to bias_out: fused into the product's epilogue where the
+// large-tile kernel covers it, the partials reduced by the part's deferred reduction q.
+hipError_t dgrad(spz_ctx* c, int ni, int nn, int l, const DgradIn* d, int col0, int64_t ldw, bool transposed, int N,
+                 int64_t ldo, bool out_f32, int q, hipStream_t s) {
+  const Lay& L = c->net[ni].L[l];
+  const bool sums = d[0].bias_out != nullptr;
+  for (int k = 1; k < nn; ++k)
+    if ((d[k].bias_out != nullptr) != sums || (d[k].m_dyn != nullptr) != (d[0].m_dyn != nullptr))
+      return hipErrorInvalidValue;
+  if (sums) HK(red_room(c, q, nn, s));
+  const bool fused = sums && gemm_colsum_fused(c->bf16, GEMM_DGRAD, c->Bp, N, L.out_p);
   const int chunks = fused ? c->Bp / 256 : colsum_chunks(c->Bp);
-  float* cpart = nullptr;
-  if (bias_out && !(cpart = red_alloc(c, q, (int64_t)chunks * N))) return hipErrorOutOfMemory;
-  if (fused) {
-    g.colsum = cpart;
-    g.ldcs = N;
+  GemmArgs g[2]{};
+  float* cpart[2] = {nullptr, nullptr};
+  for (int k = 0; k < nn; ++k) {
+    const Lay& Lk = c->net[ni + k].L[l];
+    GemmArgs& gk = g[k];
+    gk.m_dyn = d[k].m_dyn;
+    gk.A = d[k].dz; gk.lda = L.out_p;
+    gk.B = elem(c, wop(c, false, Lk.w), col0); gk.ldb = ldw;
+    gk.Bt = transposed ? wt(c, Lk) : nullptr; gk.ldbt = L.out_p;
+    gk.C = d[k].out; gk.ldc = ldo; gk.out_f32 = out_f32 ? 1 : 0;
+    if (d[k].bits) {
+      gk.bits = d[k].bits;
+      gk.ldbits = c->Bp;
+    } else if (d[k].mask) {
+      gk.mask = d[k].mask;
+      gk.ldm = ldo;
+    }
+    gk.M = c->Bp; gk.N = N; gk.K = L.out_p;
+    if (sums && !(cpart[k] = red_alloc(c, q, (int64_t)chunks * N))) return hipErrorOutOfMemory;
+    if (fused) {
+      gk.colsum = cpart[k];
+      gk.ldcs = N;
+    }
   }
   // Row-restricted products do a data-dependent amount of work: their records carry
   // the launch shape and no flop count.
-  HK(timed(c, m_dyn ? "gemm_dgrad_rows" : "gemm_dgrad", g.M, g.N, g.K, m_dyn ? 0.0 : 2.0 * g.M * g.N * g.K, 0.0, s,
-           [&] { return gemm(c->bf16, GEMM_DGRAD, g, s); }));
-  if (!bias_out) return hipSuccess;
-  if (!fused) {
-    ColsumArgs cs{out, ldo, N, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
-    HK(timed(c, "colsum", c->Bp, N, 0, 0.0, (double)c->Bp * N * es(c), s,
-             [&] { return launch_colsum_partial(c->bf16, cs, s); }));
+  const bool rows = d[0].m_dyn != nullptr;
+  HK(gemm2(c, rows ? "gemm_dgrad_rows" : "gemm_dgrad", GEMM_DGRAD, g[0], nn > 1 ? &g[1] : nullptr, !rows, s));
+  if (!sums) return hipSuccess;
+  for (int k = 0; k < nn; ++k) {
+    if (!fused) {
+      ColsumArgs cs{d[k].out, ldo, N, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart[k], nullptr};
+      HK(timed(c, "colsum", c->Bp, N, 0, 0.0, (double)c->Bp * N * es(c), s,
+               [&] { return launch_colsum_partial(c->bf16, cs, s); }));
+    }
+    HK(red_colsum(c, q, cpart[k], chunks, N, d[k].bias_out, nullptr, nullptr, s));
   }
-  return red_colsum(c, q, cpart, chunks, N, bias_out, nullptr, nullptr, s);
+  return hipSuccess;
 }
 
-// Critic ni in {1, 2}: weight and bias gradients of L = sum_b dq[b] q[b] given the
-// stored hidden activations hid of the forward on X.
-hipError_t critic_backward(spz_ctx* c, int ni, const float* dq, const void* X, void* const* hid,
-                           uint32_t* const* bits, hipStream_t s) {
-  const Net& n = c->net[ni];
-  const int nl = (int)n.L.size();
-  const Lay& H = n.L[nl - 1];
+// Both critics: weight and bias gradients of L = sum_b dq_k[b] q_k[b] given the stored
+// hidden activations hid[k] (ReLU masks bits[k]) of the forward on X, layer by layer so
+// that the twins' products can share launches.
+hipError_t critic_backward(spz_ctx* c, const float* const* dq, const void* X, void* const* const* hid,
+                           uint32_t* const* const* bits, hipStream_t s) {
+  const int nl = (int)c->net[1].L.size();
   // dz of the last hidden layer comes from the head backward. With the mask as bits,
   // that kernel also takes the column sums of dz (the last hidden layer's bias
   // gradient) and, reading the stored last hidden layer in the same pass, the output
   // layer's weight and bias gradients; otherwise those come from a column-sum pass and
   // the weight gradient. Every later dz comes from a dgrad that also produces its bias
   // gradient.
-  const bool hb_sums = bits[nl - 2] != nullptr;
-  HK(red_room(c, 0, 3, s));
-  if (!hb_sums) {
-    const int chunks = colsum_chunks(c->Bp);
-    float* cpart = red_alloc(c, 0, (int64_t)chunks * H.in_p);
-    float* cextra = red_alloc(c, 0, chunks);
-    if (!cpart || !cextra) return hipErrorOutOfMemory;
-    ColsumArgs cs{hid[nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq, 1, cpart, cextra};
-    HK(timed(c, "colsum", c->Bp, H.in_p, 1, 0.0, (double)c->Bp * H.in_p * es(c), s,
-             [&] { return launch_colsum_partial(c->bf16, cs, s); }));
-    HK(red_colsum(c, 0, cpart, chunks, H.in_p, c->G + H.w, cextra, c->G + H.b, s));
-  }
-  const int hblocks = head_bwd_blocks(c->Bp);
-  float *hpart = nullptr, *wpart = nullptr, *wextra = nullptr;
-  if (hb_sums) {
-    hpart = red_alloc(c, 0, (int64_t)hblocks * H.in_p);
-    wpart = red_alloc(c, 0, (int64_t)hblocks * H.in_p);
-    wextra = red_alloc(c, 0, hblocks);
-    if (!hpart || !wpart || !wextra) return hipErrorOutOfMemory;
-  }
-  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->c_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp, hpart,
-                 nullptr, nullptr, wpart, wextra};
-  HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0,
-           head_bwd_bytes(c, H.in_p, bits[nl - 2]) + (hb_sums ? (double)c->Bp * H.in_p * es(c) : 0.0), s,
-           [&] { return launch_head_bwd(c->bf16, hb, s); }));
-  if (hb_sums) {
-    HK(red_colsum(c, 0, hpart, hblocks, H.in_p, c->G + n.L[nl - 2].b, nullptr, nullptr, s));
-    HK(red_colsum(c, 0, wpart, hblocks, H.in_p, c->G + H.w, wextra, c->G + H.b, s));
+  const bool hb_sums = bits[0][nl - 2] != nullptr;
+  void* dzb[2][2] = {{c->c_dz[0], c->c_dz[1]}, {c->c_dz2[0], c->c_dz2[1]}};
+  for (int k = 0; k < 2; ++k) {
+    const Net& n = c->net[1 + k];
+    const Lay& H = n.L[nl - 1];
+    HK(red_room(c, 0, 3, s));
+    if (!hb_sums) {
+      const int chunks = colsum_chunks(c->Bp);
+      float* cpart = red_alloc(c, 0, (int64_t)chunks * H.in_p);
+      float* cextra = red_alloc(c, 0, chunks);
+      if (!cpart || !cextra) return hipErrorOutOfMemory;
+      ColsumArgs cs{hid[k][nl - 2], H.in_p, H.in_p, c->Bp, COLSUM_CHUNK, dq[k], 1, cpart, cextra};
+      HK(timed(c, "colsum", c->Bp, H.in_p, 1, 0.0, (double)c->Bp * H.in_p * es(c), s,
+               [&] { return launch_colsum_partial(c->bf16, cs, s); }));
+      HK(red_colsum(c, 0, cpart, chunks, H.in_p, c->G + H.w, cextra, c->G + H.b, s));
+    }
+    const int hblocks = head_bwd_blocks(c->Bp);
+    float *hpart = nullptr, *wpart = nullptr, *wextra = nullptr;
+    if (hb_sums) {
+      hpart = red_alloc(c, 0, (int64_t)hblocks * H.in_p);
+      wpart = red_alloc(c, 0, (int64_t)hblocks * H.in_p);
+      wextra = red_alloc(c, 0, hblocks);
+      if (!hpart || !wpart || !wextra) return hipErrorOutOfMemory;
+    }
+    HeadBwdArgs hb{dq[k], wop(c, false, H.w), hid[k][nl - 2], dzb[k][0], H.in_p, H.in_p, c->Bp, bits[k][nl - 2],
+                   c->Bp, hpart, nullptr, nullptr, wpart, wextra};
+    HK(timed(c, "head_bwd", c->Bp, H.in_p, 0, 0.0,
+             head_bwd_bytes(c, H.in_p, bits[k][nl - 2]) + (hb_sums ? (double)c->Bp * H.in_p * es(c) : 0.0), s,
+             [&] { return launch_head_bwd(c->bf16, hb, s); }));
+    if (hb_sums) {
+      HK(red_colsum(c, 0, hpart, hblocks, H.in_p, c->G + n.L[nl - 2].b, nullptr, nullptr, s));
+      HK(red_colsum(c, 0, wpart, hblocks, H.in_p, c->G + H.w, wextra, c->G + H.b, s));
+    }
   }
   int cur = 0;
   for (int l = nl - 2; l >= 0; --l) {
-    const Lay& L = n.L[l];
-    const void* Xl = l == 0 ? X : hid[l - 1];
-    const int64_t ldx = l == 0 ? c->Kc : L.in_p;
-    HK(wgrad(c, 0, c->c_dz[cur], L.out_p, Xl, ldx, L, l == nl - 2 && !hb_sums, s));
+    const Lay& L = c->net[1].L[l];
+    const void* dz[2] = {dzb[0][cur], dzb[1][cur]};
+    const void* Xl[2] = {l == 0 ? X : hid[0][l - 1], l == 0 ? X : hid[1][l - 1]};
+    HK(wgrad(c, 0, 1, 2, l, dz, Xl, l == 0 ? c->Kc : L.in_p, l == nl - 2 && !hb_sums, s));
     if (l > 0) {
-      HK(dgrad(c, c->c_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, hid[l - 1], bits[l - 1],
-               c->c_dz[cur ^ 1], L.in_p, false, c->G + n.L[l - 1].b, 0, s));
+      DgradIn d[2];
+      for (int k = 0; k < 2; ++k)
+        d[k] = DgradIn{dz[k], hid[k][l - 1], bits[k][l - 1], dzb[k][cur ^ 1], c->G + c->net[1 + k].L[l - 1].b, nullptr};
+      HK(dgrad(c, 1, 2, l, d, 0, L.in_p, true, L.in_p, L.in_p, false, 0, s));
       cur ^= 1;
     }
   }
@@ -629,43 +700,51 @@ hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* 
   int cur = 0;
   for (int l = nl - 2; l >= 1; --l) {
     const Lay& L = n.L[l];
-    HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, hid[l - 1], bits[l - 1],
-             c->a_dz[cur ^ 1], L.in_p, false, nullptr, 1, s));
+    const DgradIn d{c->a_dz[cur], hid[l - 1], bits[l - 1], c->a_dz[cur ^ 1], nullptr, nullptr};
+    HK(dgrad(c, ni, 1, l, &d, 0, L.in_p, true, L.in_p, L.in_p, false, 1, s));
     cur ^= 1;
   }
-  const Lay& L0 = n.L[0];
-  return dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, nullptr, c->Ap, nullptr, nullptr, da,
-               c->Ap, true, nullptr, 1, s);
+  const DgradIn d0{c->a_dz[cur], nullptr, nullptr, da, nullptr, nullptr};
+  return dgrad(c, ni, 1, 0, &d0, c->Ka, c->Kc, false, c->Ap, c->Ap, true, 1, s);
 }
 
-// The same restricted to the rows listed in map (padded with -1 to the device-side
-// length *rows): the head backward gathers those rows, every later product runs on
-// the first *rows rows only, and the action gradient is scattered back to da's rows
-// (rows of da outside the map are left as they are). Each row's arithmetic is that
-// of the unrestricted chain.
-hipError_t critic_action_grad_rows(spz_ctx* c, int ni, const float* dq, void* const* hid, uint32_t* const* bits,
-                                   const int32_t* map, const int32_t* rows, float* da, hipStream_t s) {
-  const Net& n = c->net[ni];
-  const int nl = (int)n.L.size();
-  const Lay& H = n.L[nl - 1];
-  HeadBwdArgs hb{dq, wop(c, false, H.w), hid[nl - 2], c->a_dz[0], H.in_p, H.in_p, c->Bp, bits[nl - 2], c->Bp,
-                 nullptr, map, rows};
-  HK(timed(c, "head_bwd_rows", c->Bp, H.in_p, 0, 0.0, 0.0, s, [&] { return launch_head_bwd(c->bf16, hb, s); }));
+// The same for both critics, each restricted to the rows listed in its map (critic k:
+// rmap + k Bp, padded with -1 to the device-side length rrows[k]): the head backward
+// gathers those rows, every later product runs on the leading rows only (the twins'
+// products layer by layer, so that they can share launches), and each action gradient
+// is scattered back to da's rows (rows of da outside the maps are left as they are).
+// Each row's arithmetic is that of the unrestricted chain.
+hipError_t critic_action_grad_rows(spz_ctx* c, const float* const* dq, void* const* const* hid,
+                                   uint32_t* const* const* bits, float* da, hipStream_t s) {
+  const int nl = (int)c->net[1].L.size();
+  void* dzb[2][2] = {{c->a_dz[0], c->a_dz[1]}, {c->a_dz2[0], c->a_dz2[1]}};
+  uint32_t* rb[2] = {c->rbits, c->rbits2};
+  for (int k = 0; k < 2; ++k) {
+    const Lay& H = c->net[1 + k].L[nl - 1];
+    HeadBwdArgs hb{dq[k], wop(c, false, H.w), hid[k][nl - 2], dzb[k][0], H.in_p, H.in_p, c->Bp, bits[k][nl - 2], c->Bp,
+                   nullptr, c->rmap + (int64_t)k * c->Bp, c->rrows + k};
+    HK(timed(c, "head_bwd_rows", c->Bp, H.in_p, 0, 0.0, 0.0, s, [&] { return launch_head_bwd(c->bf16, hb, s); }));
+  }
   int cur = 0;
   for (int l = nl - 2; l >= 1; --l) {
-    const Lay& L = n.L[l];
-    RowBitsGatherArgs gb{bits[l - 1], c->rbits, c->Bp, L.in_p / 32, map, rows, c->Bp};
-    HK(timed(c, "row_bits_gather", c->Bp, L.in_p, 0, 0.0, 0.0, s, [&] { return launch_row_bits_gather(gb, s); }));
-    HK(dgrad(c, c->a_dz[cur], L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, nullptr, c->rbits, c->a_dz[cur ^ 1],
-             L.in_p, false, nullptr, 1, s, rows));
+    const Lay& L = c->net[1].L[l];
+    DgradIn d[2];
+    for (int k = 0; k < 2; ++k) {
+      RowBitsGatherArgs gb{bits[k][l - 1], rb[k], c->Bp, L.in_p / 32, c->rmap + (int64_t)k * c->Bp, c->rrows + k, c->Bp};
+      HK(timed(c, "row_bits_gather", c->Bp, L.in_p, 0, 0.0, 0.0, s, [&] { return launch_row_bits_gather(gb, s); }));
+      d[k] = DgradIn{dzb[k][cur], nullptr, rb[k], dzb[k][cur ^ 1], nullptr, c->rrows + k};
+    }
+    HK(dgrad(c, 1, 2, l, d, 0, L.in_p, true, L.in_p, L.in_p, false, 1, s));
     cur ^= 1;
   }
-  // The action gradient of the listed rows lands in da2 (free here) and then in da.
-  const Lay& L0 = n.L[0];
-  HK(dgrad(c, c->a_dz[cur], L0, elem(c, wop(c, false, L0.w), c->Ka), c->Kc, nullptr, c->Ap, nullptr, nullptr,
-           c->da2, c->Ap, true, nullptr, 1, s, rows));
-  RowScatterArgs sa{c->da2, da, c->Ap, c->Ap, map, rows, c->Bp};
-  return timed(c, "row_scatter", c->Bp, c->Ap, 0, 0.0, 0.0, s, [&] { return launch_row_scatter(sa, s); });
+  // Each action gradient of the listed rows lands in da2 (free here) and then in da.
+  for (int k = 0; k < 2; ++k) {
+    const DgradIn d0{dzb[k][cur], nullptr, nullptr, c->da2, nullptr, c->rrows + k};
+    HK(dgrad(c, 1 + k, 1, 0, &d0, c->Ka, c->Kc, false, c->Ap, c->Ap, true, 1, s));
+    RowScatterArgs sa{c->da2, da, c->Ap, c->Ap, c->rmap + (int64_t)k * c->Bp, c->rrows + k, c->Bp};
+    HK(timed(c, "row_scatter", c->Bp, c->Ap, 0, 0.0, 0.0, s, [&] { return launch_row_scatter(sa, s); }));
+  }
+  return hipSuccess;
 }
 
 hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
@@ -676,11 +755,10 @@ hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
   for (int l = nl - 1; l >= 0; --l) {
     const Lay& L = n.L[l];
     const void* Xl = l == 0 ? c->xsa : c->ha[l - 1];
-    const int64_t ldx = l == 0 ? c->Kc : L.in_p;
-    HK(wgrad(c, 1, cur, L.out_p, Xl, ldx, L, l == nl - 1, s));
+    HK(wgrad(c, 1, 0, 1, l, &cur, &Xl, l == 0 ? c->Kc : L.in_p, l == nl - 1, s));
     if (l > 0) {
-      HK(dgrad(c, cur, L, wop(c, false, L.w), L.in_p, wt(c, L), L.in_p, c->ha[l - 1], c->bha[l - 1], c->a_dz[nxt],
-               L.in_p, false, c->G + n.L[l - 1].b, 1, s));
+      const DgradIn d{cur, c->ha[l - 1], c->bha[l - 1], c->a_dz[nxt], c->G + n.L[l - 1].b, nullptr};
+      HK(dgrad(c, 0, 1, l, &d, 0, L.in_p, true, L.in_p, L.in_p, false, 1, s));
       cur = c->a_dz[nxt];
       nxt ^= 1;
     }
@@ -695,32 +773,37 @@ const float* log_alpha_ptr(const spz_ctx* c) { return c->P + c->la; }
 hipError_t critic_part(spz_ctx* c, hipStream_t s) {
   const int pa = c->net[0].L.back().out_p;
   const spz_hparams& hp = c->hp;
+  const NetOut act{c->cs_hid.data(), nullptr, nullptr, c->z2, nullptr};
   if (!c->td3) {
-    HK(forward(c, 0, false, c->xs2, c->Kc, c->cs_hid.data(), nullptr, true, nullptr, c->z2, s));
+    HK(forward(c, 0, 1, false, c->xs2, c->Kc, &act, true, s));
     SacHeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_TGT, hp.log_std_min, hp.log_std_max,
                   c->xs2, c->Kc, c->Ka, c->logp2, nullptr, nullptr, nullptr};
     HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, h, s); }));
   } else {
-    HK(forward(c, 0, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, true, nullptr, c->z2, s));
+    HK(forward(c, 0, 1, true, c->xs2, c->Kc, &act, true, s));
     Td3HeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, 1, hp.policy_noise, hp.noise_clip,
                   c->xs2, c->Kc, c->Ka, nullptr};
     HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
-  QSrc q1, q2;
-  HK(forward(c, 1, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, false, c->c_rdot[0], c->qt1, s, &q1));
-  HK(forward(c, 2, true, c->xs2, c->Kc, c->cs_hid.data(), nullptr, false, c->c_rdot[1], c->qt2, s, &q2));
-  TdArgs td{q1, q2, c->r, c->d, c->td3 ? nullptr : c->logp2, log_alpha_ptr(c), c->y, hp.gamma, c->B, c->Bp};
+  QSrc q[2];
+  const NetOut tgt[2] = {{c->cs_hid.data(), nullptr, c->c_rdot[0], c->qt1, &q[0]},
+                         {c->cs_hid2.data(), nullptr, c->c_rdot[1], c->qt2, &q[1]}};
+  HK(forward(c, 1, 2, true, c->xs2, c->Kc, tgt, false, s));
+  TdArgs td{q[0], q[1], c->r, c->d, c->td3 ? nullptr : c->logp2, log_alpha_ptr(c), c->y, hp.gamma, c->B, c->Bp};
   HK(timed(c, "td_target", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_td_target(td, s); }));
   // the target critics' partials were consumed by the TD target: their buffers are free
-  HK(forward(c, 1, false, c->xsa, c->Kc, c->hc[0].data(), c->bhc[0].data(), true, c->c_rdot[0], c->q1, s, &q1));
-  HK(forward(c, 2, false, c->xsa, c->Kc, c->hc[1].data(), c->bhc[1].data(), true, c->c_rdot[1], c->q2, s, &q2));
-  CriticLossArgs cl{q1, q2, c->y, c->dq1, c->dq2, c->c_lpart, c->B, c->Bp};
+  const NetOut onl[2] = {{c->hc[0].data(), c->bhc[0].data(), c->c_rdot[0], c->q1, &q[0]},
+                         {c->hc[1].data(), c->bhc[1].data(), c->c_rdot[1], c->q2, &q[1]}};
+  HK(forward(c, 1, 2, false, c->xsa, c->Kc, onl, true, s));
+  CriticLossArgs cl{q[0], q[1], c->y, c->dq1, c->dq2, c->c_lpart, c->B, c->Bp};
   HK(timed(c, "critic_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_critic_loss(cl, s); }));
   c->red[0].jobs.n = 0;
   c->red[0].off = 0;
   c->red[0].bytes = 0.0;
-  HK(critic_backward(c, 1, c->dq1, c->xsa, c->hc[0].data(), c->bhc[0].data(), s));
-  HK(critic_backward(c, 2, c->dq2, c->xsa, c->hc[1].data(), c->bhc[1].data(), s));
+  const float* dq[2] = {c->dq1, c->dq2};
+  void* const* hid[2] = {c->hc[0].data(), c->hc[1].data()};
+  uint32_t* const* bits[2] = {c->bhc[0].data(), c->bhc[1].data()};
+  HK(critic_backward(c, dq, c->xsa, hid, bits, s));
   return red_flush(c, 0, s);
 }
 
@@ -729,7 +812,8 @@ hipError_t critic_part(spz_ctx* c, hipStream_t s) {
 hipError_t actor_part(spz_ctx* c, hipStream_t s) {
   const int pa = c->net[0].L.back().out_p;
   const spz_hparams& hp = c->hp;
-  HK(forward(c, 0, false, c->xsa, c->Kc, c->ha.data(), c->bha.data(), true, nullptr, c->z, s));
+  const NetOut act{c->ha.data(), c->bha.data(), nullptr, c->z, nullptr};
+  HK(forward(c, 0, 1, false, c->xsa, c->Kc, &act, true, s));
   if (!c->td3) {
     SacHeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_POL, hp.log_std_min, hp.log_std_max,
                   c->xs_act, c->Kc, c->Ka, c->logp, c->th, c->se, c->lm};
@@ -738,13 +822,12 @@ hipError_t actor_part(spz_ctx* c, hipStream_t s) {
     Td3HeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, 0, 0.0f, 0.0f, c->xs_act, c->Kc, c->Ka, c->th};
     HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));
   }
-  QSrc qp1, qp2{};
-  HK(forward(c, 1, false, c->xs_act, c->Kc, c->hpc[0].data(), c->bhpc[0].data(), false, c->a_rdot[0], c->qp1, s,
-             &qp1));
-  if (!c->td3)
-    HK(forward(c, 2, false, c->xs_act, c->Kc, c->hpc[1].data(), c->bhpc[1].data(), false, c->a_rdot[1], c->qp2, s,
-               &qp2));
-  ActorLossArgs al{qp1, qp2, c->td3 ? 0 : 1, c->logp, log_alpha_ptr(c), c->dqp1,
+  // TD3's actor loss takes critic 1 only.
+  QSrc qp[2]{};
+  const NetOut cr[2] = {{c->hpc[0].data(), c->bhpc[0].data(), c->a_rdot[0], c->qp1, &qp[0]},
+                        {c->hpc[1].data(), c->bhpc[1].data(), c->a_rdot[1], c->qp2, &qp[1]}};
+  HK(forward(c, 1, c->td3 ? 1 : 2, false, c->xs_act, c->Kc, cr, false, s));
+  ActorLossArgs al{qp[0], qp[1], c->td3 ? 0 : 1, c->logp, log_alpha_ptr(c), c->dqp1,
                    c->td3 ? nullptr : c->dqp2, c->a_lpart, c->B, c->Bp, c->row_split ? c->rcnt : nullptr};
   HK(timed(c, "actor_loss", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_actor_loss(al, s); }));
   if (c->row_split) {
@@ -752,9 +835,10 @@ hipError_t actor_part(spz_ctx* c, hipStream_t s) {
     // only: each critic's chain runs on its own rows and both land in da1.
     MinqSplitArgs ms{c->qp1, c->qp2, c->rcnt, c->B, c->Bp, c->rmap, c->rmap + c->Bp, c->rrows};
     HK(timed(c, "minq_split", c->Bp, 0, 0, 0.0, 0.0, s, [&] { return launch_minq_split(ms, s); }));
-    HK(critic_action_grad_rows(c, 1, c->dqp1, c->hpc[0].data(), c->bhpc[0].data(), c->rmap, c->rrows, c->da1, s));
-    HK(critic_action_grad_rows(c, 2, c->dqp2, c->hpc[1].data(), c->bhpc[1].data(), c->rmap + c->Bp, c->rrows + 1,
-                               c->da1, s));
+    const float* dq[2] = {c->dqp1, c->dqp2};
+    void* const* hid[2] = {c->hpc[0].data(), c->hpc[1].data()};
+    uint32_t* const* bits[2] = {c->bhpc[0].data(), c->bhpc[1].data()};
+    HK(critic_action_grad_rows(c, dq, hid, bits, c->da1, s));
   } else {
     HK(critic_action_grad(c, 1, c->dqp1, c->hpc[0].data(), c->bhpc[0].data(), c->da1, s));
     if (!c->td3) HK(critic_action_grad(c, 2, c->dqp2, c->hpc[1].data(), c->bhpc[1].data(), c->da2, s));
@@ -977,8 +1061,11 @@ int setup(spz_ctx* c) {
   CK(dalloc(c, &c->dzh, (size_t)Bp * pa * e));
   for (int i = 0; i < 2; ++i) {
     CK(dalloc(c, &c->cs_h[i], hb));
+    CK(dalloc(c, &c->cs_h2[i], hb));
     CK(dalloc(c, &c->c_dz[i], hb));
+    CK(dalloc(c, &c->c_dz2[i], hb));
     CK(dalloc(c, &c->a_dz[i], hb));
+    CK(dalloc(c, &c->a_dz2[i], hb));
     c->hc[i].assign(nh, nullptr);
     c->hpc[i].assign(nh, nullptr);
     for (int l = 0; l < nh; ++l) {
@@ -988,9 +1075,11 @@ int setup(spz_ctx* c) {
   }
   c->ha.assign(nh, nullptr);
   c->cs_hid.assign(nh, nullptr);
+  c->cs_hid2.assign(nh, nullptr);
   for (int l = 0; l < nh; ++l) {
     CK(dalloc(c, &c->ha[l], (size_t)Bp * pad32(c->hidden[l]) * e));
     c->cs_hid[l] = c->cs_h[l & 1];
+    c->cs_hid2[l] = c->cs_h2[l & 1];
   }
   // ReLU masks as bits where the large-tile kernel produces and consumes them (the
   // same condition holds for every product that reads a layer's mask), and the
@@ -1026,6 +1115,7 @@ int setup(spz_ctx* c) {
     CK(dalloc_t(c, &c->rrows, 64));
     CK(dalloc_t(c, &c->rcnt, (size_t)(Bp / 256) * 4));
     CK(dalloc_t(c, &c->rbits, (size_t)Bp * (c->hmax / 32) * 4));
+    CK(dalloc_t(c, &c->rbits2, (size_t)Bp * (c->hmax / 32) * 4));
   }
   // deferred-reduction workspaces, sized for the created batch (spz_set_batch checks
   // that a smaller one fits)
@@ -1385,7 +1475,8 @@ int spz_act(spz_ctx* c, const float* obs, int64_t n, int32_t stochastic, uint32_
     if (e == hipSuccess) e = launch_obs_operand(c->bf16, oa, s);
     c->B = m;
     c->Bp = rows;
-    if (e == hipSuccess) e = forward(c, 0, false, c->xsp, c->Kc, c->ha.data(), nullptr, true, nullptr, c->z, s);
+    const NetOut out{c->ha.data(), nullptr, nullptr, c->z, nullptr};
+    if (e == hipSuccess) e = forward(c, 0, 1, false, c->xsp, c->Kc, &out, true, s);
     c->B = saveB;
     c->Bp = saveBp;
     ActHeadArgs ha{c->z, pa, c->A, m, r0, c->td3 ? 0 : 1, stochastic ? 1 : 0, c->seed, counter,
@@ -1461,7 +1552,8 @@ int spz_act_noalloc(spz_ctx* c, const float* obs, int64_t n, int32_t stochastic,
   c->B = (int)n;
   c->Bp = rows;
   c->prof = false;
-  const hipError_t e = forward(c, 0, false, xop, c->Ka, hid, nullptr, true, nullptr, z, s);
+  const NetOut out{hid, nullptr, nullptr, z, nullptr};
+  const hipError_t e = forward(c, 0, 1, false, xop, c->Ka, &out, true, s);
   c->B = saveB;
   c->Bp = saveBp;
   c->prof = saveProf;

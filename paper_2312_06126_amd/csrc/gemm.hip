@@ -422,7 +422,11 @@ bool gemm_fused_ok(bool bf16, GemmMode mode, int M, int N, int K) {
   return bf16 && N % 128 == 0 && big_gemm_fits(mode, M, N, K, 1);
 }
 
-hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
+namespace {
+
+// The launch contract of gemm(): hipSuccess when the product is valid; *big tells
+// whether it runs on the large-tile kernel.
+hipError_t route(bool bf16, GemmMode mode, const GemmArgs& g, bool* big) {
   if (g.colsum && !gemm_colsum_fused(bf16, mode, g.M, g.N, g.K)) return hipErrorInvalidValue;
   // A device-side row count: input-gradient products only, whole 256-row tiles, and
   // no per-tile column sums (the skipped tiles would leave theirs unwritten).
@@ -445,11 +449,40 @@ hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
   const int vec = bf16 ? 8 : 4;
   if (g.lda % vec || g.ldb % vec) return hipErrorInvalidValue;
   if (mode == GEMM_WGRAD && (g.splits < 1 || g.K % g.splits)) return hipErrorInvalidValue;
-  if (bf16 && big_gemm_fits(mode, g.M, g.N, g.K, mode == GEMM_WGRAD ? g.splits : 1) &&
-      big_epilogue_supported(mode, epilogue_flags(mode, g)) && (mode != GEMM_DGRAD || g.Bt) &&
-      big_gemm_ld_ok(mode, g))
-    return gemm_big(mode, g, s);
-  return gemm_generic(bf16, mode, g, s);
+  *big = bf16 && big_gemm_fits(mode, g.M, g.N, g.K, mode == GEMM_WGRAD ? g.splits : 1) &&
+         big_epilogue_supported(mode, epilogue_flags(mode, g)) && (mode != GEMM_DGRAD || g.Bt) &&
+         big_gemm_ld_ok(mode, g);
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s) {
+  bool big = false;
+  const hipError_t e = route(bf16, mode, g, &big);
+  if (e != hipSuccess) return e;
+  return big ? gemm_big(mode, g, s) : gemm_generic(bf16, mode, g, s);
+}
+
+hipError_t gemm_pair(bool bf16, GemmMode mode, const GemmArgs& g0, const GemmArgs& g1, hipStream_t s) {
+  bool big0 = false, big1 = false;
+  hipError_t e = route(bf16, mode, g0, &big0);
+  if (e == hipSuccess) e = route(bf16, mode, g1, &big1);
+  if (e != hipSuccess) return e;
+  // One launch when both take the large-tile kernel with the same launch shape and one
+  // product alone leaves compute units idle (fewer workgroups than 256).
+  if (big0 && big1 && gemm_pairs(bf16, mode, g0, g1)) return gemm_big_pair(mode, g0, g1, s);
+  e = gemm(bf16, mode, g0, s);
+  return e != hipSuccess ? e : gemm(bf16, mode, g1, s);
+}
+
+bool gemm_pairs(bool bf16, GemmMode mode, const GemmArgs& g0, const GemmArgs& g1) {
+  bool big0 = false, big1 = false;
+  if (route(bf16, mode, g0, &big0) != hipSuccess || route(bf16, mode, g1, &big1) != hipSuccess || !big0 || !big1)
+    return false;
+  return g0.M == g1.M && g0.N == g1.N && g0.K == g1.K && epilogue_flags(mode, g0) == epilogue_flags(mode, g1) &&
+         (mode != GEMM_WGRAD || g0.splits == g1.splits) && (!g0.m_dyn) == (!g1.m_dyn) &&
+         big_gemm_tiles(mode, g0) < 256;
 }
 
 int splitk_groups(int M, int N, int splits) {

@@ -658,9 +658,11 @@ __device__ inline void chunk_main_loop(const GemmArgs& g, f32x16 (&acc)[BM / WM 
 
 // One kernel per (product, column tile, epilogue variant): a runtime switch over the
 // variants inside one kernel let common code move above the switch and raised the
-// register pressure of every variant to the point of spilling.
+// register pressure of every variant to the point of spilling. A launch runs one
+// product or two of the same shape and epilogue (GemmPair: the twin critics' layers),
+// the second's tiles after the first's.
 template <int MODE, int BN, int F, bool RG>
-__global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int tiles_n) {
+__global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmPair pr, int tiles_m, int tiles_n) {
   constexpr bool AKC = MODE != GEMM_WGRAD;
   constexpr bool BKC = MODE == GEMM_FWD;
   using TA = BigTile<AKC, BM>;
@@ -671,17 +673,22 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   bf16_t* S = reinterpret_cast<bf16_t*>(smem);
 
-  // XCD-aware logical tile: contiguous logical ranges per XCD, column tiles fastest.
-  int total = gridDim.x;
+  // Tiles of each product. A device-side row count (input gradient) leaves only its
+  // leading row tiles; the tiles of both products are spread over the XCDs as one range.
+  const int per = tiles_m * tiles_n * (MODE == GEMM_WGRAD ? pr.g[0].splits : 1);
+  int t0 = per, t1 = pr.n > 1 ? per : 0;
   if constexpr (MODE == GEMM_DGRAD) {
-    // A device-side row count: only its tiles run, spread over the XCDs as usual.
-    if (g.m_dyn) {
-      total = (*g.m_dyn / BM) * tiles_n;
-      if ((int)blockIdx.x >= total) return;
-    }
+    if (pr.g[0].m_dyn) t0 = (*pr.g[0].m_dyn / BM) * tiles_n;
+    if (pr.n > 1 && pr.g[1].m_dyn) t1 = (*pr.g[1].m_dyn / BM) * tiles_n;
   }
+  const int total = t0 + t1;
+  if ((int)blockIdx.x >= total) return;
+  // XCD-aware logical tile: contiguous logical ranges per XCD, column tiles fastest.
   int L = blockIdx.x;
   if ((total & 7) == 0) L = (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3);
+  const int pi = L >= t0 ? 1 : 0;
+  const GemmArgs& g = pr.g[pi];
+  L -= pi * t0;
   const int nt = L % tiles_n;
   const int mt = (L / tiles_n) % tiles_m;
   const int z = L / (tiles_n * tiles_m);
@@ -838,7 +845,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm_big(GemmArgs g, int tiles_m, int
 }
 
 template <int MODE, int BN, int F, bool RG>
-hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
+hipError_t launch_big_f(const GemmPair& p, hipStream_t s) {
+  const GemmArgs& g = p.g[0];
   using TA = BigTile<MODE != GEMM_WGRAD, BM>;
   using TB = BigTile<MODE == GEMM_FWD, BN>;
   const size_t tiles = MODE != GEMM_WGRAD ? 2 * ChunkLds<BN>::BYTES
@@ -854,19 +862,20 @@ hipError_t launch_big_f(const GemmArgs& g, hipStream_t s) {
   }
   const int tiles_m = g.M / BM, tiles_n = (g.N + BN - 1) / BN;
   const int splits = MODE == GEMM_WGRAD ? g.splits : 1;
-  k_gemm_big<MODE, BN, F, RG><<<tiles_m * tiles_n * splits, NT, lds, s>>>(g, tiles_m, tiles_n);
+  k_gemm_big<MODE, BN, F, RG><<<tiles_m * tiles_n * splits * p.n, NT, lds, s>>>(p, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
 template <int MODE, int BN>
-hipError_t launch_big(const GemmArgs& g, hipStream_t s) {
+hipError_t launch_big(const GemmPair& p, hipStream_t s) {
+  const GemmArgs& g = p.g[0];
   const bool rg = g.N % BN != 0;
 #define SPZ_CASE(F) \
-  case (F): return rg ? launch_big_f<MODE, BN, (F), true>(g, s) : launch_big_f<MODE, BN, (F), false>(g, s)
+  case (F): return rg ? launch_big_f<MODE, BN, (F), true>(p, s) : launch_big_f<MODE, BN, (F), false>(p, s)
 #define SPZ_CASE_WHOLE(F) \
-  case (F): return rg ? hipErrorInvalidValue : launch_big_f<MODE, BN, (F), false>(g, s)
+  case (F): return rg ? hipErrorInvalidValue : launch_big_f<MODE, BN, (F), false>(p, s)
   if constexpr (MODE == GEMM_WGRAD) {
-    return rg ? launch_big_f<MODE, BN, EPI_F32, true>(g, s) : launch_big_f<MODE, BN, EPI_F32, false>(g, s);
+    return rg ? launch_big_f<MODE, BN, EPI_F32, true>(p, s) : launch_big_f<MODE, BN, EPI_F32, false>(p, s);
   } else if constexpr (MODE == GEMM_FWD) {
     switch (epilogue_flags((GemmMode)MODE, g)) {
       SPZ_CASE(EPI_F32);
@@ -949,27 +958,65 @@ bool big_gemm_ld_ok(GemmMode mode, const GemmArgs& g) {
   return g.lda < LIM && (mode == GEMM_FWD ? g.ldb : g.ldbt) < LIM && g.ldc < LIM && (!g.mask || g.ldm < LIM);
 }
 
-hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s) {
+namespace {
+
+// Checks one product against the large-tile kernel's launch contract; its launch form
+// (the input gradient reads the transposed weight image as B) goes to *t.
+hipError_t big_prepare(GemmMode mode, const GemmArgs& g, GemmArgs* t) {
   if (!big_gemm_ld_ok(mode, g)) return hipErrorInvalidValue;
   // The forward reads its bias four columns at a time.
   if (mode == GEMM_FWD && g.bias && ((uintptr_t)g.bias & 15)) return hipErrorInvalidValue;
   const int f = epilogue_flags(mode, g);
   const bool fused = f & (EPI_BITS | EPI_BITS_OUT | EPI_RDOT | EPI_CSUM | EPI_NOSTORE);
   if (fused && g.N % 128) return hipErrorInvalidValue;
+  *t = g;
+  if (mode == GEMM_DGRAD) {
+    // The input-gradient product reads the weight as Bt [N, K] (k-contiguous).
+    if (!g.Bt || g.ldbt % 8 || g.ldbt < g.K) return hipErrorInvalidValue;
+    t->B = g.Bt;
+    t->ldb = g.ldbt;
+  }
+  return hipSuccess;
+}
+
+hipError_t big_launch(GemmMode mode, const GemmPair& p, hipStream_t s) {
+  const GemmArgs& g = p.g[0];
+  const int f = epilogue_flags(mode, g);
+  const bool fused = f & (EPI_BITS | EPI_BITS_OUT | EPI_RDOT | EPI_CSUM | EPI_NOSTORE);
   const bool bn256 = big_bn(mode, g.M, g.N, fused) == 256;
   switch (mode) {
-    case GEMM_FWD: return bn256 ? launch_big<GEMM_FWD, 256>(g, s) : launch_big<GEMM_FWD, 128>(g, s);
-    case GEMM_DGRAD: {
-      // The input-gradient product reads the weight as Bt [N, K] (k-contiguous).
-      if (!g.Bt || g.ldbt % 8 || g.ldbt < g.K) return hipErrorInvalidValue;
-      GemmArgs t = g;
-      t.B = g.Bt;
-      t.ldb = g.ldbt;
-      return bn256 ? launch_big<GEMM_DGRAD, 256>(t, s) : launch_big<GEMM_DGRAD, 128>(t, s);
-    }
-    case GEMM_WGRAD: return bn256 ? launch_big<GEMM_WGRAD, 256>(g, s) : launch_big<GEMM_WGRAD, 128>(g, s);
+    case GEMM_FWD: return bn256 ? launch_big<GEMM_FWD, 256>(p, s) : launch_big<GEMM_FWD, 128>(p, s);
+    case GEMM_DGRAD: return bn256 ? launch_big<GEMM_DGRAD, 256>(p, s) : launch_big<GEMM_DGRAD, 128>(p, s);
+    case GEMM_WGRAD: return bn256 ? launch_big<GEMM_WGRAD, 256>(p, s) : launch_big<GEMM_WGRAD, 128>(p, s);
   }
   return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s) {
+  GemmPair p{};
+  p.n = 1;
+  const hipError_t e = big_prepare(mode, g, &p.g[0]);
+  return e != hipSuccess ? e : big_launch(mode, p, s);
+}
+
+int big_gemm_tiles(GemmMode mode, const GemmArgs& g) {
+  const int f = epilogue_flags(mode, g);
+  const bool fused = f & (EPI_BITS | EPI_BITS_OUT | EPI_RDOT | EPI_CSUM | EPI_NOSTORE);
+  const int bn = big_bn(mode, g.M, g.N, fused);
+  return (g.M / BM) * ((g.N + bn - 1) / bn) * (mode == GEMM_WGRAD ? g.splits : 1);
+}
+
+hipError_t gemm_big_pair(GemmMode mode, const GemmArgs& g0, const GemmArgs& g1, hipStream_t s) {
+  if (g0.M != g1.M || g0.N != g1.N || g0.K != g1.K || epilogue_flags(mode, g0) != epilogue_flags(mode, g1) ||
+      (mode == GEMM_WGRAD && g0.splits != g1.splits) || (!g0.m_dyn) != (!g1.m_dyn))
+    return hipErrorInvalidValue;
+  GemmPair p{};
+  p.n = 2;
+  hipError_t e = big_prepare(mode, g0, &p.g[0]);
+  if (e == hipSuccess) e = big_prepare(mode, g1, &p.g[1]);
+  return e != hipSuccess ? e : big_launch(mode, p, s);
 }
 
 }  // namespace spz

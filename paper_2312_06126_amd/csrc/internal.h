@@ -145,6 +145,12 @@ __host__ __device__ inline int epilogue_flags(GemmMode mode, const GemmArgs& g) 
 // C = A B with A: [M, K] k-contiguous (FWD, DGRAD) or [K, M] (WGRAD),
 // B: [N, K] (FWD) or [K, N] (DGRAD, WGRAD). Returns a hipError_t.
 hipError_t gemm(bool bf16, GemmMode mode, const GemmArgs& g, hipStream_t s);
+// Two independent products of one mode: a single large-tile launch when gemm_pairs
+// holds, else gemm() twice.
+hipError_t gemm_pair(bool bf16, GemmMode mode, const GemmArgs& g0, const GemmArgs& g1, hipStream_t s);
+// Both products run on the large-tile kernel with the same launch shape and one of them
+// alone would leave compute units idle (fewer workgroups than 256).
+bool gemm_pairs(bool bf16, GemmMode mode, const GemmArgs& g0, const GemmArgs& g1);
 // Threads per output piece of the split-K reduction of an M x N product from `splits`
 // slices (the grouping ReduceJob::groups reproduces).
 int splitk_groups(int M, int N, int splits);
@@ -167,6 +173,13 @@ bool big_gemm_colsum(GemmMode mode, int M, int N, int K);
 // below 2^22 elements).
 bool big_gemm_ld_ok(GemmMode mode, const GemmArgs& g);
 hipError_t gemm_big(GemmMode mode, const GemmArgs& g, hipStream_t s);
+// Two products of the same mode, shape, epilogue and split count in one launch of the
+// large-tile kernel (the second's tiles after the first's); each must satisfy the
+// single-product contract. GemmPair is the kernel's argument.
+struct GemmPair { GemmArgs g[2]; int n; };
+hipError_t gemm_big_pair(GemmMode mode, const GemmArgs& g0, const GemmArgs& g1, hipStream_t s);
+// Workgroups of one large-tile launch of this product.
+int big_gemm_tiles(GemmMode mode, const GemmArgs& g);
 // True when a product of this shape runs entirely on the large-tile kernel, so that
 // bits_out / bits / rdot_w / no_store / colsum may be used.
 bool gemm_fused_ok(bool bf16, GemmMode mode, int M, int N, int K);
