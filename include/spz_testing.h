@@ -62,6 +62,18 @@ int spzt_gemm_dgrad_rows(int32_t bf16, int32_t M, int32_t N, int32_t K, const vo
 /* Columns per row-dot partial of an M x N forward product (its column tile over 2). */
 int spzt_rdot_cols(int32_t M, int32_t N);
 /*
+ * The deferred reduction kernel on n <= 24 jobs in one launch (host arrays of the
+ * per-job fields; part[i], out[i] device pointers): out[r * ldo + c] = sum over slices
+ * z < slices of part[z * zstride + r * ld + c] for r < rows, c < cols, summed in a
+ * fixed order: thread g of `groups` (a power of two up to 256) adds slices g,
+ * g + groups, ... in turn, then the group sums are added in g order; vec (4 or 1)
+ * columns per piece (4: cols, ld, ldo, zstride multiples of 4, 16-byte aligned
+ * pointers). SPZ_EINVAL on a bad job. Synchronous.
+ */
+int spzt_reduce_jobs(int32_t n, const float* const* part, float* const* out, const int64_t* zstride,
+                     const int64_t* ld, const int64_t* ldo, const int32_t* rows, const int32_t* cols,
+                     const int32_t* slices, const int32_t* groups, const int32_t* vec);
+/*
  * Checks the device float32 -> bfloat16 rounding used by every kernel against an
  * integer round-to-nearest-even over the float bit patterns [begin, begin + count)
  * (begin + count <= 2^32); a NaN input must give a NaN. *mismatches receives the

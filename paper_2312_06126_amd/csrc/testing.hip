@@ -121,6 +121,24 @@ extern "C" int spzt_gemm_dgrad_rows(int32_t bf16, int32_t M, int32_t N, int32_t 
 
 extern "C" int spzt_rdot_cols(int32_t M, int32_t N) { return gemm_rdot_cols(M, N); }
 
+extern "C" int spzt_reduce_jobs(int32_t n, const float* const* part, float* const* out, const int64_t* zstride,
+                                const int64_t* ld, const int64_t* ldo, const int32_t* rows, const int32_t* cols,
+                                const int32_t* slices, const int32_t* groups, const int32_t* vec) {
+  if (n < 1 || n > MAX_REDUCE_JOBS || !part || !out || !zstride || !ld || !ldo || !rows || !cols || !slices ||
+      !groups || !vec)
+    return SPZ_EINVAL;
+  ReduceJobs J{};
+  J.n = n;
+  for (int i = 0; i < n; ++i) {
+    if (!part[i] || !out[i]) return SPZ_EINVAL;
+    J.j[i] = ReduceJob{part[i], out[i], zstride[i], ld[i], ldo[i], rows[i], cols[i], slices[i], groups[i], vec[i], 0};
+  }
+  hipError_t e = launch_reduce_jobs(J, nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e == hipErrorInvalidValue) return SPZ_EINVAL;
+  return e == hipSuccess ? SPZ_OK : SPZ_EHIP;
+}
+
 // Rounding check of the device float32 -> bfloat16 conversion against an integer
 // round-to-nearest-even written out here: every input bit pattern in
 // [begin, begin + count) must give the same 16 bits, except that a NaN input only
