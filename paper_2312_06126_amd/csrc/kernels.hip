@@ -702,7 +702,7 @@ __global__ void __launch_bounds__(256) k_reduce_jobs(ReduceJobs J) {
     col = (int)(piece - r * cv) * jb.vec;
     const float* src = jb.part + r * jb.ld + col;
     if (jb.vec == 4) {
-#pragma unroll 4
+#pragma unroll 16
       for (int z = grp; z < jb.slices; z += G) {
         const float4 v = *reinterpret_cast<const float4*>(src + (int64_t)z * jb.zstride);
         acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
