@@ -535,8 +535,22 @@ hipError_t wgrad(spz_ctx* c, int q, int ni, int nn, int l, const void* const* dz
     gk.B = X[k]; gk.ldb = ldx;
     gk.M = L.out_p; gk.N = L.in_p; gk.K = c->Bp;
     gk.splits = wgrad_splits(c->bf16, gk.M, gk.N, gk.K);
-    if (!(part[k] = red_alloc(c, q, (int64_t)gk.splits * gk.M * gk.N))) return hipErrorOutOfMemory;
-    gk.C = part[k]; gk.ldc = L.in_p;
+    gk.ldc = L.in_p;
+  }
+  // Twins: half the K-split each, so that the two products fill the GPU together in one
+  // launch with half the partial slices to write and reduce (where the pair qualifies).
+  if (nn == 2 && g[0].splits > 1) {
+    GemmArgs h0 = g[0], h1 = g[1];
+    h0.splits /= 2;
+    h1.splits /= 2;
+    if (gemm_pairs(c->bf16, GEMM_WGRAD, h0, h1)) {
+      g[0].splits = h0.splits;
+      g[1].splits = h1.splits;
+    }
+  }
+  for (int k = 0; k < nn; ++k) {
+    if (!(part[k] = red_alloc(c, q, (int64_t)g[k].splits * g[k].M * g[k].N))) return hipErrorOutOfMemory;
+    g[k].C = part[k];
   }
   HK(gemm2(c, "gemm_wgrad", GEMM_WGRAD, g[0], nn > 1 ? &g[1] : nullptr, true, s));
   for (int k = 0; k < nn; ++k)
