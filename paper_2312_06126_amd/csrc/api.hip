@@ -519,26 +519,34 @@ hipError_t forward(spz_ctx* c, int ni, int nn, bool target, const void* X, int64
   return hipSuccess;
 }
 
-// Weight gradients of layer l of nets ni .. ni + nn - 1 from dz[k] [Bp, out_p] and the
-// layer inputs X[k] [Bp, ldx] (split-K over the batch, slices reduced in order by the
-// part's deferred reduction q) and, when `bias`, the bias gradients as the column sums
-// of dz[k].
-hipError_t wgrad(spz_ctx* c, int q, int ni, int nn, int l, const void* const* dz, const void* const* X, int64_t ldx,
-                 bool bias, hipStream_t s) {
+// One weight-gradient product: layer l of net ni from dz [Bp, out_p] and the layer
+// input X [Bp, ldx].
+struct WgradIn {
+  int ni, l;
+  const void* dz;
+  const void* X;
+  int64_t ldx;
+};
+
+// Weight gradients of nn (1 or 2) layers, split-K over the batch (slices reduced in order
+// by the part's deferred reduction q) and, when `bias`, the bias gradients as the column
+// sums of dz. Two products of one shape (a layer of both twin critics, or two equal layers
+// of one net) split K half as finely and share one launch where the large-tile kernel
+// takes them: half the slices to write and reduce (which also pays where the pair leaves
+// compute units idle: there the reduction outweighs the product).
+hipError_t wgrad(spz_ctx* c, int q, int nn, const WgradIn* w, bool bias, hipStream_t s) {
   HK(red_room(c, q, 2 * nn, s));
-  const Lay& L = c->net[ni].L[l];
   GemmArgs g[2]{};
   float* part[2] = {nullptr, nullptr};
   for (int k = 0; k < nn; ++k) {
+    const Lay& L = c->net[w[k].ni].L[w[k].l];
     GemmArgs& gk = g[k];
-    gk.A = dz[k]; gk.lda = L.out_p;
-    gk.B = X[k]; gk.ldb = ldx;
+    gk.A = w[k].dz; gk.lda = L.out_p;
+    gk.B = w[k].X; gk.ldb = w[k].ldx;
     gk.M = L.out_p; gk.N = L.in_p; gk.K = c->Bp;
     gk.splits = wgrad_splits(c->bf16, gk.M, gk.N, gk.K);
     gk.ldc = L.in_p;
   }
-  // Twins: half the K-split each, so that the two products fill the GPU together in one
-  // launch with half the partial slices to write and reduce (where the pair qualifies).
   if (nn == 2 && g[0].splits > 1) {
     GemmArgs h0 = g[0], h1 = g[1];
     h0.splits /= 2;
@@ -554,17 +562,19 @@ hipError_t wgrad(spz_ctx* c, int q, int ni, int nn, int l, const void* const* dz
   }
   HK(gemm2(c, "gemm_wgrad", GEMM_WGRAD, g[0], nn > 1 ? &g[1] : nullptr, true, s));
   for (int k = 0; k < nn; ++k)
-    HK(red_job(c, q, ReduceJob{part[k], c->G + c->net[ni + k].L[l].w, (int64_t)g[k].M * g[k].ldc, g[k].ldc, L.in_p,
-                               g[k].M, g[k].N, g[k].splits, splitk_groups(g[k].M, g[k].N, g[k].splits), 4, 0}, s));
+    HK(red_job(c, q, ReduceJob{part[k], c->G + c->net[w[k].ni].L[w[k].l].w, (int64_t)g[k].M * g[k].ldc, g[k].ldc,
+                               g[k].N, g[k].M, g[k].N, g[k].splits, splitk_groups(g[k].M, g[k].N, g[k].splits), 4, 0},
+                       s));
   if (!bias) return hipSuccess;
   const int chunks = colsum_chunks(c->Bp);
   for (int k = 0; k < nn; ++k) {
-    float* cpart = red_alloc(c, q, (int64_t)chunks * L.out_p);
+    const int N = g[k].M;   // the layer's outputs
+    float* cpart = red_alloc(c, q, (int64_t)chunks * N);
     if (!cpart) return hipErrorOutOfMemory;
-    ColsumArgs cs{dz[k], L.out_p, L.out_p, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
-    HK(timed(c, "colsum", c->Bp, L.out_p, 0, 0.0, (double)c->Bp * L.out_p * es(c), s,
+    ColsumArgs cs{w[k].dz, N, N, c->Bp, COLSUM_CHUNK, nullptr, 0, cpart, nullptr};
+    HK(timed(c, "colsum", c->Bp, N, 0, 0.0, (double)c->Bp * N * es(c), s,
              [&] { return launch_colsum_partial(c->bf16, cs, s); }));
-    HK(red_colsum(c, q, cpart, chunks, L.out_p, c->G + c->net[ni + k].L[l].b, nullptr, nullptr, s));
+    HK(red_colsum(c, q, cpart, chunks, N, c->G + c->net[w[k].ni].L[w[k].l].b, nullptr, nullptr, s));
   }
   return hipSuccess;
 }
@@ -689,7 +699,8 @@ hipError_t critic_backward(spz_ctx* c, const float* const* dq, const void* X, vo
     const Lay& L = c->net[1].L[l];
     const void* dz[2] = {dzb[0][cur], dzb[1][cur]};
     const void* Xl[2] = {l == 0 ? X : hid[0][l - 1], l == 0 ? X : hid[1][l - 1]};
-    HK(wgrad(c, 0, 1, 2, l, dz, Xl, l == 0 ? c->Kc : L.in_p, l == nl - 2 && !hb_sums, s));
+    const WgradIn w[2] = {{1, l, dz[0], Xl[0], l == 0 ? c->Kc : L.in_p}, {2, l, dz[1], Xl[1], l == 0 ? c->Kc : L.in_p}};
+    HK(wgrad(c, 0, 2, w, l == nl - 2 && !hb_sums, s));
     if (l > 0) {
       DgradIn d[2];
       for (int k = 0; k < 2; ++k)
@@ -766,10 +777,24 @@ hipError_t actor_backward(spz_ctx* c, hipStream_t s) {
   const int nl = (int)n.L.size();
   const void* cur = c->dzh;
   int nxt = 0;
+  // A hidden layer's weight gradient waits for the layer below when the two have one
+  // shape, so that both can share a launch; its dz stays intact until then (the input
+  // gradients alternate between two buffers).
+  WgradIn held{};
+  bool holding = false;
   for (int l = nl - 1; l >= 0; --l) {
     const Lay& L = n.L[l];
-    const void* Xl = l == 0 ? c->xsa : c->ha[l - 1];
-    HK(wgrad(c, 1, 0, 1, l, &cur, &Xl, l == 0 ? c->Kc : L.in_p, l == nl - 1, s));
+    const WgradIn w{0, l, cur, l == 0 ? c->xsa : c->ha[l - 1], l == 0 ? c->Kc : L.in_p};
+    if (holding) {
+      const WgradIn two[2] = {held, w};
+      HK(wgrad(c, 1, 2, two, false, s));
+      holding = false;
+    } else if (l > 0 && l < nl - 1 && n.L[l - 1].out_p == L.out_p && n.L[l - 1].in_p == L.in_p) {
+      held = w;
+      holding = true;
+    } else {
+      HK(wgrad(c, 1, 1, &w, l == nl - 1, s));
+    }
     if (l > 0) {
       const DgradIn d{cur, c->ha[l - 1], c->bha[l - 1], c->a_dz[nxt], c->G + n.L[l - 1].b, nullptr};
       HK(dgrad(c, 0, 1, l, &d, 0, L.in_p, true, L.in_p, L.in_p, false, 1, s));
