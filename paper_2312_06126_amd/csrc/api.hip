@@ -450,7 +450,14 @@ struct NetOut {
   float* rdot;
   float* head;
   QSrc* qs;
+  const SacHeadArgs* sac = nullptr;   // actor: the SAC head fused into the output product (head unused)
 };
+
+// Whether the actor's output product takes the SAC head in its epilogue.
+bool sac_head_fused(const spz_ctx* c) {
+  const Lay& H = c->net[0].L.back();
+  return !c->td3 && gemm_sac_head_ok(c->Bp, H.out_p, H.in_p, c->A);
+}
 
 bool fused_layer(const spz_ctx* c, const Lay& L) { return gemm_fused_ok(c->bf16, GEMM_FWD, c->Bp, L.out_p, L.in_p); }
 
@@ -465,7 +472,7 @@ hipError_t forward(spz_ctx* c, int ni, int nn, bool target, const void* X, int64
                    bool keep_last, hipStream_t s) {
   if (nn < 1 || nn > 2 || (ni == 0 && nn != 1) || ni + nn > 3) return hipErrorInvalidValue;
   for (int k = 0; k < nn; ++k)
-    if (ni != 0 && !o[k].qs) return hipErrorInvalidValue;
+    if ((ni != 0 && !o[k].qs) || (o[k].sac && ni != 0)) return hipErrorInvalidValue;
   const int nl = (int)c->net[ni].L.size();
   const void* in[2] = {X, X};
   int64_t ld = ldx;
@@ -505,6 +512,11 @@ hipError_t forward(spz_ctx* c, int ni, int nn, bool target, const void* X, int64
         gk.ldrd = c->Bp;
         gk.no_store = keep_last ? 0 : 1;
       }
+    }
+    if (l == nl - 1 && o[0].sac) {   // the actor's output layer with the SAC head
+      HK(timed(c, "gemm_fwd", g[0].M, g[0].N, g[0].K, 2.0 * g[0].M * g[0].N * g[0].K, 0.0, s,
+               [&] { return gemm_fwd_sac_head(c->bf16, g[0], *o[0].sac, s); }));
+      return hipSuccess;
     }
     HK(gemm2(c, "gemm_fwd", GEMM_FWD, g[0], nn > 1 ? &g[1] : nullptr, true, s));
     if (folded) {
@@ -812,12 +824,14 @@ const float* log_alpha_ptr(const spz_ctx* c) { return c->P + c->la; }
 hipError_t critic_part(spz_ctx* c, hipStream_t s) {
   const int pa = c->net[0].L.back().out_p;
   const spz_hparams& hp = c->hp;
-  const NetOut act{c->cs_hid.data(), nullptr, nullptr, c->z2, nullptr};
+  NetOut act{c->cs_hid.data(), nullptr, nullptr, c->z2, nullptr};
   if (!c->td3) {
+    const SacHeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_TGT, hp.log_std_min, hp.log_std_max,
+                        c->xs2, c->Kc, c->Ka, c->logp2, nullptr, nullptr, nullptr};
+    if (sac_head_fused(c)) act.sac = &h;
     HK(forward(c, 0, 1, false, c->xs2, c->Kc, &act, true, s));
-    SacHeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_TGT, hp.log_std_min, hp.log_std_max,
-                  c->xs2, c->Kc, c->Ka, c->logp2, nullptr, nullptr, nullptr};
-    HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, h, s); }));
+    if (!act.sac)
+      HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, h, s); }));
   } else {
     HK(forward(c, 0, 1, true, c->xs2, c->Kc, &act, true, s));
     Td3HeadArgs h{c->z2, pa, c->A, c->B, c->seed, c->d_step, 1, hp.policy_noise, hp.noise_clip,
@@ -851,12 +865,14 @@ hipError_t critic_part(spz_ctx* c, hipStream_t s) {
 hipError_t actor_part(spz_ctx* c, hipStream_t s) {
   const int pa = c->net[0].L.back().out_p;
   const spz_hparams& hp = c->hp;
-  const NetOut act{c->ha.data(), c->bha.data(), nullptr, c->z, nullptr};
+  NetOut act{c->ha.data(), c->bha.data(), nullptr, c->z, nullptr};
+  const SacHeadArgs sh{c->z, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_POL, hp.log_std_min, hp.log_std_max,
+                       c->xs_act, c->Kc, c->Ka, c->logp, c->th, c->se, c->lm};
+  if (sac_head_fused(c)) act.sac = &sh;
   HK(forward(c, 0, 1, false, c->xsa, c->Kc, &act, true, s));
   if (!c->td3) {
-    SacHeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, P_NOISE_POL, hp.log_std_min, hp.log_std_max,
-                  c->xs_act, c->Kc, c->Ka, c->logp, c->th, c->se, c->lm};
-    HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, h, s); }));
+    if (!act.sac)
+      HK(timed(c, "sac_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_sac_head(c->bf16, sh, s); }));
   } else {
     Td3HeadArgs h{c->z, pa, c->A, c->B, c->seed, c->d_step, 0, 0.0f, 0.0f, c->xs_act, c->Kc, c->Ka, c->th};
     HK(timed(c, "td3_head", c->B, c->A, 0, 0.0, 0.0, s, [&] { return launch_td3_head(c->bf16, h, s); }));

@@ -120,8 +120,10 @@ template <int BM, int BN> struct Shape {
 // multiples of 32); operand reads there are clamped and the epilogue stores nothing there.
 // BT (input gradient): B is the transposed weight image [N, K], read k-contiguous like
 // the forward's weight (16-byte fragment reads instead of element-wise ones).
-template <typename T, int MODE, int BM, int BN, bool RG, bool BT>
-__global__ void __launch_bounds__(gemm_threads(BM, BN)) k_gemm(GemmArgs g) {
+// HEAD (forward, the actor's output layer): the SAC head runs in the epilogue on whole
+// rows of z (the tile spans all N columns) instead of z being stored; h describes it.
+template <typename T, int MODE, int BM, int BN, bool RG, bool BT, bool HEAD = false>
+__global__ void __launch_bounds__(gemm_threads(BM, BN)) k_gemm(GemmArgs g, SacHeadArgs h) {
   using S = Shape<BM, BN>;
   constexpr int TM = S::TM, TN = S::TN, NT = S::NT;
   constexpr bool AKC = MODE != GEMM_WGRAD;
@@ -204,6 +206,45 @@ __global__ void __launch_bounds__(gemm_threads(BM, BN)) k_gemm(GemmArgs g) {
 
   // Epilogue. 32x32 accumulator layout: lane holds column lane%32; register q holds
   // row 8*(q/4) + 4*(lane/32) + q%4.
+  if constexpr (HEAD) {
+    // z = acc + b for the tile's rows goes to LDS (the value a stored z would hold), then
+    // one thread per (row, action) element runs the head and each row's log-density
+    // terms are added in action order, as the head kernel does.
+    static_assert(MODE == GEMM_FWD && !RG && !BT, "the head follows the forward product");
+    constexpr int ZP = BN + 1;
+    __shared__ float zt[HEAD ? BM * ZP : 1];
+    __shared__ float lt[HEAD ? BM * (BN / 2) : 1];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int cl = (wn * TN + j) * 32 + (lane & 31);
+        const int rl = (wm * TM + i) * 32 + 4 * (lane >> 5);
+        const float bias = g.bias ? g.bias[cl] : 0.0f;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          float v = acc[i][j][q];
+          v += bias;
+          zt[(rl + 8 * (q >> 2) + (q & 3)) * ZP + cl] = v;
+        }
+      }
+    __syncthreads();
+    const int rows = min(BM, h.B - m0);
+    const uint32_t t = (uint32_t)(*h.step + 1);
+    for (int e = tid; e < rows * h.A; e += NT) {
+      const int r = e / h.A, j = e - r * h.A;
+      const int b = m0 + r;
+      lt[e] = sac_head_element<T>(h, zt[r * ZP + j], zt[r * ZP + h.A + j], b, j,
+                                  normal_at(h.seed, (uint64_t)b * h.A + j, t, h.purpose));
+    }
+    __syncthreads();
+    if (tid < rows) {
+      float lp = 0.0f;
+      for (int j = 0; j < h.A; ++j) lp += lt[tid * h.A + j];
+      h.logp[m0 + tid] = lp;
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -300,8 +341,8 @@ int fit_tile(int n) {
 template <typename T, int MODE, int BM, int BN, bool BT>
 hipError_t launch_rg(const GemmArgs& g, hipStream_t s) {
   dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, MODE == GEMM_WGRAD ? g.splits : 1);
-  if (g.N % BN || g.M % BM) k_gemm<T, MODE, BM, BN, true, BT><<<grid, Shape<BM, BN>::NT, 0, s>>>(g);
-  else k_gemm<T, MODE, BM, BN, false, BT><<<grid, Shape<BM, BN>::NT, 0, s>>>(g);
+  if (g.N % BN || g.M % BM) k_gemm<T, MODE, BM, BN, true, BT><<<grid, Shape<BM, BN>::NT, 0, s>>>(g, SacHeadArgs{});
+  else k_gemm<T, MODE, BM, BN, false, BT><<<grid, Shape<BM, BN>::NT, 0, s>>>(g, SacHeadArgs{});
   return hipGetLastError();
 }
 
@@ -366,6 +407,37 @@ hipError_t launch_mode(const GemmArgs& g, hipStream_t s) {
 }
 
 }  // namespace
+
+bool gemm_sac_head_ok(int M, int N, int K, int A) {
+  return (N == 32 || N == 64) && A >= 1 && 2 * A <= N && M > 0 && M % 128 == 0 && K > 0 && K % BK == 0;
+}
+
+namespace {
+template <typename T, int BM, int BN>
+hipError_t launch_head(const GemmArgs& g, const SacHeadArgs& h, hipStream_t s) {
+  k_gemm<T, GEMM_FWD, BM, BN, false, false, true><<<dim3(1, g.M / BM), Shape<BM, BN>::NT, 0, s>>>(g, h);
+  return hipGetLastError();
+}
+template <typename T, int BN>
+hipError_t launch_head_bm(const GemmArgs& g, const SacHeadArgs& h, int bm, hipStream_t s) {
+  return bm == 64 ? launch_head<T, 64, BN>(g, h, s) : launch_head<T, 32, BN>(g, h, s);
+}
+template <typename T>
+hipError_t launch_head_t(const GemmArgs& g, const SacHeadArgs& h, int bm, hipStream_t s) {
+  return g.N == 64 ? launch_head_bm<T, 64>(g, h, bm, s) : launch_head_bm<T, 32>(g, h, bm, s);
+}
+}  // namespace
+
+hipError_t gemm_fwd_sac_head(bool bf16, const GemmArgs& g, const SacHeadArgs& h, hipStream_t s) {
+  if (!gemm_sac_head_ok(g.M, g.N, g.K, h.A) || h.B < 0 || h.B > g.M || !h.step || !h.x || !h.logp)
+    return hipErrorInvalidValue;
+  const int vec = bf16 ? 8 : 4;
+  if (g.lda % vec || g.ldb % vec || g.lda < g.K || g.ldb < g.K) return hipErrorInvalidValue;
+  // Row tiles of 64 (the z tile and the log-density terms stay within static LDS), or 32
+  // while the grid is short of two workgroups per CU.
+  const int bm = g.M / 64 >= GEN_TARGET_WGS ? 64 : 32;
+  return bf16 ? launch_head_t<bf16_t>(g, h, bm, s) : launch_head_t<float>(g, h, bm, s);
+}
 
 int wgrad_splits(bool bf16, int M, int N, int K) {
   int tiles, target;

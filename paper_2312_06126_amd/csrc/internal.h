@@ -85,6 +85,63 @@ __host__ __device__ inline uint32_t philox_word(uint64_t seed, uint64_t i, uint3
 
 enum Purpose : uint32_t { P_INIT = 0, P_IDX = 1, P_NOISE_TGT = 2, P_NOISE_POL = 3, P_ACT = 4 };
 
+// ----------------------------------------------------------------------------- device math
+constexpr float LN2F = 0.69314718055994531f;
+constexpr float HALF_LN_2PI_F = 0.91893853320467274f;
+
+__device__ inline float softplusf(float x) { return x > 0.0f ? x + log1pf(expf(-x)) : log1pf(expf(x)); }
+
+// Clamp that keeps a NaN operand (fminf / fmaxf would drop it), so that a non-finite
+// network output reaches the loss record as it does in exact arithmetic.
+__device__ inline float clamp_keep_nan(float x, float lo, float hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+// Standard normal deviate for flat element i of the stream (seed, step, purpose):
+// Box-Muller on words (0,1) -> lanes 0,1 and (2,3) -> lanes 2,3 of each Philox block.
+__device__ inline float normal_at(uint64_t seed, uint64_t i, uint32_t step, uint32_t purpose) {
+  const U4 w = philox(U4{(uint32_t)(i >> 2), step, purpose, 0u}, (uint32_t)seed, (uint32_t)(seed >> 32));
+  const int lane = (int)(i & 3);
+  const uint32_t wa = lane < 2 ? w.x : w.z, wb = lane < 2 ? w.y : w.w;
+  const float u1 = (float)((wa >> 8) + 1u) * 5.9604644775390625e-8f;  // (0, 1]
+  const float u2 = (float)(wb >> 8) * 5.9604644775390625e-8f;          // [0, 1)
+  const float rad = sqrtf(-2.0f * logf(u1));
+  float sn, cs;
+  sincospif(2.0f * u2, &sn, &cs);
+  return rad * ((lane & 1) ? sn : cs);
+}
+
+// ----------------------------------------------------------------------------- SAC head
+// z = [mu | l] per row -> a = tanh(mu + exp(clip(l)) eps), written into the action
+// columns of the next operand tensor x, and the tanh-Gaussian log-density of a.
+struct SacHeadArgs {
+  const float* z; int ldz; int A, B;
+  uint64_t seed; const int64_t* step; uint32_t purpose;
+  float lmin, lmax;
+  void* x; int64_t ldx; int xoff;      // action columns of the next operand tensor
+  float* logp;
+  float *th, *se, *lm;                 // backward cache [B, A] (null for the target side)
+};
+
+// Element (row b, action j) of the SAC head from its mean mu, log-std l and deviate eps
+// (normal_at of element b A + j at the step's counter word): stores the action (and the backward cache) and returns
+// the element's log-density term, in the overflow-free form of log(1 - tanh^2 u) =
+// 2 (ln 2 - u - softplus(-2u)). Shared by the head kernel and the head product's fused
+// epilogue, so both compute the same bits.
+template <typename T>
+__device__ inline float sac_head_element(const SacHeadArgs& h, float mu, float l, int b, int j, float eps) {
+  const uint64_t e = (uint64_t)b * h.A + j;
+  const float lc = clamp_keep_nan(l, h.lmin, h.lmax);
+  const float sig = expf(lc);
+  const float u = mu + sig * eps;
+  const float a = tanhf(u);
+  static_cast<T*>(h.x)[(int64_t)b * h.ldx + h.xoff + j] = from_f<T>(a);
+  if (h.th) {
+    h.th[e] = a;
+    h.se[e] = sig * eps;
+    h.lm[e] = (l >= h.lmin && l <= h.lmax) ? 1.0f : 0.0f;
+  }
+  return -0.5f * eps * eps - lc - HALF_LN_2PI_F - 2.0f * (LN2F - u - softplusf(-2.0f * u));
+}
+
 // ----------------------------------------------------------------------------- GEMM
 enum GemmMode { GEMM_FWD = 0, GEMM_DGRAD = 1, GEMM_WGRAD = 2 };
 
@@ -188,5 +245,10 @@ bool gemm_fused_ok(bool bf16, GemmMode mode, int M, int N, int K);
 int gemm_rdot_cols(int M, int N);
 // True when the large-tile kernel has an epilogue for these flags.
 bool big_epilogue_supported(GemmMode mode, int flags);
+// The actor's output product z = X W^T + b with the SAC head fused into its epilogue
+// (z itself is not stored; h.z is ignored): every row's outputs must fall in one tile,
+// 2 A <= N with N one of 32, 64; M % 128 == 0 and K % 32 == 0 as for gemm().
+bool gemm_sac_head_ok(int M, int N, int K, int A);
+hipError_t gemm_fwd_sac_head(bool bf16, const GemmArgs& g, const SacHeadArgs& h, hipStream_t s);
 
 }  // namespace spz

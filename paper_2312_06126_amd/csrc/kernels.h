@@ -25,15 +25,6 @@ struct PackArgs {
   const float *obs, *act, *rew, *done, *nobs;   // device staging
 };
 
-struct SacHeadArgs {
-  const float* z; int ldz; int A, B;
-  uint64_t seed; const int64_t* step; uint32_t purpose;
-  float lmin, lmax;
-  void* x; int64_t ldx; int xoff;      // action columns of the next operand tensor
-  float* logp;
-  float *th, *se, *lm;                 // backward cache [B, A] (null for the target side)
-};
-
 struct Td3HeadArgs {
   const float* z; int ldz; int A, B;
   uint64_t seed; const int64_t* step;

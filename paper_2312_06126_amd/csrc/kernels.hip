@@ -11,29 +11,8 @@
 namespace spz {
 namespace {
 
-constexpr float LN2F = 0.69314718055994531f;
-constexpr float HALF_LN_2PI_F = 0.91893853320467274f;
-
-__device__ inline float softplusf(float x) { return x > 0.0f ? x + log1pf(expf(-x)) : log1pf(expf(x)); }
-
-// Clamp and minimum that keep a NaN operand (fminf / fmaxf would drop it), so that a
-// non-finite network output reaches the loss record as it does in exact arithmetic.
-__device__ inline float clamp_keep_nan(float x, float lo, float hi) { return x < lo ? lo : (x > hi ? hi : x); }
+// Minimum that keeps a NaN operand (fminf would drop it), like clamp_keep_nan.
 __device__ inline float min_keep_nan(float a, float b) { return (a < b || a != a) ? a : b; }
-
-// Standard normal deviate for flat element i of the stream (seed, step, purpose):
-// Box-Muller on words (0,1) -> lanes 0,1 and (2,3) -> lanes 2,3 of each Philox block.
-__device__ inline float normal_at(uint64_t seed, uint64_t i, uint32_t step, uint32_t purpose) {
-  const U4 w = philox(U4{(uint32_t)(i >> 2), step, purpose, 0u}, (uint32_t)seed, (uint32_t)(seed >> 32));
-  const int lane = (int)(i & 3);
-  const uint32_t wa = lane < 2 ? w.x : w.z, wb = lane < 2 ? w.y : w.w;
-  const float u1 = (float)((wa >> 8) + 1u) * 5.9604644775390625e-8f;  // (0, 1]
-  const float u2 = (float)(wb >> 8) * 5.9604644775390625e-8f;          // [0, 1)
-  const float rad = sqrtf(-2.0f * logf(u1));
-  float sn, cs;
-  sincospif(2.0f * u2, &sn, &cs);
-  return rad * ((lane & 1) ? sn : cs);
-}
 
 template <int NT>
 __device__ inline double block_sum(double v, double* sh) {
@@ -154,11 +133,9 @@ __global__ void __launch_bounds__(256) k_pack_rows(PackArgs p) {
 }
 
 // ------------------------------------------------------------------------------ heads
-// SAC head: z = [mu | l] -> a = tanh(mu + exp(clip(l)) eps) written into the action
-// columns of x, and the tanh-Gaussian log-density (overflow-free form of
-// log(1 - tanh^2 u) = 2 (ln 2 - u - softplus(-2u))). Optional cache for backward.
-// One thread per (row, action) element, so that loads and stores of consecutive
-// threads are contiguous; a block covers HEAD_ROWS rows and adds each row's
+// SAC head (sac_head_element) on a stored z, where the head product could not take it in
+// its epilogue. One thread per (row, action) element, so that loads and stores of
+// consecutive threads are contiguous; a block covers HEAD_ROWS rows and adds each row's
 // per-action terms in action order through LDS.
 constexpr int HEAD_ROWS = 64;
 template <typename T>
@@ -172,20 +149,7 @@ __global__ void __launch_bounds__(256) k_sac_head(SacHeadArgs h) {
     const int r = e / h.A, j = e - r * h.A;
     const int b = r0 + r;
     const float* z = h.z + (int64_t)b * h.ldz;
-    const float eps = normal_at(h.seed, (uint64_t)r0 * h.A + e, t, h.purpose);
-    const float mu = z[j], l = z[h.A + j];
-    const float lc = clamp_keep_nan(l, h.lmin, h.lmax);
-    const float sig = expf(lc);
-    const float u = mu + sig * eps;
-    const float a = tanhf(u);
-    static_cast<T*>(h.x)[(int64_t)b * h.ldx + h.xoff + j] = from_f<T>(a);
-    lterm[e] = -0.5f * eps * eps - lc - HALF_LN_2PI_F - 2.0f * (LN2F - u - softplusf(-2.0f * u));
-    if (h.th) {
-      const int64_t c = (int64_t)r0 * h.A + e;
-      h.th[c] = a;
-      h.se[c] = sig * eps;
-      h.lm[c] = (l >= h.lmin && l <= h.lmax) ? 1.0f : 0.0f;
-    }
+    lterm[e] = sac_head_element<T>(h, z[j], z[h.A + j], b, j, normal_at(h.seed, (uint64_t)b * h.A + j, t, h.purpose));
   }
   __syncthreads();
   if ((int)threadIdx.x < rows) {
