@@ -297,6 +297,31 @@ def test_teacher_forced_sac_fp32(w, rows, before):
     teacher_forced(w, rows, steps_before=before)
 
 
+# 2A = 80 actor outputs: wider than the head product's fused epilogue takes (at most 64
+# columns), so these run the SAC head as its own kernel.
+WIDE_ACT = RAGGED.replace(name="wide_action_sac", act_dim=40, target_entropy=-40.0)
+WIDE_ACT_BF16 = RAGGED_BF16.replace(name="wide_action_sac_bf16", act_dim=40, target_entropy=-40.0)
+
+
+@pytest.mark.parametrize("w,fused", [(RAGGED, True), (RAGGED_BF16, True), (WIDE_ACT, False), (WIDE_ACT_BF16, False)],
+                         ids=["ragged_fp32", "ragged_bf16", "wide_fp32", "wide_bf16"])
+def test_sac_head_paths(w, fused):
+    """The SAC head runs inside the actor's output product where 2A fits its tile and as its
+    own kernel otherwise (checked from the kernel records); both paths give the oracle's
+    gradients, moments and losses on a teacher-forced step."""
+    log("SAC head path %s" % w.name)
+    g = make_gpu(w)
+    g.buffer_push(*synth.workload_rows(w, 0, 5000, 0))
+    g.profile_enable(True, 100)
+    g.update(1)
+    names = {s["name"] for s in g.profile_read()}
+    g.close()
+    assert ("sac_head" not in names) == fused, names
+    bf16 = w.prec == "bf16"
+    teacher_forced(w, 5000, steps_before=1, tol_grad=1e-3 if bf16 else FP32_TOL,
+                   tol_loss=BF16_LOSS_TOL if bf16 else FP32_TOL)
+
+
 def test_teacher_forced_td3_fp32():
     log("teacher-forced ragged_td3")
     teacher_forced(RAGGED_TD3, 5000, steps_before=1, n_steps=2)
