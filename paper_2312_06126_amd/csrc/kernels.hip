@@ -285,12 +285,13 @@ __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
   if (rs < rpi) {
     const uint4 w4 = *reinterpret_cast<const uint4*>(w + k);
     const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
-    for (int r = rs; r < HB_ROWS; r += rpi) {
-      const int b = r0 + r;
-      if (b >= rows) break;
+    const bf16_t* __restrict__ H = static_cast<const bf16_t*>(a.H);
+    bf16_t* __restrict__ dH = static_cast<bf16_t*>(a.dH);
+    // One row of the thread: the output-layer weight-gradient terms (rows in order), then
+    // dz and its column sums.
+    auto row = [&](int r, int b, const uint4& h4) {
       const float dq = dq_row[r];
       if (a.wpart) {
-        const uint4 h4 = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(a.H) + (int64_t)b * a.ld + k);
         const uint32_t hh[4] = {h4.x, h4.y, h4.z, h4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -309,7 +310,20 @@ __global__ void __launch_bounds__(256) k_head_bwd_bits(HeadBwdArgs a) {
         cs[2 * e + 1] += bf2f(h1);
         o[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
       }
-      *reinterpret_cast<uint4*>(static_cast<bf16_t*>(a.dH) + (int64_t)b * a.ld + k) = make_uint4(o[0], o[1], o[2], o[3]);
+      *reinterpret_cast<uint4*>(dH + (int64_t)b * a.ld + k) = make_uint4(o[0], o[1], o[2], o[3]);
+    };
+    // Two rows per pass, both rows' loads issued before either row's store.
+    for (int r = rs; r < HB_ROWS; r += 2 * rpi) {
+      const int b = r0 + r, r1 = r + rpi, b1 = b + rpi;
+      if (b >= rows) break;
+      const bool two = r1 < HB_ROWS && b1 < rows;
+      uint4 h0 = make_uint4(0u, 0u, 0u, 0u), h1 = h0;
+      if (a.wpart) {
+        h0 = *reinterpret_cast<const uint4*>(H + (int64_t)b * a.ld + k);
+        if (two) h1 = *reinterpret_cast<const uint4*>(H + (int64_t)b1 * a.ld + k);
+      }
+      row(r, b, h0);
+      if (two) row(r1, b1, h1);
     }
   }
   if (!a.colpart) return;
