@@ -99,9 +99,11 @@ struct spz_ctx {
   // bf16 contexts: transposed images of the online weights the input-gradient products
   // read (layer l >= 1 of each net, the critics' output layers aside), at the same
   // arena offsets as Pb: WT + L.w holds W^T [in_p, out_p], so that those products read
-  // both operands k-contiguous (the large-tile kernel needs it). Refreshed whenever P
-  // changes. float32 contexts read W itself: there the per-step transpose costs about
-  // what the k-contiguous reads save.
+  // both operands k-contiguous (the large-tile kernel needs it). For a critic's first
+  // layer WT + L.w holds the transposed action block [Ap, out_p] (columns Ka .. Ka + Ap
+  // of W), the weight of the gradient to the action. Refreshed whenever P changes.
+  // float32 contexts read W itself: there the per-step transpose costs about what the
+  // k-contiguous reads save.
   void* WT = nullptr;
   TransposeJob* tjobs = nullptr;
   int n_tjobs = 0, t_tiles = 0;
@@ -606,10 +608,10 @@ struct DgradIn {
 
 // Input gradients through layer l of nets ni .. ni + nn - 1: out = (dz . W) masked by
 // mask > 0 (or by the mask bits), N columns of W from column col0 on (row stride ldw),
-// or, with `transposed`, the layer's transposed weight image, which both GEMM kernels
-// then read instead (bf16 contexts; float32 contexts have none and read W). Column sums
-// of the stored out go to bias_out: fused into the product's epilogue where the
-// large-tile kernel covers it, the partials reduced by the part's deferred reduction q.
+// or, with `transposed`, the transposed image of those columns (WT + L.w), which both
+// GEMM kernels then read instead (bf16 contexts; float32 contexts have none and read W).
+// Column sums of the stored out go to bias_out: fused into the product's epilogue where
+// the large-tile kernel covers it, the partials reduced by the part's deferred reduction q.
 hipError_t dgrad(spz_ctx* c, int ni, int nn, int l, const DgradIn* d, int col0, int64_t ldw, bool transposed, int N,
                  int64_t ldo, bool out_f32, int q, hipStream_t s) {
   const Lay& L = c->net[ni].L[l];
@@ -742,7 +744,7 @@ hipError_t critic_action_grad(spz_ctx* c, int ni, const float* dq, void* const* 
     cur ^= 1;
   }
   const DgradIn d0{c->a_dz[cur], nullptr, nullptr, da, nullptr, nullptr};
-  return dgrad(c, ni, 1, 0, &d0, c->Ka, c->Kc, false, c->Ap, c->Ap, true, 1, s);
+  return dgrad(c, ni, 1, 0, &d0, c->Ka, c->Kc, c->WT != nullptr, c->Ap, c->Ap, true, 1, s);
 }
 
 // The same for both critics, each restricted to the rows listed in its map (critic k:
@@ -777,7 +779,7 @@ hipError_t critic_action_grad_rows(spz_ctx* c, const float* const* dq, void* con
   // Each action gradient of the listed rows lands in da2 (free here) and then in da.
   for (int k = 0; k < 2; ++k) {
     const DgradIn d0{dzb[k][cur], nullptr, nullptr, c->da2, nullptr, c->rrows + k};
-    HK(dgrad(c, 1 + k, 1, 0, &d0, c->Ka, c->Kc, false, c->Ap, c->Ap, true, 1, s));
+    HK(dgrad(c, 1 + k, 1, 0, &d0, c->Ka, c->Kc, c->WT != nullptr, c->Ap, c->Ap, true, 1, s));
     RowScatterArgs sa{c->da2, da, c->Ap, c->Ap, c->rmap + (int64_t)k * c->Bp, c->rrows + k, c->Bp};
     HK(timed(c, "row_scatter", c->Bp, c->Ap, 0, 0.0, 0.0, s, [&] { return launch_row_scatter(sa, s); }));
   }
@@ -1081,6 +1083,12 @@ int setup(spz_ctx* c) {
         jobs.push_back(TransposeJob{L.w, L.w, L.in_p, L.out_p, L.out_p, L.in_p, tiles});
         tiles += transpose_tiles(L.out_p, L.in_p);
         c->t_elems += (double)L.out_p * L.in_p;
+      }
+      if (ni != 0) {   // a critic's first layer: the action block only, for the action gradient
+        const Lay& L = n.L[0];
+        jobs.push_back(TransposeJob{L.w + c->Ka, L.w, L.in_p, L.out_p, L.out_p, c->Ap, tiles});
+        tiles += transpose_tiles(L.out_p, c->Ap);
+        c->t_elems += (double)L.out_p * c->Ap;
       }
     }
     c->n_tjobs = (int)jobs.size();
