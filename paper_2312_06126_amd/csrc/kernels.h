@@ -44,7 +44,7 @@ struct HeadBwdArgs {
   // bit k % 32 of bits[(k / 32) * ldbits + b].
   const uint32_t* bits; int64_t ldbits;
   // With bits: when set, the column sums of the stored dH over each block of rows go
-  // to colpart[block, K] (head_bwd_blocks(rows) blocks; reduce with launch_colsum_final).
+  // to colpart[block, K] (head_bwd_blocks(rows) blocks; reduced by a deferred reduction).
   float* colpart;
   // With bits and without colpart: when map is set, row r < *m_dyn of dH is row
   // map[r] of the product (dq, bits read there), a zero row where map[r] < 0; rows
@@ -157,8 +157,7 @@ hipError_t launch_row_scatter(const RowScatterArgs& a, hipStream_t s);
 hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream_t s);
 int colsum_chunks(int rows);
 int head_bwd_blocks(int rows);
-hipError_t launch_colsum(bool bf16, const ColsumArgs& a, float* out, float* out_extra, hipStream_t s);
-// The first pass alone: a.part[chunks, N] (and a.part_extra[chunks]) for a deferred
+// Column-sum partials a.part[chunks, N] (and a.part_extra[chunks]) for a deferred
 // reduction (ReduceJob with colsum_groups()).
 hipError_t launch_colsum_partial(bool bf16, const ColsumArgs& a, hipStream_t s);
 int colsum_groups();
@@ -167,8 +166,7 @@ int colsum_groups();
 // part[z * zstride + r * ld + c], for r < rows, c < cols. A piece of vec (4 or 1)
 // output columns is summed by `groups` threads (a power of two): thread g takes
 // z = g, g + groups, ... in order, then the group sums are added in g order -- a
-// fixed order for a fixed job, the same as the split-K and column-sum reductions
-// that launch on their own. block0: first block of the job (set by the launch).
+// fixed order for a fixed job. block0: first block of the job (set by the launch).
 struct ReduceJob {
   const float* part; float* out; int64_t zstride, ld, ldo;
   int rows, cols, slices, groups, vec, block0;
@@ -177,8 +175,6 @@ constexpr int MAX_REDUCE_JOBS = 24;
 struct ReduceJobs { ReduceJob j[MAX_REDUCE_JOBS]; int n; };
 // All jobs in one launch (n <= MAX_REDUCE_JOBS).
 hipError_t launch_reduce_jobs(ReduceJobs& jobs, hipStream_t s);
-// out[n] = sum over c in order of part[c, n] (c < chunks), n < N.
-hipError_t launch_colsum_final(const float* part, int chunks, int N, float* out, hipStream_t s);
 hipError_t launch_adam(const AdamArgs& a, hipStream_t s);
 hipError_t launch_finish(const FinishArgs& f, hipStream_t s);
 hipError_t launch_to_bf16(const float* src, bf16_t* dst, int64_t n, hipStream_t s);

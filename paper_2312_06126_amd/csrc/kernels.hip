@@ -616,48 +616,11 @@ __global__ void __launch_bounds__(256) k_colsum(ColsumArgs a) {
   }
 }
 
-// Second pass: out[n] = sum over chunks c of part[c, n]. A block owns CSF_COLS
-// columns (CSF_CV float4 lanes) and splits the chunks over CSF_G groups g (c = g,
-// g + CSF_G, ...); the group sums are then added in g order through LDS: a fixed order
-// for a fixed chunk count. Narrow blocks and many groups keep each thread's chain of
-// loads short (the partials are few and read once). The extra scalar (when present)
-// is summed the same way by block 0.
-constexpr int CSF_CV = 4, CSF_G = 256 / CSF_CV, CSF_COLS = 4 * CSF_CV;
-__global__ void __launch_bounds__(256) k_colsum_final(const float* __restrict__ part, const float* __restrict__ part_extra,
-                                                      int chunks, int N, int extra, float* __restrict__ out,
-                                                      float* __restrict__ out_extra) {
-  __shared__ float4 sh[256];
-  __shared__ float she[CSF_G];
-  const int cv = threadIdx.x % CSF_CV, grp = threadIdx.x / CSF_CV;
-  const int col = blockIdx.x * CSF_COLS + cv * 4;
-  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-  float ex = 0.0f;
-  if (col < N) {
-#pragma unroll 4
-    for (int c = grp; c < chunks; c += CSF_G) {
-      const float4 v = *reinterpret_cast<const float4*>(part + (int64_t)c * N + col);
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-    }
-  }
-  if (extra && blockIdx.x == 0 && cv == 0)
-    for (int c = grp; c < chunks; c += CSF_G) ex += part_extra[c];
-  sh[threadIdx.x] = acc;
-  if (cv == 0) she[grp] = ex;
-  __syncthreads();
-  if (grp == 0 && col < N) {
-    float4 t = sh[cv];
-    for (int g = 1; g < CSF_G; ++g) {
-      const float4 v = sh[g * CSF_CV + cv];
-      t.x += v.x; t.y += v.y; t.z += v.z; t.w += v.w;
-    }
-    *reinterpret_cast<float4*>(out + col) = t;
-  }
-  if (extra && blockIdx.x == 0 && threadIdx.x == 0) {
-    float t = 0.0f;
-    for (int g = 0; g < CSF_G; ++g) t += she[g];
-    *out_extra = t;
-  }
-}
+// Column-sum partials are reduced by the deferred reduction (k_reduce_jobs) with
+// CSF_G groups: group g adds chunks g, g + CSF_G, ... in order and the group sums are
+// added in g order, a fixed order for a fixed chunk count (many groups keep each
+// thread's chain of loads short: the partials are few and read once).
+constexpr int CSF_G = 64;
 
 // Deferred reductions (ReduceJob): a block belongs to the last job whose block0 it has
 // reached; 256 / groups pieces per block, `groups` threads per piece.
@@ -939,16 +902,6 @@ hipError_t launch_actor_head_bwd(bool bf16, const ActorHeadBwdArgs& h, hipStream
   return hipGetLastError();
 }
 int colsum_chunks(int rows) { return (int)blocks(rows, COLSUM_CHUNK); }
-hipError_t launch_colsum(bool bf16, const ColsumArgs& a, float* out, float* out_extra, hipStream_t s) {
-  const int vec = bf16 ? 8 : 4;
-  if (a.N % vec || a.ld % vec || a.N % 4) return hipErrorInvalidValue;
-  const int nvec = a.N / vec, ct = nvec < 32 ? nvec : 32;
-  const int chunks = (int)blocks(a.rows, a.chunk);
-  dim3 grid(blocks(nvec, ct), chunks);
-  SPZ_LAUNCH_T(bf16, k_colsum, grid, 256, s, a);
-  k_colsum_final<<<blocks(a.N, CSF_COLS), 256, 0, s>>>(a.part, a.part_extra, chunks, a.N, a.extra, out, out_extra);
-  return hipGetLastError();
-}
 hipError_t launch_colsum_partial(bool bf16, const ColsumArgs& a, hipStream_t s) {
   const int vec = bf16 ? 8 : 4;
   if (a.N % vec || a.ld % vec || a.N % 4) return hipErrorInvalidValue;
@@ -975,11 +928,6 @@ hipError_t launch_reduce_jobs(ReduceJobs& J, hipStream_t s) {
   }
   if (nb == 0) return hipSuccess;
   k_reduce_jobs<<<nb, 256, 0, s>>>(J);
-  return hipGetLastError();
-}
-hipError_t launch_colsum_final(const float* part, int chunks, int N, float* out, hipStream_t s) {
-  if (N % 4) return hipErrorInvalidValue;
-  k_colsum_final<<<blocks(N, CSF_COLS), 256, 0, s>>>(part, nullptr, chunks, N, 0, out, nullptr);
   return hipGetLastError();
 }
 hipError_t launch_adam(const AdamArgs& a, hipStream_t s) {
