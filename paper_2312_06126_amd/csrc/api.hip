@@ -392,7 +392,7 @@ hipError_t red_flush(spz_ctx* c, int q, hipStream_t s) {
   return hipSuccess;
 }
 
-hipError_t red_job(spz_ctx* c, int q, const ReduceJob& j, hipStream_t s) {
+hipError_t red_job(spz_ctx* c, int q, const ReduceJob& j) {
   spz_ctx::RedQueue& r = c->red[q];
   if (r.jobs.n == MAX_REDUCE_JOBS) return hipErrorInvalidValue;   // callers flush before allocating
   r.jobs.j[r.jobs.n++] = j;
@@ -406,21 +406,21 @@ hipError_t red_room(spz_ctx* c, int q, int jobs, hipStream_t s) {
 }
 
 // Reduction of column-sum partials part[slices, N] into out[N] (and of the extra
-// scalars part_extra[slices] into *out_extra), in the order of the standalone pass.
+// scalars part_extra[slices] into *out_extra), in the fixed group order of colsum_groups().
 hipError_t red_colsum(spz_ctx* c, int q, const float* part, int slices, int N, float* out, const float* part_extra,
                       float* out_extra, hipStream_t s) {
-  HK(red_job(c, q, ReduceJob{part, out, N, 0, 0, 1, N, slices, colsum_groups(), 4, 0}, s));
+  HK(red_job(c, q, ReduceJob{part, out, N, 0, 0, 1, N, slices, colsum_groups(), 4, 0}));
   if (!part_extra) return hipSuccess;
-  return red_job(c, q, ReduceJob{part_extra, out_extra, 1, 0, 0, 1, 1, slices, colsum_groups(), 1, 0}, s);
+  return red_job(c, q, ReduceJob{part_extra, out_extra, 1, 0, 0, 1, 1, slices, colsum_groups(), 1, 0});
 }
 
-int colsum_rows(const spz_ctx* c, int Bp) {
+int colsum_rows(int Bp) {
   return std::max({colsum_chunks(Bp), Bp / 256, head_bwd_blocks(Bp)});
 }
 
 // Workspace floats a part's deferred reductions may need at padded batch Bp.
 int64_t red_need(const spz_ctx* c, int q, int Bp) {
-  const int chunks = colsum_rows(c, Bp);
+  const int chunks = colsum_rows(Bp);
   int64_t n = 0;
   for (int ni = (q == 0 ? 1 : 0); ni <= (q == 0 ? 2 : 0); ++ni)
     for (const Lay& L : c->net[ni].L) {
@@ -577,8 +577,8 @@ hipError_t wgrad(spz_ctx* c, int q, int nn, const WgradIn* w, bool bias, hipStre
   HK(gemm2(c, "gemm_wgrad", GEMM_WGRAD, g[0], nn > 1 ? &g[1] : nullptr, true, s));
   for (int k = 0; k < nn; ++k)
     HK(red_job(c, q, ReduceJob{part[k], c->G + c->net[w[k].ni].L[w[k].l].w, (int64_t)g[k].M * g[k].ldc, g[k].ldc,
-                               g[k].N, g[k].M, g[k].N, g[k].splits, splitk_groups(g[k].M, g[k].N, g[k].splits), 4, 0},
-                       s));
+                               g[k].N, g[k].M, g[k].N, g[k].splits, splitk_groups(g[k].M, g[k].N, g[k].splits), 4,
+                               0}));
   if (!bias) return hipSuccess;
   const int chunks = colsum_chunks(c->Bp);
   for (int k = 0; k < nn; ++k) {
