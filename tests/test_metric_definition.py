@@ -35,3 +35,18 @@ def test_frame_rate_is_frequency_times_batch():
 
 def test_throughput_scales_with_steps_and_time():
     assert bench.frames_per_second(131072, 500, 2.0) == 131072 * 250.0
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The benchmark runs on one GPU: --gpus above 1 (or a multi-rank launch) exits with
+    status 2 and says so, before touching a GPU."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr, (r.returncode, r.stderr)
+    env = dict(os.environ, WORLD_SIZE="2")
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py")], capture_output=True, text=True,
+                       timeout=120, env=env)
+    assert r.returncode == 2 and "single process" in r.stderr, (r.returncode, r.stderr)
